@@ -1,0 +1,242 @@
+"""Outer-step benchmark: one JSON line on stdout.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+per-step edge masks and their Metropolis weights on the host, then the fused
+kernel (outer gradient, Mix2, Mix1, Nesterov, consensus distance of every
+intermediate) and the consensus finalize kernel.  Inputs are resident in HBM
+before the timed region starts.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+
+The default workload is 8 workers x 1.1e9 parameters with bf16 parameter
+storage, float32 momentum and float32 arithmetic (global-mean Mix1, ring Mix2
+with every edge dropped with probability 0.1 per step and Metropolis
+reweighting).  Only one GPU is used.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+METRIC = "outer-step HBM GB/s and % of MI355X HBM peak; params·workers/sec"
+
+
+def kernel_source_hash():
+    """Hash of the HIP sources; traffic counters are valid only for this hash."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_22768_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload, bytes_per_launch):
+    """HBM traffic per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_fused_step_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return {"fetch_bytes": t["fetch_bytes_per_launch"], "write_bytes": t["write_bytes_per_launch"],
+            "total_bytes": t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"],
+            "ratio_to_algorithmic": (t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"]) / bytes_per_launch}
+
+
+def host_cpu():
+    model = platform.processor() or ""
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return model, os.cpu_count()
+
+
+def host_slice(tp, tl, v, dtype, p_slice):
+    """Host copies of the first p_slice parameters of every worker row."""
+    import numpy as np
+    import torch
+
+    if dtype == "bf16":
+        h_tp = tp[:, :p_slice].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        h_tl = tl[:, :p_slice].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    else:
+        h_tp = tp[:, :p_slice].contiguous().cpu().numpy()
+        h_tl = tl[:, :p_slice].contiguous().cpu().numpy()
+    return h_tp, h_tl, v[:, :p_slice].contiguous().cpu().numpy()
+
+
+def cpu_baseline(sl, w, topo1, topo2):
+    """The CPU oracle, single-threaded, on the first parameters of every worker
+    row of the GPU's own first-step inputs (every parameter index is
+    independent given W, so the work scales exactly with the slice)."""
+    import oracle
+    from synth import configs
+
+    M = w["M"]
+    h_tp, h_tl, h_v = sl
+    p_slice = h_tp.shape[1]
+    m1, m2 = oracle.Mix.from_topology(topo1), oracle.Mix.from_topology(topo2)
+    t0 = time.perf_counter()
+    oracle.outer_step(h_tp, h_tl, h_v, m1, m2, lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=w["dtype"])
+    dt = time.perf_counter() - t0
+    gbs = configs.min_bytes_per_step(M, p_slice, w["dtype"]) / dt / 1e9
+    model, ncpu = host_cpu()
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {p_slice} of {w['P']} parameters x {M} workers of the GPU's first-step inputs "
+                      f"and topology, {dt:.2f} s single-threaded; GB/s from the same algorithmic byte count",
+            "params_workers_per_s": round(M * p_slice / dt, 1), "host_cpu": model, "host_nproc": ncpu}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="m8_p1100m_bf16")
+    ap.add_argument("--cpu-slice", type=int, default=1 << 25, help="parameters per worker in the CPU sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(each parameter index is independent, so a P-sharded run needs no exchange); "
+              "use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_22768_amd as fgd
+    from synth import configs, tensors
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    w = configs.WORKLOADS[args.workload]
+    M, P, dtype = w["M"], w["P"], w["dtype"]
+    ld = -(-P // 8) * 8
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {args.workload} inputs", file=sys.stderr, flush=True)
+    tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
+                                     mom_std=w["mom_std"], seed=w["seed"], device=dev)
+    sl = None if args.no_cpu_baseline else host_slice(tp, tl, v, dtype, min(args.cpu_slice, P))
+    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0)
+    topo1 = configs.topology(w["mix1"], M, w["k1"], w["seed"])
+    eng.set_topology_dict("mix1", topo1)
+    per_step_masks = w["mix2"][1] == "metropolis" and w["mix2"][0] == "ring"
+
+    def topo2_for(step):
+        return configs.topology(w["mix2"], M, w["k2"], w["seed"], step=step)
+
+    topo2 = topo2_for(0)
+    eng.set_topology_dict("mix2", topo2)
+    cd = torch.zeros((eng.num_cd_rows(), M), dtype=torch.float64, device=dev)
+    # Mask tables for every step are drawn before timing (input generation);
+    # the engine still builds the weights and uploads them inside each step.
+    step_topos = [topo2_for(s) for s in range(args.warmup + args.steps)] if per_step_masks else None
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        if step_topos is not None:
+            eng.set_topology_dict("mix2", step_topos[i])
+        eng.outer_step(tp, tl, v, cd, stream)
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    eng.enable_timing(True)
+    print("[bench] timed steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernel_ms, n_kernels = eng.read_timing()
+    eng.enable_timing(False)
+
+    bytes_step = eng.min_bytes_per_step()
+    ms_step = elapsed * 1e3 / args.steps
+    gbs = bytes_step * args.steps / elapsed / 1e9
+    kernel_avg_ms = kernel_ms / max(n_kernels, 1)
+    achieved = bytes_step / (kernel_avg_ms * 1e-3) / 1e9
+    cd_host = cd.cpu().numpy()
+
+    # Plain copy reference (practical streaming ceiling), timed with torch events.
+    copy_gbs = None
+    if args.copy_gb > 0:
+        n = int(args.copy_gb * 1e9) // 16 * 16
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty(n, dtype=torch.uint8, device=dev)
+        fgd.fgd_stream_copy(b, a, n)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            fgd.fgd_stream_copy(b, a, n)
+        e1.record()
+        torch.cuda.synchronize()
+        copy_gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        del a, b
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
+        "params_workers_per_s": round(M * P * args.steps / elapsed, 1),
+        "config": {"workload": args.workload, "workers": M, "params_per_worker": P, "row_stride": ld,
+                   "storage": "bf16 parameters, f32 momentum" if dtype == "bf16" else "f32 parameters and momentum",
+                   "mix1": f"{w['mix1']} x{w['k1']}", "mix2": f"{w['mix2']} x{w['k2']}",
+                   "outer_lr": configs.OUTER_LR, "momentum": configs.MOMENTUM,
+                   "consensus": "fused, every intermediate", "algorithmic_bytes_per_step": bytes_step,
+                   "parallelism": "single GPU, workers simulated as rows"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": read_traffic(args.workload, bytes_step),
+                     "kernel": "fused outer-step kernel", "kernel_avg_ms": round(kernel_avg_ms, 4),
+                     "timed_launches": n_kernels, "bytes_per_launch": bytes_step},
+        "copy_reference_gbs": None if copy_gbs is None else round(copy_gbs, 1),
+        "consensus_last_step": {"rows": int(cd_host.shape[0]),
+                                "cd_sq_mean_per_row": [float(x) for x in cd_host.mean(axis=1)]},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(sl, w, topo1, topo2)
+    else:
+        out["cpu_baseline"] = None
+    eng.close()
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,194 @@
+/*
+ * fgd.h -- C ABI of the fused Factored Gossip DiLoCo outer-step engine for
+ * AMD MI355X (gfx950).
+ *
+ * The engine runs the outer synchronization step of Factored Gossip DiLoCo
+ * over M simulated worker replicas that live in one GPU's memory
+ * (Sec. 4.1, factored outer step; Appendix A, Algorithm 1, outer-step part):
+ *
+ *   g0_m    = theta_prev_m - theta_local_m        outer gradient; the paper's
+ *                                                 Delta = y_H - y_0 enters the
+ *                                                 outer optimizer negated
+ *   ghat    = Mix2(g0)                            K2 gossip rounds (blocking mix)
+ *   x       = Mix1(theta_prev)                    K1 rounds or the global mean
+ *                                                 (non-blocking mix)
+ *   v'_m    = mu v_m + ghat_m                     Nesterov, two-line form
+ *   theta'_m = x_m - lr (ghat_m + mu v'_m)        (Appendix B)
+ *
+ * A Mix round maps row m to sum_n w_{m,n} u_n (Sec. 3, gossip mixing
+ * operator), with W given as CSR: row m lists the workers it pulls from.
+ * The step optionally reports, per worker, S_m(u) = sum_p (u_m,p - mean_n
+ * u_n,p)^2 for every intermediate u (Sec. 4.4 L2 consensus distance; the
+ * mean of sqrt(S_m) is the Sec. 4.4 form and the mean of S_m the
+ * Appendix D.1 form).
+ *
+ * Conventions for every call:
+ *  - Every call returns an fgd_status.  Nothing throws or aborts across the
+ *    ABI.  On failure nothing is launched and fgd_last_error() (per thread)
+ *    holds a readable reason.
+ *  - Device arrays are worker-major [M][ld] with ld >= P elements; element p
+ *    of worker m is at index m * ld + p.  Each row must start on a 16-byte
+ *    boundary (base pointer 16-byte aligned and ld * element size a multiple
+ *    of 16).
+ *  - The caller owns every device buffer; the engine only borrows them for
+ *    the work it enqueues, so they must stay alive until `stream` has passed
+ *    that work.  Host arrays handed to the engine are copied before return.
+ *  - `stream` is a hipStream_t (NULL = the device's null stream).  Compute
+ *    calls are asynchronous with respect to the host.
+ *  - An engine is not thread-safe; use one engine per host thread.
+ */
+#ifndef FGD_H
+#define FGD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct fgd_engine fgd_engine; /* opaque */
+
+typedef enum {
+    FGD_OK = 0,
+    FGD_ERR_INVALID_ARG = 1,   /* bad pointer, size, alignment, enum or alias */
+    FGD_ERR_TOPOLOGY = 2,      /* malformed CSR or masks, or W not doubly stochastic */
+    FGD_ERR_UNSUPPORTED = 3,   /* valid request this build does not implement */
+    FGD_ERR_OUT_OF_MEMORY = 4, /* host or device allocation failed */
+    FGD_ERR_HIP = 5,           /* a HIP runtime call or launch failed */
+    FGD_ERR_STATE = 6          /* call not allowed in the engine's current state */
+} fgd_status;
+
+typedef enum { FGD_F32 = 0, FGD_BF16 = 1 } fgd_dtype;
+
+/* Which Mix slot a topology call sets. */
+typedef enum { FGD_MIX1 = 1, FGD_MIX2 = 2 } fgd_mix;
+
+/* How a Mix slot mixes. */
+typedef enum {
+    FGD_W_IDENTITY = 0,    /* no mixing */
+    FGD_W_GLOBAL_MEAN = 1, /* exact mean over all workers, W = 11^T / M (Sec. 3) */
+    FGD_W_CSR = 2          /* num_rounds rounds of a sparse W given in CSR */
+} fgd_wkind;
+
+/* How the weights of a CSR round are obtained from the structure, the given
+ * weights and that round's edge mask.  A dropped link mixes less rather than
+ * aborting the round (Sec. 1 and Sec. 5.2 describe this behaviour of gossip
+ * under transient failures; the reweighting rules are this engine's). */
+typedef enum {
+    FGD_REWEIGHT_NONE = 0,       /* given weights; masks must be NULL or all ones */
+    FGD_REWEIGHT_METROPOLIS = 1, /* live graph of the round: d_i = live neighbours of i,
+                                    w_ij = 1/(1+max(d_i,d_j)), w_ii = 1 - sum_j w_ij
+                                    (ascending j), computed in double, rounded to
+                                    float; given weights are ignored (may be NULL) */
+    FGD_REWEIGHT_SELF = 2        /* given weights; a dropped entry's weight is added to
+                                    its row's diagonal (double, ascending j, rounded) */
+} fgd_reweight;
+
+#define FGD_MAX_WORKERS 64 /* largest M this build runs */
+#define FGD_MAX_ROUNDS 8   /* largest number of rounds per Mix slot */
+
+typedef struct {
+    uint32_t struct_size; /* sizeof(fgd_config), for forward compatibility */
+    int32_t num_workers;  /* M, 1..FGD_MAX_WORKERS */
+    int64_t num_params;   /* P >= 0 parameters per worker */
+    int64_t ld;           /* row stride in elements, >= P, ld * elem size % 16 == 0 */
+    int32_t param_dtype;  /* fgd_dtype of theta_prev and theta_local (momentum is
+                             always float32; arithmetic is float32) */
+    float outer_lr;       /* lr (gamma), e.g. 0.7 (Sec. 5, Appendix A) */
+    float momentum;       /* mu, e.g. 0.9 */
+    int32_t device;       /* HIP device ordinal; -1 creates a host-only engine that
+                             validates topologies but cannot run compute calls */
+} fgd_config;
+
+/* Creates an engine.  Allocates the device-side topology slots and the
+ * consensus-distance scratch on cfg->device (never later, inside a step).
+ * Both Mix slots start unset. */
+fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out);
+
+/* Frees the engine and its device memory after synchronizing its device.
+ * NULL is accepted. */
+fgd_status fgd_destroy(fgd_engine *e);
+
+/* Sets the topology of one Mix slot.
+ *   kind        fgd_wkind.  IDENTITY and GLOBAL_MEAN ignore every array
+ *               argument and num_rounds.
+ *   row_ptr     host int32[M+1]: row_ptr[0] = 0, non-decreasing, row_ptr[M] = nnz
+ *   col_idx     host int32[nnz]: strictly ascending within each row, in [0, M),
+ *               with the diagonal entry present in every row
+ *   weights     host float[nnz] >= 0, finite; NULL only with METROPOLIS
+ *   num_rounds  K in [0, FGD_MAX_ROUNDS]; 0 makes the slot the identity
+ *   edge_masks  host uint8[K][nnz] with values 0/1, NULL = every entry live.
+ *               Diagonal entries must be live.  On a structurally symmetric
+ *               graph, entry (i,j) and entry (j,i) must carry the same mask.
+ *   reweight    fgd_reweight
+ * Per round the engine forms the effective weights, checks that every row
+ * and every column of the effective W sums to 1 within 1e-6 (else
+ * FGD_ERR_TOPOLOGY; METROPOLIS also needs a structurally symmetric graph),
+ * and keeps them.  They are uploaded, stream-ordered, by the next
+ * fgd_outer_step.  Host arrays are copied before return. */
+fgd_status fgd_set_topology(fgd_engine *e, int32_t which, int32_t kind, const int32_t *row_ptr,
+                            const int32_t *col_idx, const float *weights, int32_t num_rounds,
+                            const uint8_t *edge_masks, int32_t reweight);
+
+/* Number of consensus-distance rows fgd_outer_step writes:
+ * (K2 + 1) + (K1 + 1) + 1, where a GLOBAL_MEAN slot counts as one round and
+ * IDENTITY as zero.  Needs both slots set. */
+fgd_status fgd_num_cd_rows(const fgd_engine *e, int32_t *n_rows);
+
+/* One fused outer step, enqueued on `stream`.
+ *   theta_prev   device [M][ld] param_dtype, read and overwritten with theta'
+ *   theta_local  device [M][ld] param_dtype, read only; must not overlap
+ *                theta_prev or momentum
+ *   momentum     device [M][ld] float32, read and overwritten with v'
+ *   cd_out       device double[n_rows][M] or NULL (no consensus distances).
+ *                Rows in order: g^0..g^K2 (Mix2 input and round outputs),
+ *                x^0..x^K1 (Mix1 input and round outputs), then the stored
+ *                theta'.  Entry [r][m] is S_m of that intermediate.
+ * Arithmetic is float32 (bf16 storage is widened exactly; theta' is rounded
+ * to bf16 to nearest even); consensus sums accumulate in double.  Both Mix
+ * slots must be set (else FGD_ERR_STATE). */
+fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
+                          double *cd_out, void *stream);
+
+/* S_m = sum_p (x_m,p - mean_n x_n,p)^2 of a device [M][ld] array of the
+ * given dtype, written to device double out[M], enqueued on `stream`
+ * (Sec. 4.4; Appendix D.1). */
+fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, double *out, void *stream);
+
+/* Effective float weights of one round of one slot, in the slot's CSR entry
+ * order (dropped entries read 0).  out: host float[nnz]. */
+fgd_status fgd_get_effective_weights(const fgd_engine *e, int32_t which, int32_t round, float *out);
+
+/* The same computation without an engine, for one round:
+ * mask = host uint8[nnz] or NULL.  Pure host code. */
+fgd_status fgd_effective_weights(int32_t num_workers, const int32_t *row_ptr, const int32_t *col_idx,
+                                 const float *weights, const uint8_t *mask, int32_t reweight, float *out);
+
+/* Algorithmic minimum HBM traffic of one step:
+ * M * P * (3 * elem_size(param_dtype) + 2 * 4) bytes (read theta_prev,
+ * theta_local, momentum; write theta_prev, momentum). */
+fgd_status fgd_min_bytes_per_step(const fgd_engine *e, int64_t *bytes);
+
+/* Kernel timing.  While enabled, every fgd_outer_step brackets its fused
+ * kernel with HIP events on its stream.  fgd_read_timing waits for the
+ * recorded events and returns the summed kernel milliseconds and the number
+ * of timed kernels since the last reset (enabling resets). */
+fgd_status fgd_enable_timing(fgd_engine *e, int32_t enable);
+fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count);
+
+/* Plain device copy of `bytes` bytes (16-byte aligned pointers, bytes % 16 ==
+ * 0) on `stream`: the streaming reference against which the step's
+ * bandwidth and traffic counters are read. */
+fgd_status fgd_stream_copy(void *dst, const void *src, int64_t bytes, void *stream);
+
+/* Static name of a status; never NULL. */
+const char *fgd_status_string(int32_t status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *fgd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FGD_H */

@@ -1,0 +1,276 @@
+"""Python binding of libfgd (include/fgd.h): the fused Factored Gossip DiLoCo
+outer step for AMD MI355X.
+
+Every function here has the name of the C entry point it wraps and only
+marshals arguments: numpy arrays become host pointers, torch tensors become
+device pointers, and the current torch stream becomes the hipStream_t.  All
+arithmetic of the step runs in the library's HIP kernels.  If libfgd.so has
+not been built, importing this package raises ImportError.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfgd.so")
+
+FGD_OK, FGD_ERR_INVALID_ARG, FGD_ERR_TOPOLOGY, FGD_ERR_UNSUPPORTED = 0, 1, 2, 3
+FGD_ERR_OUT_OF_MEMORY, FGD_ERR_HIP, FGD_ERR_STATE = 4, 5, 6
+FGD_F32, FGD_BF16 = 0, 1
+FGD_MIX1, FGD_MIX2 = 1, 2
+FGD_W_IDENTITY, FGD_W_GLOBAL_MEAN, FGD_W_CSR = 0, 1, 2
+FGD_REWEIGHT_NONE, FGD_REWEIGHT_METROPOLIS, FGD_REWEIGHT_SELF = 0, 1, 2
+FGD_MAX_WORKERS, FGD_MAX_ROUNDS = 64, 8
+
+DTYPES = {"f32": FGD_F32, "bf16": FGD_BF16}
+KINDS = {"identity": FGD_W_IDENTITY, "global": FGD_W_GLOBAL_MEAN, "csr": FGD_W_CSR}
+REWEIGHTS = {"none": FGD_REWEIGHT_NONE, "metropolis": FGD_REWEIGHT_METROPOLIS, "self": FGD_REWEIGHT_SELF}
+MIXES = {"mix1": FGD_MIX1, "mix2": FGD_MIX2, 1: FGD_MIX1, 2: FGD_MIX2}
+
+
+class FgdError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: {fgd_status_string(status)}: {detail}")
+        self.status = status
+
+
+class fgd_config(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("num_workers", ctypes.c_int32),
+                ("num_params", ctypes.c_int64), ("ld", ctypes.c_int64), ("param_dtype", ctypes.c_int32),
+                ("outer_lr", ctypes.c_float), ("momentum", ctypes.c_float), ("device", ctypes.c_int32)]
+
+
+def _load():
+    # PyTorch supplies device memory and streams.  Its HIP runtime and the one
+    # libfgd.so links against share the soname libamdhip64.so.7; loading torch
+    # first makes the dynamic loader bind libfgd.so to torch's copy, so one
+    # runtime serves both and torch stream handles are valid here.
+    import torch  # noqa: F401
+
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_22768_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "fgd_create": (I32, [ctypes.POINTER(fgd_config), ctypes.POINTER(ctypes.c_void_p)]),
+        "fgd_destroy": (I32, [P]),
+        "fgd_set_topology": (I32, [P, I32, I32, P, P, P, I32, P, I32]),
+        "fgd_num_cd_rows": (I32, [P, ctypes.POINTER(I32)]),
+        "fgd_outer_step": (I32, [P, P, P, P, P, P]),
+        "fgd_consensus_distance": (I32, [P, P, I32, P, P]),
+        "fgd_get_effective_weights": (I32, [P, I32, I32, P]),
+        "fgd_effective_weights": (I32, [I32, P, P, P, P, I32, P]),
+        "fgd_min_bytes_per_step": (I32, [P, ctypes.POINTER(I64)]),
+        "fgd_enable_timing": (I32, [P, I32]),
+        "fgd_read_timing": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
+        "fgd_stream_copy": (I32, [P, P, I64, P]),
+        "fgd_status_string": (ctypes.c_char_p, [I32]),
+        "fgd_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype, f.argtypes = res, args
+    return L
+
+
+lib = _load()
+
+
+def fgd_status_string(status: int) -> str:
+    return lib.fgd_status_string(int(status)).decode()
+
+
+def fgd_last_error() -> str:
+    return lib.fgd_last_error().decode()
+
+
+def _check(status: int, where: str):
+    if status != FGD_OK:
+        raise FgdError(status, where, fgd_last_error())
+
+
+def _host(a, dtype):
+    """Contiguous numpy copy (kept alive by the caller) and its address, or (None, None)."""
+    if a is None:
+        return None, None
+    arr = np.ascontiguousarray(a, dtype=dtype)
+    return arr, arr.ctypes.data
+
+
+def _dev(t):
+    """Device address of a torch tensor (or an int address), None for None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# --------------------------------------------------------------- raw C ABI
+
+def fgd_create(num_workers, num_params, ld=None, param_dtype="f32", outer_lr=0.7, momentum=0.9, device=0):
+    cfg = fgd_config(ctypes.sizeof(fgd_config), int(num_workers), int(num_params),
+                     int(num_params if ld is None else ld), DTYPES.get(param_dtype, param_dtype),
+                     float(outer_lr), float(momentum), int(device))
+    h = ctypes.c_void_p()
+    _check(lib.fgd_create(ctypes.byref(cfg), ctypes.byref(h)), "fgd_create")
+    return h
+
+
+def fgd_destroy(h):
+    _check(lib.fgd_destroy(h), "fgd_destroy")
+
+
+def fgd_set_topology(h, which, kind, row_ptr=None, col_idx=None, weights=None, num_rounds=0, edge_masks=None,
+                     reweight="none"):
+    rp, prp = _host(row_ptr, np.int32)
+    ci, pci = _host(col_idx, np.int32)
+    w, pw = _host(weights, np.float32)
+    mk, pmk = _host(edge_masks, np.uint8)
+    _check(lib.fgd_set_topology(h, MIXES[which], KINDS.get(kind, kind), prp, pci, pw, int(num_rounds), pmk,
+                                REWEIGHTS.get(reweight, reweight)), "fgd_set_topology")
+
+
+def fgd_num_cd_rows(h) -> int:
+    n = ctypes.c_int32()
+    _check(lib.fgd_num_cd_rows(h, ctypes.byref(n)), "fgd_num_cd_rows")
+    return n.value
+
+
+def fgd_outer_step(h, theta_prev, theta_local, momentum, cd_out=None, stream=None):
+    _check(lib.fgd_outer_step(h, _dev(theta_prev), _dev(theta_local), _dev(momentum), _dev(cd_out),
+                              _stream(stream)), "fgd_outer_step")
+
+
+def fgd_consensus_distance(h, x, dtype, out, stream=None):
+    _check(lib.fgd_consensus_distance(h, _dev(x), DTYPES.get(dtype, dtype), _dev(out), _stream(stream)),
+           "fgd_consensus_distance")
+
+
+def fgd_get_effective_weights(h, which, rnd, nnz):
+    out = np.zeros(int(nnz), dtype=np.float32)
+    _check(lib.fgd_get_effective_weights(h, MIXES[which], int(rnd), out.ctypes.data), "fgd_get_effective_weights")
+    return out
+
+
+def fgd_effective_weights(num_workers, row_ptr, col_idx, weights=None, mask=None, reweight="none"):
+    rp, prp = _host(row_ptr, np.int32)
+    ci, pci = _host(col_idx, np.int32)
+    w, pw = _host(weights, np.float32)
+    mk, pmk = _host(mask, np.uint8)
+    out = np.zeros(0 if ci is None else ci.shape[0], dtype=np.float32)
+    _check(lib.fgd_effective_weights(int(num_workers), prp, pci, pw, pmk, REWEIGHTS.get(reweight, reweight),
+                                     out.ctypes.data if out.size else None), "fgd_effective_weights")
+    return out
+
+
+def fgd_min_bytes_per_step(h) -> int:
+    b = ctypes.c_int64()
+    _check(lib.fgd_min_bytes_per_step(h, ctypes.byref(b)), "fgd_min_bytes_per_step")
+    return b.value
+
+
+def fgd_enable_timing(h, enable=True):
+    _check(lib.fgd_enable_timing(h, 1 if enable else 0), "fgd_enable_timing")
+
+
+def fgd_read_timing(h):
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    _check(lib.fgd_read_timing(h, ctypes.byref(ms), ctypes.byref(n)), "fgd_read_timing")
+    return ms.value, n.value
+
+
+def fgd_stream_copy(dst, src, nbytes, stream=None):
+    _check(lib.fgd_stream_copy(_dev(dst), _dev(src), int(nbytes), _stream(stream)), "fgd_stream_copy")
+
+
+# ------------------------------------------------------ tensor-level wrapper
+
+class Engine:
+    """One engine over M worker rows of P parameters stored [M][ld].
+
+    Methods map one-to-one onto the C entry points; they only check that
+    tensors have the layout the engine was created for.
+    """
+
+    def __init__(self, num_workers, num_params, ld=None, param_dtype="f32", outer_lr=0.7, momentum=0.9, device=0):
+        self.M, self.P = int(num_workers), int(num_params)
+        self.ld = self.P if ld is None else int(ld)
+        self.dtype = param_dtype
+        self.device = device
+        self.handle = fgd_create(self.M, self.P, self.ld, param_dtype, outer_lr, momentum, device)
+        self._nnz = {1: 0, 2: 0}
+
+    def close(self):
+        if self.handle is not None:
+            fgd_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_topology(self, which, kind, row_ptr=None, col_idx=None, weights=None, rounds=0, masks=None,
+                     reweight="none"):
+        fgd_set_topology(self.handle, which, kind, row_ptr, col_idx, weights, rounds, masks, reweight)
+        self._nnz[MIXES[which]] = 0 if col_idx is None else len(col_idx)
+
+    def set_topology_dict(self, which, t):
+        """From the dict produced by synth.configs.topology."""
+        self.set_topology(which, t["kind"], t["row_ptr"], t["col_idx"], t["weights"], t["rounds"], t["masks"],
+                          t["reweight"])
+
+    def num_cd_rows(self):
+        return fgd_num_cd_rows(self.handle)
+
+    def _check_rows(self, t, name, dtype):
+        import torch
+
+        want = {"f32": torch.float32, "bf16": torch.bfloat16}[dtype]
+        if t.dtype != want:
+            raise TypeError(f"{name}: expected {want}, got {t.dtype}")
+        if t.dim() != 2 or t.shape[0] != self.M or t.shape[1] < self.P:
+            raise ValueError(f"{name}: expected shape [{self.M}, >= {self.P}], got {tuple(t.shape)}")
+        if t.stride(1) != 1 or (self.M > 1 and t.stride(0) != self.ld):
+            raise ValueError(f"{name}: rows must be contiguous with row stride ld = {self.ld}")
+
+    def outer_step(self, theta_prev, theta_local, momentum, cd_out=None, stream=None):
+        self._check_rows(theta_prev, "theta_prev", self.dtype)
+        self._check_rows(theta_local, "theta_local", self.dtype)
+        self._check_rows(momentum, "momentum", "f32")
+        fgd_outer_step(self.handle, theta_prev, theta_local, momentum, cd_out, stream)
+
+    def consensus_distance(self, x, out, stream=None, dtype=None):
+        dtype = dtype or self.dtype
+        self._check_rows(x, "x", dtype)
+        fgd_consensus_distance(self.handle, x, dtype, out, stream)
+
+    def effective_weights(self, which, rnd):
+        return fgd_get_effective_weights(self.handle, which, rnd, self._nnz[MIXES[which]])
+
+    def min_bytes_per_step(self):
+        return fgd_min_bytes_per_step(self.handle)
+
+    def enable_timing(self, on=True):
+        fgd_enable_timing(self.handle, on)
+
+    def read_timing(self):
+        return fgd_read_timing(self.handle)

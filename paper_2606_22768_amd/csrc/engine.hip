@@ -1,0 +1,500 @@
+// engine.hip -- the C ABI of include/fgd.h: engine state, argument checks,
+// stream-ordered topology upload and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/fgd.h"
+#include "kernels.hpp"
+#include "topology.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fgd_status fail(fgd_status st, const char *f, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, f);
+    std::vsnprintf(buf, sizeof buf, f, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+fgd_status hip_fail(hipError_t e, const char *what) {
+    return fail(FGD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+fgd_status from_topo(fgd::TopoStatus s, const std::string &err) {
+    if (s == fgd::TopoStatus::ok) return FGD_OK;
+    g_last_error = err;
+    return s == fgd::TopoStatus::invalid_arg ? FGD_ERR_INVALID_ARG : FGD_ERR_TOPOLOGY;
+}
+
+int elem_size(int32_t dtype) { return dtype == FGD_BF16 ? 2 : 4; }
+
+// Device copies of the packed topology tables.  A ring of slots, each with a
+// pinned host staging buffer and an event recorded after the last kernel
+// that read the slot, so a slot is refilled only once that kernel is done.
+constexpr int kTopoRing = 8;
+constexpr int kMaxBlocksPerCu = 8;
+constexpr int kTimingPool = 4096;
+
+}  // namespace
+
+struct fgd_engine {
+    fgd_config cfg{};
+    bool host_only = true;
+    fgd::MixTopology slot[2];   // [0] Mix1, [1] Mix2
+    bool slot_set[2] = {false, false};
+    uint64_t topo_version = 0;  // bumped by every fgd_set_topology
+
+    // Device side (absent for host-only engines).
+    int num_cus = 0;
+    size_t topo_capacity = 0;   // bytes per ring slot
+    void *d_topo[kTopoRing] = {};
+    void *h_topo[kTopoRing] = {};
+    hipEvent_t topo_done[kTopoRing] = {};
+    bool topo_pending[kTopoRing] = {};
+    int topo_next = 0;
+    int topo_current = -1;      // ring slot holding topo_version
+    uint64_t topo_current_version = ~0ull;
+    hipStream_t topo_stream = nullptr;
+    double *d_partials = nullptr;
+    size_t partials_capacity = 0;  // doubles
+
+    // Kernel timing.
+    bool timing = false;
+    std::vector<hipEvent_t> ev_start, ev_stop;
+    int64_t timed = 0;
+};
+
+namespace {
+
+fgd_status check_engine(const fgd_engine *e) {
+    if (!e) return fail(FGD_ERR_INVALID_ARG, "engine is NULL");
+    return FGD_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Byte range [lo, hi) spanned by an [M][ld] array of element size es, P used.
+void span(const void *p, int64_t M, int64_t ld, int64_t P, int es, uintptr_t &lo, uintptr_t &hi) {
+    lo = reinterpret_cast<uintptr_t>(p);
+    hi = lo + static_cast<uintptr_t>(((M - 1) * ld + P) * es);
+}
+
+bool overlap(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
+
+int32_t n_cd_rows(const fgd_engine *e) {
+    return e->slot[1].effective_rounds() + 1 + e->slot[0].effective_rounds() + 1 + 1;
+}
+
+fgd::MixDev mix_dev(const fgd::MixTopology &t, const void *tables) {
+    fgd::MixDev d{};
+    d.kind = t.kind;
+    d.rounds = t.rounds;
+    d.width = t.width;
+    d.table = static_cast<const int2 *>(tables);
+    return d;
+}
+
+bool lookup(int M, int32_t dtype, int k1, int k2, fgd::KernelSet &ks) {
+    return dtype == FGD_BF16 ? fgd::kernels_bf16(M, k1, k2, &ks) : fgd::kernels_f32(M, k1, k2, &ks);
+}
+
+// Makes sure the device holds the current topology for `stream` and returns
+// the ring slot.  Uploads (stream-ordered) when the topology changed or the
+// stream differs from the one that received the last upload.
+fgd_status ensure_topology(fgd_engine *e, hipStream_t stream, int &ring) {
+    if (e->topo_current >= 0 && e->topo_current_version == e->topo_version && e->topo_stream == stream) {
+        ring = e->topo_current;
+        return FGD_OK;
+    }
+    std::vector<int32_t> t1, t2;
+    e->slot[0].pack_tables(t1);
+    e->slot[1].pack_tables(t2);
+    const size_t b1 = t1.size() * sizeof(int32_t), b2 = t2.size() * sizeof(int32_t);
+    if (b1 + b2 > e->topo_capacity) return fail(FGD_ERR_UNSUPPORTED, "topology tables exceed the device slot");
+    const int r = e->topo_next;
+    e->topo_next = (e->topo_next + 1) % kTopoRing;
+    if (e->topo_pending[r]) {
+        hipError_t err = hipEventSynchronize(e->topo_done[r]);
+        if (err != hipSuccess) return hip_fail(err, "waiting for a topology slot");
+        e->topo_pending[r] = false;
+    }
+    char *h = static_cast<char *>(e->h_topo[r]);
+    if (b1) std::memcpy(h, t1.data(), b1);
+    if (b2) std::memcpy(h + b1, t2.data(), b2);
+    if (b1 + b2) {
+        hipError_t err = hipMemcpyAsync(e->d_topo[r], h, b1 + b2, hipMemcpyHostToDevice, stream);
+        if (err != hipSuccess) return hip_fail(err, "uploading the topology");
+    }
+    e->topo_current = r;
+    e->topo_current_version = e->topo_version;
+    e->topo_stream = stream;
+    ring = r;
+    return FGD_OK;
+}
+
+// Offsets of the Mix1 and Mix2 tables inside a ring slot.
+void table_ptrs(const fgd_engine *e, int ring, const void *&t1, const void *&t2) {
+    const size_t b1 = static_cast<size_t>(e->slot[0].kind == 2 ? e->slot[0].rounds * e->slot[0].width : 0) *
+                      e->cfg.num_workers * 2 * sizeof(int32_t);
+    t1 = e->d_topo[ring];
+    t2 = static_cast<const char *>(e->d_topo[ring]) + b1;
+}
+
+int64_t tiles_of(int64_t P, int v) {
+    const int64_t per = static_cast<int64_t>(fgd::kBlock) * v;
+    return (P + per - 1) / per;
+}
+
+fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntiles, int &grid) {
+    int per_cu = 0;
+    if (lds > 65536) {
+        hipError_t err = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (err != hipSuccess) return hip_fail(err, "raising the kernel's LDS limit");
+    }
+    hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, fgd::kBlock, lds);
+    if (err != hipSuccess) return hip_fail(err, "occupancy query");
+    if (per_cu < 1) return fail(FGD_ERR_UNSUPPORTED, "kernel does not fit on a compute unit (LDS %zu bytes)", lds);
+    per_cu = std::min(per_cu, kMaxBlocksPerCu);
+    const int64_t g = std::min<int64_t>(static_cast<int64_t>(per_cu) * e->num_cus, std::max<int64_t>(ntiles, 1));
+    grid = static_cast<int>(g);
+    return FGD_OK;
+}
+
+fgd_status launch(const void *kernel, int grid, size_t lds, hipStream_t stream, void *arg) {
+    void *args[] = {arg};
+    if (lds > 65536) {
+        hipError_t err = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (err != hipSuccess) return hip_fail(err, "raising the kernel's LDS limit");
+    }
+    hipError_t err = hipLaunchKernel(kernel, dim3(grid), dim3(fgd::kBlock), args, lds, stream);
+    if (err != hipSuccess) return hip_fail(err, "kernel launch");
+    return FGD_OK;
+}
+
+fgd_status launch_finalize(const double *partials, int nblocks, int n, double *out, hipStream_t stream) {
+    hipLaunchKernelGGL(fgd::finalize_kernel, dim3(n), dim3(256), 0, stream, partials, nblocks, n, out);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(err, "finalize launch");
+    return FGD_OK;
+}
+
+void release(fgd_engine *e) {
+    for (int r = 0; r < kTopoRing; ++r) {
+        if (e->d_topo[r]) (void)hipFree(e->d_topo[r]);
+        if (e->h_topo[r]) (void)hipHostFree(e->h_topo[r]);
+        if (e->topo_done[r]) (void)hipEventDestroy(e->topo_done[r]);
+    }
+    if (e->d_partials) (void)hipFree(e->d_partials);
+    for (auto ev : e->ev_start) (void)hipEventDestroy(ev);
+    for (auto ev : e->ev_stop) (void)hipEventDestroy(ev);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fgd_status_string(int32_t s) {
+    switch (s) {
+        case FGD_OK: return "FGD_OK";
+        case FGD_ERR_INVALID_ARG: return "FGD_ERR_INVALID_ARG";
+        case FGD_ERR_TOPOLOGY: return "FGD_ERR_TOPOLOGY";
+        case FGD_ERR_UNSUPPORTED: return "FGD_ERR_UNSUPPORTED";
+        case FGD_ERR_OUT_OF_MEMORY: return "FGD_ERR_OUT_OF_MEMORY";
+        case FGD_ERR_HIP: return "FGD_ERR_HIP";
+        case FGD_ERR_STATE: return "FGD_ERR_STATE";
+        default: return "FGD_UNKNOWN_STATUS";
+    }
+}
+
+const char *fgd_last_error(void) { return g_last_error.c_str(); }
+
+fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
+    g_last_error.clear();
+    if (!cfg || !out) return fail(FGD_ERR_INVALID_ARG, "cfg and out must not be NULL");
+    *out = nullptr;
+    if (cfg->struct_size != sizeof(fgd_config))
+        return fail(FGD_ERR_INVALID_ARG, "struct_size %u does not match sizeof(fgd_config) %zu", cfg->struct_size,
+                    sizeof(fgd_config));
+    if (cfg->num_workers < 1 || cfg->num_workers > FGD_MAX_WORKERS)
+        return fail(FGD_ERR_INVALID_ARG, "num_workers %d is outside [1, %d]", cfg->num_workers, FGD_MAX_WORKERS);
+    if (cfg->num_params < 0) return fail(FGD_ERR_INVALID_ARG, "num_params is negative");
+    if (cfg->param_dtype != FGD_F32 && cfg->param_dtype != FGD_BF16)
+        return fail(FGD_ERR_INVALID_ARG, "unknown param_dtype %d", cfg->param_dtype);
+    if (cfg->ld < cfg->num_params) return fail(FGD_ERR_INVALID_ARG, "ld < num_params");
+    if ((cfg->ld * elem_size(cfg->param_dtype)) % 16 != 0 || cfg->ld % 4 != 0)
+        return fail(FGD_ERR_INVALID_ARG, "rows must be 16-byte aligned: ld * elem_size and ld * 4 must be multiples of 16");
+    if (!std::isfinite(cfg->outer_lr) || !std::isfinite(cfg->momentum))
+        return fail(FGD_ERR_INVALID_ARG, "outer_lr and momentum must be finite");
+
+    fgd_engine *e = new (std::nothrow) fgd_engine();
+    if (!e) return fail(FGD_ERR_OUT_OF_MEMORY, "host allocation failed");
+    e->cfg = *cfg;
+    e->host_only = cfg->device < 0;
+    if (!e->host_only) {
+        hipError_t err = hipSetDevice(cfg->device);
+        if (err != hipSuccess) {
+            delete e;
+            return hip_fail(err, "hipSetDevice");
+        }
+        err = hipDeviceGetAttribute(&e->num_cus, hipDeviceAttributeMultiprocessorCount, cfg->device);
+        if (err != hipSuccess) {
+            delete e;
+            return hip_fail(err, "querying the compute-unit count");
+        }
+        const size_t M = static_cast<size_t>(cfg->num_workers);
+        // Largest packed tables: both slots, FGD_MAX_ROUNDS rounds, width M.
+        e->topo_capacity = 2 * static_cast<size_t>(FGD_MAX_ROUNDS) * M * M * 2 * sizeof(int32_t);
+        const int n_cd_max = 2 * FGD_MAX_ROUNDS + 3;
+        e->partials_capacity = static_cast<size_t>(e->num_cus) * kMaxBlocksPerCu * n_cd_max * M;
+        for (int r = 0; r < kTopoRing && err == hipSuccess; ++r) {
+            err = hipMalloc(&e->d_topo[r], e->topo_capacity);
+            if (err == hipSuccess) err = hipHostMalloc(&e->h_topo[r], e->topo_capacity, hipHostMallocDefault);
+            if (err == hipSuccess) err = hipEventCreateWithFlags(&e->topo_done[r], hipEventDisableTiming);
+        }
+        if (err == hipSuccess) err = hipMalloc(&e->d_partials, e->partials_capacity * sizeof(double));
+        if (err != hipSuccess) {
+            release(e);
+            delete e;
+            return fail(err == hipErrorOutOfMemory ? FGD_ERR_OUT_OF_MEMORY : FGD_ERR_HIP, "device set-up: %s",
+                        hipGetErrorString(err));
+        }
+    }
+    *out = e;
+    return FGD_OK;
+}
+
+fgd_status fgd_destroy(fgd_engine *e) {
+    if (!e) return FGD_OK;
+    if (!e->host_only) {
+        (void)hipSetDevice(e->cfg.device);
+        (void)hipDeviceSynchronize();
+        release(e);
+    }
+    delete e;
+    return FGD_OK;
+}
+
+fgd_status fgd_set_topology(fgd_engine *e, int32_t which, int32_t kind, const int32_t *row_ptr,
+                            const int32_t *col_idx, const float *weights, int32_t num_rounds,
+                            const uint8_t *edge_masks, int32_t reweight) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (which != FGD_MIX1 && which != FGD_MIX2) return fail(FGD_ERR_INVALID_ARG, "which must be FGD_MIX1 or FGD_MIX2");
+    fgd::MixTopology t;
+    std::string err;
+    fgd::TopoStatus ts = fgd::build_mix_topology(e->cfg.num_workers, kind, row_ptr, col_idx, weights, num_rounds,
+                                                 edge_masks, reweight, t, err);
+    if (ts != fgd::TopoStatus::ok) return from_topo(ts, err);
+    e->slot[which - 1] = std::move(t);
+    e->slot_set[which - 1] = true;
+    ++e->topo_version;
+    return FGD_OK;
+}
+
+fgd_status fgd_num_cd_rows(const fgd_engine *e, int32_t *n_rows) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (!n_rows) return fail(FGD_ERR_INVALID_ARG, "n_rows is NULL");
+    if (!e->slot_set[0] || !e->slot_set[1]) return fail(FGD_ERR_STATE, "both Mix slots must be set");
+    *n_rows = n_cd_rows(e);
+    return FGD_OK;
+}
+
+fgd_status fgd_get_effective_weights(const fgd_engine *e, int32_t which, int32_t round, float *out) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (which != FGD_MIX1 && which != FGD_MIX2) return fail(FGD_ERR_INVALID_ARG, "which must be FGD_MIX1 or FGD_MIX2");
+    if (!out) return fail(FGD_ERR_INVALID_ARG, "out is NULL");
+    const fgd::MixTopology &t = e->slot[which - 1];
+    if (!e->slot_set[which - 1]) return fail(FGD_ERR_STATE, "slot is not set");
+    if (t.kind != 2) return fail(FGD_ERR_STATE, "slot is not a CSR topology");
+    if (round < 0 || round >= t.rounds) return fail(FGD_ERR_INVALID_ARG, "round %d is outside [0, %d)", round, t.rounds);
+    const size_t nnz = t.col_idx.size();
+    std::memcpy(out, t.eff.data() + round * nnz, nnz * sizeof(float));
+    return FGD_OK;
+}
+
+fgd_status fgd_effective_weights(int32_t num_workers, const int32_t *row_ptr, const int32_t *col_idx,
+                                 const float *weights, const uint8_t *mask, int32_t reweight, float *out) {
+    g_last_error.clear();
+    if (reweight < 0 || reweight > 2) return fail(FGD_ERR_INVALID_ARG, "unknown reweighting %d", reweight);
+    std::string err;
+    return from_topo(fgd::effective_round_weights(num_workers, row_ptr, col_idx, weights, mask, reweight, out, err),
+                     err);
+}
+
+fgd_status fgd_min_bytes_per_step(const fgd_engine *e, int64_t *bytes) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (!bytes) return fail(FGD_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = static_cast<int64_t>(e->cfg.num_workers) * e->cfg.num_params * (3 * elem_size(e->cfg.param_dtype) + 2 * 4);
+    return FGD_OK;
+}
+
+fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
+                          double *cd_out, void *stream_handle) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (e->host_only) return fail(FGD_ERR_STATE, "host-only engine cannot run a step");
+    if (!e->slot_set[0] || !e->slot_set[1]) return fail(FGD_ERR_STATE, "both Mix slots must be set before a step");
+    const fgd_config &c = e->cfg;
+    if (!theta_prev || !theta_local || !momentum) return fail(FGD_ERR_INVALID_ARG, "NULL device array");
+    if (!aligned16(theta_prev) || !aligned16(theta_local) || !aligned16(momentum))
+        return fail(FGD_ERR_INVALID_ARG, "device arrays must be 16-byte aligned");
+    if (cd_out && (reinterpret_cast<uintptr_t>(cd_out) & 7u)) return fail(FGD_ERR_INVALID_ARG, "cd_out must be 8-byte aligned");
+    const int es = elem_size(c.param_dtype);
+    if (c.num_params > 0) {
+        uintptr_t a0, a1, b0, b1, v0, v1;
+        span(theta_prev, c.num_workers, c.ld, c.num_params, es, a0, a1);
+        span(theta_local, c.num_workers, c.ld, c.num_params, es, b0, b1);
+        span(momentum, c.num_workers, c.ld, c.num_params, 4, v0, v1);
+        if (overlap(a0, a1, b0, b1) || overlap(b0, b1, v0, v1) || overlap(a0, a1, v0, v1))
+            return fail(FGD_ERR_INVALID_ARG, "theta_prev, theta_local and momentum must not overlap");
+    }
+    hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    fgd::KernelSet ks;
+    if (!lookup(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, ks))
+        return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
+    hipError_t herr = hipSetDevice(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+
+    int ring = 0;
+    if (fgd_status st = ensure_topology(e, stream, ring)) return st;
+
+    fgd::StepParams p{};
+    p.theta_prev = theta_prev;
+    p.theta_local = theta_local;
+    p.mom = momentum;
+    p.P = c.num_params;
+    p.ld = c.ld;
+    p.ntiles = tiles_of(c.num_params, ks.v);
+    p.M = c.num_workers;
+    p.n_cd = n_cd_rows(e);
+    p.lr = c.outer_lr;
+    p.mu = c.momentum;
+    const void *t1, *t2;
+    table_ptrs(e, ring, t1, t2);
+    p.mix1 = mix_dev(e->slot[0], t1);
+    p.mix2 = mix_dev(e->slot[1], t2);
+    const bool tables = e->slot[0].kind == 2 || e->slot[1].kind == 2;
+    size_t lds = tables ? static_cast<size_t>(c.num_workers + 1) * fgd::kBlock * ks.v * sizeof(float) : 0;
+    if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
+
+    int grid = 0;
+    if (fgd_status st = grid_for(e, ks.step, lds, p.ntiles, grid)) return st;
+    if (cd_out) {
+        if (static_cast<size_t>(grid) * p.n_cd * c.num_workers > e->partials_capacity)
+            return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
+        p.cd_partials = e->d_partials;
+    }
+
+    const bool timed = e->timing && e->timed < kTimingPool;
+    if (timed) {
+        if (static_cast<int64_t>(e->ev_start.size()) <= e->timed) {
+            hipEvent_t a, b;
+            herr = hipEventCreate(&a);
+            if (herr == hipSuccess) herr = hipEventCreate(&b);
+            if (herr != hipSuccess) return hip_fail(herr, "creating timing events");
+            e->ev_start.push_back(a);
+            e->ev_stop.push_back(b);
+        }
+        herr = hipEventRecord(e->ev_start[e->timed], stream);
+        if (herr != hipSuccess) return hip_fail(herr, "recording a timing event");
+    }
+    if (fgd_status st = launch(ks.step, grid, lds, stream, &p)) return st;
+    if (timed) {
+        herr = hipEventRecord(e->ev_stop[e->timed], stream);
+        if (herr != hipSuccess) return hip_fail(herr, "recording a timing event");
+        ++e->timed;
+    }
+    herr = hipEventRecord(e->topo_done[ring], stream);
+    if (herr != hipSuccess) return hip_fail(herr, "recording the topology event");
+    e->topo_pending[ring] = true;
+    if (cd_out) return launch_finalize(e->d_partials, grid, p.n_cd * c.num_workers, cd_out, stream);
+    return FGD_OK;
+}
+
+fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, double *out, void *stream_handle) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (e->host_only) return fail(FGD_ERR_STATE, "host-only engine cannot run a kernel");
+    if (!x || !out) return fail(FGD_ERR_INVALID_ARG, "NULL device array");
+    if (dtype != FGD_F32 && dtype != FGD_BF16) return fail(FGD_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+    const fgd_config &c = e->cfg;
+    if (!aligned16(x)) return fail(FGD_ERR_INVALID_ARG, "x must be 16-byte aligned");
+    if ((c.ld * elem_size(dtype)) % 16 != 0) return fail(FGD_ERR_INVALID_ARG, "ld * elem_size must be a multiple of 16");
+    if (reinterpret_cast<uintptr_t>(out) & 7u) return fail(FGD_ERR_INVALID_ARG, "out must be 8-byte aligned");
+    fgd::KernelSet ks;
+    if (!lookup(c.num_workers, dtype, 0, 0, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
+    hipError_t herr = hipSetDevice(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    fgd::ConsensusParams p{};
+    p.x = x;
+    p.P = c.num_params;
+    p.ld = c.ld;
+    p.ntiles = tiles_of(c.num_params, ks.v);
+    p.M = c.num_workers;
+    p.partials = e->d_partials;
+    int grid = 0;
+    if (fgd_status st = grid_for(e, ks.consensus, 0, p.ntiles, grid)) return st;
+    if (static_cast<size_t>(grid) * c.num_workers > e->partials_capacity)
+        return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
+    if (fgd_status st = launch(ks.consensus, grid, 0, stream, &p)) return st;
+    return launch_finalize(e->d_partials, grid, c.num_workers, out, stream);
+}
+
+fgd_status fgd_enable_timing(fgd_engine *e, int32_t enable) {
+    if (fgd_status st = check_engine(e)) return st;
+    e->timing = enable != 0;
+    e->timed = 0;
+    return FGD_OK;
+}
+
+fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (!total_ms || !count) return fail(FGD_ERR_INVALID_ARG, "NULL output");
+    double sum = 0.0;
+    for (int64_t i = 0; i < e->timed; ++i) {
+        hipError_t err = hipEventSynchronize(e->ev_stop[i]);
+        if (err != hipSuccess) return hip_fail(err, "waiting for a timing event");
+        float ms = 0.0f;
+        err = hipEventElapsedTime(&ms, e->ev_start[i], e->ev_stop[i]);
+        if (err != hipSuccess) return hip_fail(err, "reading a timing event");
+        sum += ms;
+    }
+    *total_ms = sum;
+    *count = e->timed;
+    return FGD_OK;
+}
+
+fgd_status fgd_stream_copy(void *dst, const void *src, int64_t bytes, void *stream_handle) {
+    g_last_error.clear();
+    if (!dst || !src || bytes < 0 || bytes % 16 != 0 || !aligned16(dst) || !aligned16(src))
+        return fail(FGD_ERR_INVALID_ARG, "copy needs 16-byte aligned pointers and a size multiple of 16");
+    if (bytes == 0) return FGD_OK;
+    const int64_t n = bytes / 16;
+    int dev = 0, cus = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return hip_fail(err, "device query");
+    const int64_t blocks = std::min<int64_t>((n + 1023) / 1024, static_cast<int64_t>(cus) * 8);
+    hipLaunchKernelGGL(fgd::copy_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                       static_cast<hipStream_t>(stream_handle), static_cast<const fgd::u32x4 *>(src),
+                       static_cast<fgd::u32x4 *>(dst), n);
+    err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(err, "copy launch");
+    return FGD_OK;
+}
+
+}  // extern "C"

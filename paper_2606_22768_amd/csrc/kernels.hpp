@@ -1,0 +1,612 @@
+// kernels.hpp -- HIP kernels of the fused outer step for gfx950 (CDNA4).
+//
+// The step (Sec. 4.1 factored formulation; Appendix A, Algorithm 1, outer
+// step; Appendix B Nesterov form) is a bandwidth-bound pass over M worker
+// rows.  Every parameter index p is independent given W, so one lane owns V
+// consecutive parameters of *all* M workers and keeps them in registers:
+//
+//   phase A  load theta_prev and theta_local rows (16-byte nontemporal loads
+//            where V allows), g0 = theta_prev - theta_local
+//   mix      Mix2 on g and Mix1 on x = theta_prev: a global mean in registers,
+//            or CSR rounds.  A CSR round needs u[col] for a run-time col, so
+//            the lane parks its M values in its own column of an LDS array
+//            [M+1][block][V] (row M is all zero and pads short rows) and
+//            gathers neighbours from there.  Each lane touches only its own
+//            column, so no barrier is needed.  Per round the host supplies a
+//            padded table [width][M] of (column, weight): the d-th live entry
+//            of every row, in ascending column order, so the sum runs in the
+//            same order as the CSR row.
+//   phase D  load momentum rows, v' = mu v + g, theta' = x - lr (g + mu v'),
+//            store theta' (RNE to bf16 for bf16 storage) and v'.
+//   CD       S_m(u) = sum_p (u_m - mean_n u_n)^2 for every intermediate u
+//            (Sec. 4.4; Appendix D.1): float32 deviations, a reduce-scatter
+//            across the wave's lanes, double accumulation per (row, worker)
+//            in LDS, per-block partials and a fixed-order finalize kernel, so
+//            results are deterministic.
+//
+// No matrix cores: the work is a sparse weighted reduction across rows.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fgd {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBlock = 256;
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = kBlock / kWave;
+
+enum MixKind : int32_t { kIdentity = 0, kGlobal = 1, kTable = 2 };
+
+struct MixDev {
+    int32_t kind;       // MixKind
+    int32_t rounds;     // table rounds (kTable)
+    int32_t width;      // entries per row in each round's table
+    int32_t pad_;
+    const int2 *table;  // [rounds][width][M] of (column, bit pattern of float weight)
+};
+
+struct StepParams {
+    void *theta_prev;         // [M][ld] storage type, in/out
+    const void *theta_local;  // [M][ld] storage type
+    float *mom;               // [M][ld] float32, in/out
+    double *cd_partials;      // [gridDim.x][n_cd][M] or nullptr
+    int64_t P, ld, ntiles;
+    int32_t M, n_cd;
+    float lr, mu;
+    MixDev mix1, mix2;
+};
+
+struct ConsensusParams {
+    const void *x;            // [M][ld] storage type
+    double *partials;         // [gridDim.x][M]
+    int64_t P, ld, ntiles;
+    int32_t M, pad_;
+};
+
+constexpr int pow2_at_least(int m) { return m <= 1 ? 1 : 2 * pow2_at_least((m + 1) / 2); }
+constexpr int ilog2(int m) { return m <= 1 ? 0 : 1 + ilog2(m / 2); }
+
+// ------------------------------------------------------------ storage access
+
+// float32 storage, V in {1, 2, 4}.
+template <int V>
+struct F32Io {
+    static constexpr int kElem = 4;
+    __device__ static void load(const float *p, float (&o)[V]) {
+        if constexpr (V == 4) {
+            f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(p));
+            o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
+        } else if constexpr (V == 2) {
+            f32x2 t = __builtin_nontemporal_load(reinterpret_cast<const f32x2 *>(p));
+            o[0] = t.x; o[1] = t.y;
+        } else {
+            o[0] = __builtin_nontemporal_load(p);
+        }
+    }
+    __device__ static void store(float *p, const float (&i)[V]) {
+        if constexpr (V == 4) {
+            f32x4 t = {i[0], i[1], i[2], i[3]};
+            __builtin_nontemporal_store(t, reinterpret_cast<f32x4 *>(p));
+        } else if constexpr (V == 2) {
+            f32x2 t = {i[0], i[1]};
+            __builtin_nontemporal_store(t, reinterpret_cast<f32x2 *>(p));
+        } else {
+            __builtin_nontemporal_store(i[0], p);
+        }
+    }
+};
+
+// Elementwise store of the first n < V values (ragged tail of a row).
+template <int V>
+__device__ inline void tail_store(float *p, int n, const float (&i)[V]) {
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+        if (v < n) p[v] = i[v];
+}
+
+// Parameter storage: float32 or bf16 bit patterns.  load/store of a full
+// vector of V elements at element index row + lo of `base`, where `row` is
+// wave-uniform (row start plus tile start, kept in scalar registers) and `lo`
+// the lane's offset inside the tile; store_part writes only the first n < V
+// elements (ragged tail of a row).
+template <int V>
+struct ParamF32 {
+    static constexpr int kElem = 4;
+    __device__ static void load(const void *base, int64_t row, uint32_t lo, float (&o)[V]) {
+        F32Io<V>::load(static_cast<const float *>(base) + row + lo, o);
+    }
+    // Stores and returns the stored values in `s`.
+    __device__ static void store(void *base, int64_t row, uint32_t lo, const float (&i)[V], float (&s)[V]) {
+        F32Io<V>::store(static_cast<float *>(base) + row + lo, i);
+#pragma unroll
+        for (int v = 0; v < V; ++v) s[v] = i[v];
+    }
+    __device__ static void store_part(void *base, int64_t row, uint32_t lo, int n, const float (&i)[V],
+                                      float (&s)[V]) {
+        float *p = static_cast<float *>(base) + row + lo;
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            if (v < n) p[v] = i[v];
+            s[v] = v < n ? i[v] : 0.0f;
+        }
+    }
+};
+
+__device__ inline float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ inline float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ inline uint32_t pack_bf16(float a, float b) {
+    f32x2 f = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+}
+__device__ inline uint16_t to_bf16(float a) { return static_cast<uint16_t>(pack_bf16(a, 0.0f) & 0xFFFFu); }
+
+// bf16 storage, V in {1, 2, 4, 8}.
+template <int V>
+struct ParamBF16 {
+    static constexpr int kElem = 2;
+    __device__ static void load(const void *base, int64_t row, uint32_t lo, float (&o)[V]) {
+        const uint16_t *p = static_cast<const uint16_t *>(base) + row + lo;
+        if constexpr (V == 8) {
+            u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+            uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { o[2 * k] = bf16_lo(w[k]); o[2 * k + 1] = bf16_hi(w[k]); }
+        } else if constexpr (V == 4) {
+            u32x2 t = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(p));
+            o[0] = bf16_lo(t.x); o[1] = bf16_hi(t.x); o[2] = bf16_lo(t.y); o[3] = bf16_hi(t.y);
+        } else if constexpr (V == 2) {
+            uint32_t t = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
+            o[0] = bf16_lo(t); o[1] = bf16_hi(t);
+        } else {
+            o[0] = __uint_as_float(static_cast<uint32_t>(__builtin_nontemporal_load(p)) << 16);
+        }
+    }
+    __device__ static void store(void *base, int64_t row, uint32_t lo, const float (&i)[V], float (&s)[V]) {
+        uint16_t *p = static_cast<uint16_t *>(base) + row + lo;
+        if constexpr (V == 1) {
+            uint16_t h = to_bf16(i[0]);
+            __builtin_nontemporal_store(h, p);
+            s[0] = __uint_as_float(static_cast<uint32_t>(h) << 16);
+        } else {
+            uint32_t w[V / 2];
+#pragma unroll
+            for (int k = 0; k < V / 2; ++k) {
+                w[k] = pack_bf16(i[2 * k], i[2 * k + 1]);
+                s[2 * k] = bf16_lo(w[k]);
+                s[2 * k + 1] = bf16_hi(w[k]);
+            }
+            if constexpr (V == 8) {
+                u32x4 t = {w[0], w[1], w[2], w[3]};
+                __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(p));
+            } else if constexpr (V == 4) {
+                u32x2 t = {w[0], w[1]};
+                __builtin_nontemporal_store(t, reinterpret_cast<u32x2 *>(p));
+            } else {
+                __builtin_nontemporal_store(w[0], reinterpret_cast<uint32_t *>(p));
+            }
+        }
+    }
+    __device__ static void store_part(void *base, int64_t row, uint32_t lo, int n, const float (&i)[V],
+                                      float (&s)[V]) {
+        uint16_t *p = static_cast<uint16_t *>(base) + row + lo;
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            uint16_t h = to_bf16(i[v]);
+            if (v < n) p[v] = h;
+            s[v] = v < n ? __uint_as_float(static_cast<uint32_t>(h) << 16) : 0.0f;
+        }
+    }
+};
+
+// ------------------------------------------------------- consensus pieces
+
+// Sum over the wave of part[j] for every j < C, scattered so that lane l ends
+// up with the total of j = l >> (6 - log2 C) (every lane of that group of
+// 64 / C lanes holds it).  Halving steps swap half of the remaining values
+// with the partner lane (lane ^ s) and add; the rest is a butterfly.  The
+// order of additions is fixed, so results are deterministic.
+template <int C>
+__device__ inline float wave_reduce_scatter(float (&part)[C], int lane) {
+    int n = C;
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        if (n > 1) {
+            n >>= 1;
+            const bool upper = (lane & s) != 0;
+#pragma unroll
+            for (int i = 0; i < C / 2; ++i) {
+                if (i < n) {
+                    // Read both values first: a select between two array
+                    // lvalues would index the register array dynamically.
+                    const float lower_half = part[i], upper_half = part[i + n];
+                    const float send = upper ? lower_half : upper_half;
+                    const float keep = upper ? upper_half : lower_half;
+                    part[i] = keep + __shfl_xor(send, s);
+                }
+            }
+        } else {
+            part[0] += __shfl_xor(part[0], s);
+        }
+    }
+    return part[0];
+}
+
+// Mean over the M rows of u, per element (float32, ascending rows).
+template <int MMAX, bool EXACT, int V>
+__device__ inline void row_mean(const float (&u)[MMAX][V], int M, float (&mean)[V]) {
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        float s = 0.0f;
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m)
+            if (EXACT || m < M) s += u[m][v];
+        mean[v] = s / static_cast<float>(EXACT ? MMAX : M);
+    }
+}
+
+// Adds this lane-column's contribution to S_m(u) = sum_p (u_m - mean u)^2 into
+// the wave's double accumulators acc[m].  Workers are reduced in chunks of at
+// most 16 to bound register use.
+template <int MMAX, bool EXACT, int V>
+__device__ inline void cd_accumulate(const float (&u)[MMAX][V], int M, double *acc, int lane) {
+    constexpr int MP = pow2_at_least(MMAX);
+    constexpr int C = MP < 16 ? MP : 16;
+    constexpr int kShift = 6 - ilog2(C);
+    float mean[V];
+    row_mean<MMAX, EXACT, V>(u, M, mean);
+#pragma unroll
+    for (int c = 0; c < MP / C; ++c) {
+        float part[C];
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            const int m = c * C + j;
+            float t = 0.0f;
+            if (m < MMAX && (EXACT || m < M)) {
+#pragma unroll
+                for (int v = 0; v < V; ++v) {
+                    const float d = u[m < MMAX ? m : 0][v] - mean[v];
+                    t = fmaf(d, d, t);
+                }
+            }
+            part[j] = t;
+        }
+        const float tot = wave_reduce_scatter<C>(part, lane);
+        const int m = c * C + (lane >> kShift);
+        if ((lane & ((1 << kShift) - 1)) == 0 && m < M) acc[m] += static_cast<double>(tot);
+    }
+}
+
+// ------------------------------------------------------------------ mixing
+
+// Mix kinds as template arguments; kAny reads the kind at run time.
+constexpr int kAny = 3;
+
+// The tables are read through the constant address space: they are never
+// written by the kernel, and this lets every (column, weight) pair arrive in
+// scalar registers, shared by the wave.
+typedef const __attribute__((address_space(4))) int32_t *const_table_ptr;
+
+// One table round applied in place: u_m <- sum_d w[d][m] * u_{col[d][m]}.
+// The lane parks u in its column of the LDS rows, then gathers from there.
+template <int MMAX, bool EXACT, int V>
+__device__ inline void table_round(const_table_ptr tab, int width, int M, float (&u)[MMAX][V], float *rows,
+                                   int tid) {
+    const int Mr = EXACT ? MMAX : M;
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+        if (EXACT || m < M) {
+            float *dst = rows + (static_cast<int64_t>(m) * kBlock + tid) * V;
+            if constexpr (V == 4) {
+                *reinterpret_cast<f32x4 *>(dst) = f32x4{u[m][0], u[m][1], u[m][2], u[m][3]};
+            } else if constexpr (V == 2) {
+                *reinterpret_cast<f32x2 *>(dst) = f32x2{u[m][0], u[m][1]};
+            } else {
+#pragma unroll
+                for (int v = 0; v < V; ++v) dst[v] = u[m][v];
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < V; ++v) u[m][v] = 0.0f;
+    }
+    for (int d = 0; d < width; ++d) {
+        const_table_ptr td = tab + 2 * d * Mr;
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+            // Keep the scheduler from hoisting every row's table entry into
+            // scalar registers at once.
+            if (m % 16 == 0 && m > 0) __builtin_amdgcn_sched_barrier(0);
+            if (EXACT || m < M) {
+                const int col = td[2 * m];
+                const float w = __int_as_float(td[2 * m + 1]);
+                const float *src = rows + (static_cast<int64_t>(col) * kBlock + tid) * V;
+                float r[V];
+                if constexpr (V == 4) {
+                    const f32x4 t = *reinterpret_cast<const f32x4 *>(src);
+                    r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
+                } else if constexpr (V == 2) {
+                    const f32x2 t = *reinterpret_cast<const f32x2 *>(src);
+                    r[0] = t.x; r[1] = t.y;
+                } else {
+#pragma unroll
+                    for (int v = 0; v < V; ++v) r[v] = src[v];
+                }
+#pragma unroll
+                for (int v = 0; v < V; ++v) u[m][v] = fmaf(w, r[v], u[m][v]);
+            }
+        }
+    }
+}
+
+// Applies one Mix slot.  For a global mean the result is written to `mean`
+// only (KIND == kGlobal) or to every row (KIND == kAny).  cd_acc: the wave's
+// accumulators of the slot's first round-output row (nullptr: no consensus);
+// consecutive rounds use consecutive rows, `cd_stride` doubles apart.
+template <int MMAX, bool EXACT, int V, int KIND>
+__device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], float (&mean)[V], float *rows,
+                                 int tid, double *cd_acc, int cd_stride, int lane) {
+    if constexpr (KIND == kIdentity) {
+        return;
+    } else if constexpr (KIND == kGlobal) {
+        row_mean<MMAX, EXACT, V>(u, M, mean);
+    } else {
+        if (KIND == kAny && mx.kind == kGlobal) {
+            row_mean<MMAX, EXACT, V>(u, M, mean);
+#pragma unroll
+            for (int m = 0; m < MMAX; ++m)
+#pragma unroll
+                for (int v = 0; v < V; ++v) u[m][v] = mean[v];
+            return;  // every row equal: the consensus row stays 0
+        }
+        if (KIND == kAny && mx.kind != kTable) return;
+        const int Mr = EXACT ? MMAX : M;
+        for (int k = 0; k < mx.rounds; ++k) {
+            const_table_ptr tab = (const_table_ptr)(mx.table) + 2 * static_cast<int64_t>(k) * mx.width * Mr;
+            table_round<MMAX, EXACT, V>(tab, mx.width, M, u, rows, tid);
+            if (cd_acc) cd_accumulate<MMAX, EXACT, V>(u, M, cd_acc + k * cd_stride, lane);
+        }
+    }
+}
+
+// ------------------------------------------------------------ step kernel
+
+// Waves per SIMD the register allocator is asked to leave room for: enough
+// waves in flight to keep HBM busy while others mix.
+constexpr int waves_per_simd_target(int mmax) { return mmax <= 4 ? 4 : (mmax <= 8 ? 2 : 1); }
+
+// K1, K2: compile-time kinds of Mix1 and Mix2 (kAny = decided at run time).
+template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(waves_per_simd_target(MMAX))))
+void outer_step_kernel(StepParams a) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    constexpr int MP = pow2_at_least(MMAX);
+    constexpr int kCdStride = kWavesPerBlock * MP;  // doubles between consensus rows
+    const int M = EXACT ? MMAX : a.M;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const bool tables = (K1 == kTable || K2 == kTable) ||
+                        ((K1 == kAny || K2 == kAny) && (a.mix1.kind == kTable || a.mix2.kind == kTable));
+    float *rows = reinterpret_cast<float *>(smem);
+    const int64_t rows_bytes = tables ? static_cast<int64_t>(M + 1) * kBlock * V * 4 : 0;
+    double *cd_acc = a.cd_partials ? reinterpret_cast<double *>(smem + rows_bytes) + wave * MP : nullptr;
+    const int n2 = a.mix2.kind == kTable ? a.mix2.rounds : (a.mix2.kind == kGlobal ? 1 : 0);
+    const int n1 = a.mix1.kind == kTable ? a.mix1.rounds : (a.mix1.kind == kGlobal ? 1 : 0);
+
+    if (tables) {
+        float *z = rows + (static_cast<int64_t>(M) * kBlock + tid) * V;
+#pragma unroll
+        for (int v = 0; v < V; ++v) z[v] = 0.0f;
+    }
+    if (cd_acc) {
+        for (int i = lane; i < a.n_cd * MP; i += kWave) cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
+    }
+
+    const uint32_t lo = static_cast<uint32_t>(tid) * V;  // lane offset inside a tile
+    for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+        const int64_t tb = tile * (kBlock * V);  // first parameter of the tile (uniform)
+        const int64_t rem = a.P - tb - lo;
+        const int nv = rem >= V ? V : (rem > 0 ? static_cast<int>(rem) : 0);
+
+        // Phase A: every row's loads are issued before the first use.  A lane
+        // whose vector straddles P still loads the whole vector (the row's ld
+        // span covers it) and zeroes the elements at or beyond P.
+        float u1[MMAX][V];  // theta_prev, then Mix1 output (unless global)
+        float u2[MMAX][V];  // theta_local, then g0, then Mix2 output (unless global)
+        if (nv > 0) {
+#pragma unroll
+            for (int m = 0; m < MMAX; ++m) {
+                if (EXACT || m < M) {
+                    PIO::load(a.theta_prev, m * a.ld + tb, lo, u1[m]);
+                    PIO::load(a.theta_local, m * a.ld + tb, lo, u2[m]);
+                }
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                if ((EXACT || m < M) && v < nv) u2[m][v] = u1[m][v] - u2[m][v];
+                else { u1[m][v] = 0.0f; u2[m][v] = 0.0f; }
+            }
+        }
+        if (cd_acc) {
+            cd_accumulate<MMAX, EXACT, V>(u2, M, cd_acc, lane);
+            cd_accumulate<MMAX, EXACT, V>(u1, M, cd_acc + (n2 + 1) * kCdStride, lane);
+        }
+
+        float xbar[V], gbar[V];
+        mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, rows, tid, cd_acc ? cd_acc + (n2 + 2) * kCdStride : nullptr,
+                                      kCdStride, lane);
+        mix_apply<MMAX, EXACT, V, K2>(a.mix2, M, u2, gbar, rows, tid, cd_acc ? cd_acc + 1 * kCdStride : nullptr,
+                                      kCdStride, lane);
+
+        // Phase D: Nesterov (two-line form) and stores, a group of rows at a
+        // time.  The stored theta' replaces the row's dead input registers.
+        constexpr bool kStoreInU2 = K2 != kGlobal;
+        constexpr bool kStoreInU1 = !kStoreInU2 && K1 != kGlobal;
+        constexpr int kSep = (!kStoreInU2 && !kStoreInU1) ? MMAX : 1;
+        float sep[kSep][V];
+        constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
+        const float mu = a.mu, lr = a.lr;
+#pragma unroll
+        for (int m0 = 0; m0 < MMAX; m0 += G) {
+            float vm[G][V];
+            if (nv > 0) {
+#pragma unroll
+                for (int j = 0; j < G; ++j) {
+                    const int m = m0 + j;
+                    if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(a.mom + (m * a.ld + tb) + lo, vm[j]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                const int m = m0 + j;
+                if (m >= MMAX) continue;
+                float stored[V];
+                if ((EXACT || m < M) && nv > 0) {
+                    float t[V];
+#pragma unroll
+                    for (int e = 0; e < V; ++e) {
+                        const float g = K2 == kGlobal ? gbar[e] : u2[m][e];
+                        const float x = K1 == kGlobal ? xbar[e] : u1[m][e];
+                        vm[j][e] = fmaf(mu, vm[j][e], g);
+                        t[e] = fmaf(-lr, fmaf(mu, vm[j][e], g), x);
+                    }
+                    const int64_t row = m * a.ld + tb;
+                    if (nv == V) {
+                        F32Io<V>::store(a.mom + row + lo, vm[j]);
+                        PIO::store(a.theta_prev, row, lo, t, stored);
+                    } else {
+                        tail_store(a.mom + row + lo, nv, vm[j]);
+                        PIO::store_part(a.theta_prev, row, lo, nv, t, stored);
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < V; ++e) stored[e] = 0.0f;
+                }
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    if constexpr (kStoreInU2) u2[m][e] = stored[e];
+                    else if constexpr (kStoreInU1) u1[m][e] = stored[e];
+                    else sep[kSep == 1 ? 0 : m][e] = stored[e];
+                }
+            }
+        }
+        if (cd_acc) {
+            double *acc = cd_acc + (n2 + n1 + 2) * kCdStride;
+            if constexpr (kStoreInU2) cd_accumulate<MMAX, EXACT, V>(u2, M, acc, lane);
+            else if constexpr (kStoreInU1) cd_accumulate<MMAX, EXACT, V>(u1, M, acc, lane);
+            else cd_accumulate<MMAX, EXACT, V>(sep, M, acc, lane);
+        }
+    }
+
+    if (cd_acc) {
+        __syncthreads();
+        const double *base = reinterpret_cast<const double *>(smem + rows_bytes);
+        for (int i = tid; i < a.n_cd * M; i += kBlock) {
+            const int r = i / M, m = i % M;
+            double s = 0.0;
+#pragma unroll
+            for (int w = 0; w < kWavesPerBlock; ++w) s += base[r * kCdStride + w * MP + m];
+            a.cd_partials[(static_cast<int64_t>(blockIdx.x) * a.n_cd + r) * M + m] = s;
+        }
+    }
+}
+
+// ------------------------------------------------- standalone consensus
+
+template <int MMAX, bool EXACT, int V, class PIO>
+__global__ __launch_bounds__(kBlock) void consensus_kernel(ConsensusParams a) {
+    constexpr int MP = pow2_at_least(MMAX);
+    __shared__ double acc[kWavesPerBlock * MP];
+    const int M = EXACT ? MMAX : a.M;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    for (int i = tid; i < kWavesPerBlock * MP; i += kBlock) acc[i] = 0.0;
+    __syncthreads();
+    const uint32_t lo = static_cast<uint32_t>(tid) * V;
+    for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+        const int64_t tb = tile * (kBlock * V);
+        const int64_t rem = a.P - tb - lo;
+        const int nv = rem >= V ? V : (rem > 0 ? static_cast<int>(rem) : 0);
+        float u[MMAX][V];
+        if (nv > 0) {
+#pragma unroll
+            for (int m = 0; m < MMAX; ++m)
+                if (EXACT || m < M) PIO::load(a.x, m * a.ld + tb, lo, u[m]);
+        }
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m)
+#pragma unroll
+            for (int v = 0; v < V; ++v)
+                if (!((EXACT || m < M) && v < nv)) u[m][v] = 0.0f;
+        cd_accumulate<MMAX, EXACT, V>(u, M, acc + wave * MP, lane);
+    }
+    __syncthreads();
+    for (int m = tid; m < M; m += kBlock) {
+        double s = 0.0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) s += acc[w * MP + m];
+        a.partials[static_cast<int64_t>(blockIdx.x) * M + m] = s;
+    }
+}
+
+// out[i] = sum over blocks b of partials[b][i], i < n, in a fixed order (one
+// block per entry; launch with n blocks of 256 threads).
+__global__ void finalize_kernel(const double *partials, int nblocks, int n, double *out);
+
+// Plain 16-byte streaming copy.
+__global__ void copy_kernel(const u32x4 *src, u32x4 *dst, int64_t n);
+
+// ------------------------------------------------------------ dispatch
+
+// Launch description of one (M, dtype) instantiation.
+struct KernelSet {
+    const void *step;       // outer_step_kernel instantiation for the requested kinds
+    const void *consensus;  // consensus_kernel instantiation
+    int v;                  // elements per lane per row
+    int mmax;               // compile-time worker bound
+};
+
+// Kernel set of one instantiation; the step kernel is specialised on the
+// (Mix1, Mix2) kinds of the paper's configurations (Appendix A table:
+// GlobalM1LocalM2, LocalM1M2, GlobalM1, DiLoCo) when M is exact.
+template <template <int> class PIOT, int MMAX, bool EXACT, int V>
+KernelSet make_kernel_set(int k1, int k2) {
+    using P = PIOT<V>;
+    KernelSet ks;
+    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny>);
+    if constexpr (EXACT) {
+        if (k1 == kGlobal && k2 == kTable)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable>);
+        else if (k1 == kTable && k2 == kTable)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kTable, kTable>);
+        else if (k1 == kGlobal && k2 == kIdentity)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity>);
+        else if (k1 == kIdentity && k2 == kGlobal)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kIdentity, kGlobal>);
+    }
+    ks.consensus = reinterpret_cast<const void *>(&consensus_kernel<MMAX, EXACT, V, P>);
+    ks.v = V;
+    ks.mmax = MMAX;
+    return ks;
+}
+
+// Elements per lane per row: 16-byte float32 accesses up to 16 workers; bf16
+// parameters use 8-byte accesses (4 elements) so that momentum still moves in
+// 16-byte accesses and the register and LDS footprint per lane stays small.
+constexpr int lanes_v_f32(int mmax) { return mmax <= 16 ? 4 : (mmax == 32 ? 2 : 1); }
+constexpr int lanes_v_bf16(int mmax) { return mmax <= 16 ? 4 : (mmax == 32 ? 2 : 1); }
+
+// Defined per storage type.  k1, k2: Mix kinds (kIdentity, kGlobal, kTable);
+// a specialised step kernel is returned when one exists, else the one that
+// reads the kinds at run time.  Returns false if M is outside [1, 64].
+bool kernels_f32(int M, int k1, int k2, KernelSet *out);
+bool kernels_bf16(int M, int k1, int k2, KernelSet *out);
+
+}  // namespace fgd

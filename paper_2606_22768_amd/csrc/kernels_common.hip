@@ -1,0 +1,45 @@
+// Kernels shared by every instantiation: consensus finalize and the plain
+// streaming copy used as the bandwidth reference.
+#include "kernels.hpp"
+
+namespace fgd {
+
+// One block per output entry i: thread t sums partials[b][i] for b = t, t +
+// 256, ... in ascending b, then a fixed-shape tree in LDS adds the 256
+// thread sums.  The order of additions never changes, so the result is
+// deterministic.
+__global__ __launch_bounds__(256) void finalize_kernel(const double *partials, int nblocks, int n, double *out) {
+    __shared__ double s[256];
+    const int i = blockIdx.x, t = threadIdx.x;
+    double acc = 0.0;
+    for (int b = t; b < nblocks; b += 256) acc += partials[static_cast<int64_t>(b) * n + i];
+    s[t] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) s[t] += s[t + w];
+        __syncthreads();
+    }
+    if (t == 0) out[i] = s[0];
+}
+
+// Each block iteration moves 4 vectors of 16 bytes per thread; all four loads
+// are issued before the stores.
+__global__ __launch_bounds__(256) void copy_kernel(const u32x4 *src, u32x4 *dst, int64_t n) {
+    constexpr int kUnroll = 4;
+    const int64_t chunk = static_cast<int64_t>(blockDim.x) * kUnroll;
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * chunk; base < n; base += static_cast<int64_t>(gridDim.x) * chunk) {
+        u32x4 r[kUnroll];
+#pragma unroll
+        for (int j = 0; j < kUnroll; ++j) {
+            const int64_t i = base + j * blockDim.x + threadIdx.x;
+            if (i < n) r[j] = __builtin_nontemporal_load(src + i);
+        }
+#pragma unroll
+        for (int j = 0; j < kUnroll; ++j) {
+            const int64_t i = base + j * blockDim.x + threadIdx.x;
+            if (i < n) __builtin_nontemporal_store(r[j], dst + i);
+        }
+    }
+}
+
+}  // namespace fgd

@@ -1,0 +1,175 @@
+"""Shared helpers of the parity tests: run one outer step on the HIP engine
+and on the CPU oracle from the same seeded inputs and compare them.
+
+Tolerances (bars the engine must meet against the oracle):
+  float32 outputs   per worker row, max_p |gpu - ref| / max_p |ref| <= 1e-6
+  bf16 theta'       at most 1 ulp apart (ordered-integer distance of the encodings),
+                    or |gpu - ref| <= ulp(ref) + delta where the float32 evaluation
+                    error itself exceeds half an ulp of the result
+The float32 evaluation error of theta' is relative to the operands (the
+mixed parameters, the mixed gradient), not to theta': where theta' nearly
+cancels to 0 its bf16 ulp is tiny.  delta = 32 * eps32 * max|theta_prev|
+bounds that error for up to 3 rounds of degree <= 4 (a few float32 roundings
+per round, each relative to max|theta|); for a typical element delta is
+~1/600 of an ulp, so those elements are held to 1 ulp.
+  consensus rows    per row, max_m |gpu - ref| <= 1e-5 * max_m |ref| + floor
+The consensus bound follows from float32 deviations: each deviation carries a
+relative error of about eps32 * (2 |u| / |u - mean| + 2), at most ~1e-6 for
+these inputs, doubled by squaring; 1e-5 leaves a factor of five.  The float32
+mean of equal values need not equal them, so a row that is exactly 0 in
+double precision can come out at the rounding floor
+P * (4 * eps32 * max|theta|)^2, which is added as an absolute term.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from synth import configs, graphs, tensors
+
+F32_RTOL = 1e-6
+CD_RTOL = 1e-5
+EPS32 = 2.0 ** -24
+
+
+def ordered_bf16(bits):
+    """bf16 bit patterns -> integers ordered like the values they encode."""
+    b = np.asarray(bits, dtype=np.int64)
+    return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
+
+
+def max_row_rel_err(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.maximum(np.abs(ref).max(axis=1), 1e-300)
+    return float((np.abs(got - ref).max(axis=1) / den).max()) if got.size else 0.0
+
+
+def bf16_value(bits):
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def bf16_ulp(bits):
+    """Distance from |value| to the next bf16 value up in magnitude."""
+    mag = np.asarray(bits, np.uint16) & 0x7FFF
+    return bf16_value(mag + 1) - bf16_value(mag)
+
+
+def compare_outputs(dtype, got_t, ref_t, got_v, ref_v, P, theta_scale=None):
+    """Asserts theta' and v' parity on [:, :P]; theta_scale = max|theta_prev|
+    (needed for bf16)."""
+    got_v, ref_v = got_v[:, :P], ref_v[:, :P]
+    assert np.all(np.isfinite(got_v) == np.isfinite(ref_v))
+    e_v = max_row_rel_err(got_v, ref_v)
+    assert e_v <= F32_RTOL, f"momentum relative error {e_v:.3e}"
+    if dtype == "f32":
+        e_t = max_row_rel_err(got_t[:, :P], ref_t[:, :P])
+        assert e_t <= F32_RTOL, f"theta relative error {e_t:.3e}"
+    else:
+        g, r = got_t[:, :P], ref_t[:, :P]
+        d = np.abs(ordered_bf16(g) - ordered_bf16(r))
+        delta = 32 * EPS32 * theta_scale
+        near_zero = np.abs(bf16_value(g) - bf16_value(r)) <= bf16_ulp(r) + delta
+        bad = (d > 1) & ~near_zero
+        assert not bad.any(), (f"theta differs by {d[bad].max()} bf16 ulps at {int(bad.sum())} elements "
+                               f"(largest |ref| there {np.abs(bf16_value(r[bad])).max():.3e})")
+
+
+def cd_floor(P, scale):
+    """Absolute rounding floor of a float32-deviation sum over P parameters
+    whose values are at most `scale` in magnitude."""
+    return P * (4 * EPS32 * scale) ** 2
+
+
+def compare_cd(got, ref, floor=0.0):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape
+    for r in range(ref.shape[0]):
+        tol = CD_RTOL * np.abs(ref[r]).max() + floor
+        err = np.abs(got[r] - ref[r]).max()
+        assert err <= tol, f"consensus row {r}: error {err:.3e} > {tol:.3e} (ref max {np.abs(ref[r]).max():.3e})"
+
+
+def topo(spec, M, rounds, seed=0, step=0):
+    """Topology dict for a spec (see synth.configs.topology) plus test-only specs."""
+    name = spec[0]
+    if name == "matching":
+        rp, ci, masks = graphs.random_matching_masks(M, rounds, seed)
+        return dict(kind="csr", row_ptr=rp, col_idx=ci, weights=None, rounds=rounds, masks=masks,
+                    reweight="metropolis")
+    if name == "ring_self":
+        rp, ci, w = graphs.ring_weights(M)
+        masks = graphs.edge_drop_masks(rp, ci, rounds, spec[1], seed)
+        return dict(kind="csr", row_ptr=rp, col_idx=ci, weights=w, rounds=rounds, masks=masks, reweight="self")
+    if name == "er_mh":
+        rp, ci = graphs.random_symmetric_structure(M, spec[1], seed)
+        masks = graphs.edge_drop_masks(rp, ci, rounds, spec[2], seed + 1)
+        return dict(kind="csr", row_ptr=rp, col_idx=ci, weights=None, rounds=rounds, masks=masks,
+                    reweight="metropolis")
+    if name == "complete":
+        rp, ci, w = graphs.complete_weights(M)
+        return dict(kind="csr", row_ptr=rp, col_idx=ci, weights=w, rounds=rounds, masks=None, reweight="none")
+    return configs.topology(spec, M, rounds, seed, step)
+
+
+def run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd=True, lr=0.7, mu=0.9):
+    """One step on the GPU.  Inputs are numpy arrays; returns numpy copies of
+    (theta', v', cd or None)."""
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    if dtype == "f32":
+        g_tp = torch.from_numpy(tp).to(dev)
+        g_tl = torch.from_numpy(tl).to(dev)
+    else:
+        g_tp = torch.from_numpy(tp.view(np.int16)).to(dev).view(tdt)
+        g_tl = torch.from_numpy(tl.view(np.int16)).to(dev).view(tdt)
+    g_v = torch.from_numpy(v).to(dev)
+    eng = fgd.Engine(M, P, ld, dtype, lr, mu, device=0)
+    try:
+        eng.set_topology_dict("mix1", t1)
+        eng.set_topology_dict("mix2", t2)
+        cd = None
+        if with_cd:
+            cd = torch.full((eng.num_cd_rows(), M), float("nan"), dtype=torch.float64, device=dev)
+        eng.outer_step(g_tp, g_tl, g_v, cd)
+        torch.cuda.synchronize()
+    finally:
+        eng.close()
+    out_t = g_tp.cpu()
+    out_t = out_t.numpy() if dtype == "f32" else out_t.view(torch.int16).numpy().view(np.uint16)
+    return out_t, g_v.cpu().numpy(), (cd.cpu().numpy() if cd is not None else None)
+
+
+def aligned_ld(P):
+    """Smallest row stride >= P that keeps float32 and bf16 rows 16-byte aligned."""
+    return max(8, -(-P // 8) * 8)
+
+
+def run_case(fgd, torch, M, P, dtype, spec1, k1, spec2, k2, ld=None, seed=0, mom_std=1e-4, with_cd=True,
+             lr=0.7, mu=0.9):
+    ld = aligned_ld(P) if ld is None else ld
+    tp, tl, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, mom_std=mom_std, seed=seed)
+    t1 = topo(spec1, M, k1, seed)
+    t2 = topo(spec2, M, k2, seed + 7)
+    ref_t, ref_v, ref_cd = oracle.outer_step(tp, tl, v, oracle.Mix.from_topology(t1),
+                                             oracle.Mix.from_topology(t2), lr=lr, mu=mu, P=P, dtype=dtype)
+    got_t, got_v, got_cd = run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd, lr, mu)
+    scale = float(np.abs(tensors.bf16_bits_to_f32(tp) if dtype == "bf16" else tp).max()) if tp.size else 0.0
+    compare_outputs(dtype, got_t, ref_t, got_v, ref_v, P, scale)
+    # The padding beyond P is never written.
+    if ld > P:
+        assert np.array_equal(got_t[:, P:], tp[:, P:]) and np.array_equal(got_v[:, P:], v[:, P:])
+    if with_cd:
+        compare_cd(got_cd, theta_row_on_stored(ref_cd, got_t, P), cd_floor(P, scale))
+    return got_t, got_v, got_cd
+
+
+def theta_row_on_stored(ref_cd, got_t, P):
+    """The last consensus row is S_m of theta' as stored; its reference is the
+    oracle's S_m of the engine's stored theta' (theta' itself is compared
+    element by element separately)."""
+    ref = np.array(ref_cd, copy=True)
+    ref[-1] = oracle.consensus(got_t, P=P)
+    return ref

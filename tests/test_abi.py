@@ -1,0 +1,189 @@
+"""CPU tests of the C ABI: the library loads, exports every entry point the
+header declares, validates topologies, and computes the effective mixing
+weights bit for bit like the oracle.  No compute call needs a GPU here
+(engines are created host-only, device = -1).
+"""
+
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_22768_amd as fgd
+from synth import graphs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    with open(os.path.join(ROOT, "include", "fgd.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(fgd_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ["fgd_create", "fgd_set_topology", "fgd_outer_step", "fgd_consensus_distance", "fgd_destroy"]:
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", fgd.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = set(re.findall(r"\bT (fgd_\w+)", out.stdout))
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, f"declared but not exported: {missing}"
+    for n in declared_functions():
+        assert hasattr(fgd.lib, n)
+
+
+def test_status_strings():
+    assert fgd.fgd_status_string(0) == "FGD_OK"
+    assert fgd.fgd_status_string(2) == "FGD_ERR_TOPOLOGY"
+    assert fgd.fgd_status_string(99) == "FGD_UNKNOWN_STATUS"
+
+
+def _random_cases():
+    cases = []
+    for seed in range(40):
+        rng = np.random.default_rng(seed)
+        M = int(rng.integers(1, 17))
+        rp, ci = graphs.random_symmetric_structure(M, float(rng.uniform(0.1, 0.9)), seed)
+        mask = graphs.edge_drop_masks(rp, ci, 1, float(rng.uniform(0, 0.6)), seed)[0]
+        w = oracle.round_weights(rp, ci, None, None, "metropolis")  # a doubly-stochastic base W
+        cases.append((M, rp, ci, w, mask))
+    return cases
+
+
+@pytest.mark.parametrize("reweight", ["metropolis", "self"])
+def test_effective_weights_bit_exact_vs_oracle(reweight):
+    """Library and oracle implement the reweighting rules independently; the
+    float32 results must agree bit for bit."""
+    for M, rp, ci, w, mask in _random_cases():
+        a = fgd.fgd_effective_weights(M, rp, ci, w, mask, reweight)
+        b = oracle.round_weights(rp, ci, w, mask, reweight)
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), (M, reweight)
+
+
+def test_effective_weights_golden_cases():
+    import json
+    from fractions import Fraction
+
+    with open(os.path.join(ROOT, "tests", "golden", "metropolis_cases.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        rp, ci = graphs._csr_from_rows(c["rows"])
+        mask = graphs.masks_from_live_edges(rp, ci, [c["live"]])[0]
+        out = fgd.fgd_effective_weights(c["M"], rp, ci, None, mask, "metropolis")
+        for i in range(c["M"]):
+            for e in range(rp[i], rp[i + 1]):
+                assert out[e] == np.float32(float(Fraction(c["weights"][f"{i},{ci[e]}"]))), c["name"]
+
+
+def test_engine_rounds_match_oracle_and_upload_tables():
+    """A host-only engine stores per-round weights identical to the oracle's."""
+    M = 8
+    rp, ci = graphs.ring(M)
+    masks = graphs.edge_drop_masks(rp, ci, 3, 0.3, seed=5)
+    eng = fgd.Engine(M, 100, 104, "f32", device=-1)
+    eng.set_topology("mix2", "csr", rp, ci, None, 3, masks, "metropolis")
+    eng.set_topology("mix1", "global")
+    assert eng.num_cd_rows() == (3 + 1) + (1 + 1) + 1
+    for k in range(3):
+        a = eng.effective_weights("mix2", k)
+        b = oracle.round_weights(rp, ci, None, masks[k], "metropolis")
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert eng.min_bytes_per_step() == M * 100 * 20
+    eng.close()
+
+
+def test_host_only_engine_refuses_compute():
+    eng = fgd.Engine(4, 64, 64, "bf16", device=-1)
+    eng.set_topology("mix1", "global")
+    eng.set_topology("mix2", "identity")
+    assert eng.min_bytes_per_step() == 4 * 64 * 14
+    with pytest.raises(fgd.FgdError) as e:
+        fgd.fgd_outer_step(eng.handle, 256, 512, 1024, None, 0)
+    assert e.value.status == fgd.FGD_ERR_STATE
+    eng.close()
+
+
+@pytest.mark.parametrize("bad", ["decreasing", "unsorted", "no_diag", "out_of_range", "masked_diag",
+                                 "asym_mask", "mask_value", "masks_without_reweight", "not_doubly_stochastic",
+                                 "metropolis_directed", "negative_weight", "too_many_rounds", "no_weights"])
+def test_topology_rejections(bad):
+    M = 5
+    rp, ci, w = graphs.ring_weights(M)
+    rp, ci, w = rp.copy(), ci.copy(), w.copy()
+    masks, reweight, rounds = None, "none", 1
+    status = fgd.FGD_ERR_TOPOLOGY
+    if bad == "decreasing":
+        rp[2] = rp[3] + 1
+    elif bad == "unsorted":
+        ci[0], ci[1] = ci[1], ci[0]
+    elif bad == "no_diag":
+        rp, ci = graphs._csr_from_rows([[1, 4], [0, 1, 2], [1, 2, 3], [2, 3, 4], [0, 3, 4]])
+        w = np.full(len(ci), 0.5, np.float32)
+    elif bad == "out_of_range":
+        ci[-1] = M
+    elif bad == "masked_diag":
+        masks = np.ones((1, len(ci)), np.uint8)
+        masks[0, list(ci[rp[0]:rp[1]]).index(0)] = 0
+        reweight = "metropolis"
+    elif bad == "asym_mask":
+        masks = np.ones((1, len(ci)), np.uint8)
+        masks[0, rp[0] + list(ci[rp[0]:rp[1]]).index(1)] = 0  # (0,1) dropped but (1,0) live
+        reweight = "metropolis"
+    elif bad == "mask_value":
+        masks = np.full((1, len(ci)), 2, np.uint8)
+        reweight = "metropolis"
+    elif bad == "masks_without_reweight":
+        masks = graphs.edge_drop_masks(rp, ci, 1, 0.9, seed=0)
+    elif bad == "not_doubly_stochastic":
+        w[0] = 0.9
+    elif bad == "metropolis_directed":
+        rp, ci = graphs.exponential(M, hops=(1,))
+        w, reweight = None, "metropolis"
+    elif bad == "negative_weight":
+        w[1] = -w[1]
+    elif bad == "too_many_rounds":
+        rounds, status = fgd.FGD_MAX_ROUNDS + 1, fgd.FGD_ERR_INVALID_ARG
+    elif bad == "no_weights":
+        w, status = None, fgd.FGD_ERR_INVALID_ARG
+    eng = fgd.Engine(M, 16, 16, "f32", device=-1)
+    with pytest.raises(fgd.FgdError) as e:
+        eng.set_topology("mix2", "csr", rp, ci, w, rounds, masks, reweight)
+    assert e.value.status == status, (bad, str(e.value))
+    assert fgd.fgd_last_error()
+    eng.close()
+
+
+def test_directed_doubly_stochastic_graph_is_accepted():
+    """The directed exponential graph is doubly stochastic but not symmetric;
+    it is accepted with its given weights."""
+    rp, ci, w = graphs.exponential_weights(16)
+    eng = fgd.Engine(16, 16, 16, "f32", device=-1)
+    eng.set_topology("mix2", "csr", rp, ci, w, 2)
+    assert np.array_equal(eng.effective_weights("mix2", 1), w)
+    eng.close()
+
+
+@pytest.mark.parametrize("field,value", [("num_workers", 0), ("num_workers", 65), ("num_params", -1),
+                                         ("ld", 10), ("param_dtype", 7), ("ld", 102)])
+def test_create_rejections(field, value):
+    kw = dict(num_workers=4, num_params=100, ld=104, param_dtype="f32", device=-1)
+    kw[field] = value
+    with pytest.raises(fgd.FgdError) as e:
+        fgd.fgd_create(**kw)
+    assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+
+
+def test_zero_rounds_is_identity():
+    rp, ci, w = graphs.ring_weights(6)
+    eng = fgd.Engine(6, 8, 8, "f32", device=-1)
+    eng.set_topology("mix1", "csr", rp, ci, w, 0)
+    eng.set_topology("mix2", "global")
+    assert eng.num_cd_rows() == 2 + 1 + 1
+    eng.close()
