@@ -43,29 +43,35 @@ def _run(cmd):
     return r
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
-    """Compiles every source and links libfgd.so.  Always recompiles."""
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, jobs: int = 8, defines=(), out=None, build_dir=None) -> str:
+    """Compiles every source and links libfgd.so.  Always recompiles.
+
+    defines: extra -D tuning macros (defaults are the shipped values);
+    out / build_dir: where the library and objects go (default in-tree)."""
+    lib_path = out or LIB
+    bdir = build_dir or BUILD
+    os.makedirs(bdir, exist_ok=True)
+    extra = [f"-D{d}" for d in defines]
     hipcc = _hipcc()
     inc = ["-I", os.path.join(ROOT, "include")]
     cmds = []
     objs = []
     for s in HIP_SOURCES:
-        o = os.path.join(BUILD, s.replace(".", "_") + ".o")
-        cmds.append([hipcc, *HIP_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o])
+        o = os.path.join(bdir, s.replace(".", "_") + ".o")
+        cmds.append([hipcc, *HIP_FLAGS, *extra, *inc, "-c", os.path.join(CSRC, s), "-o", o])
         objs.append(o)
     for s in CXX_SOURCES:
-        o = os.path.join(BUILD, s.replace(".", "_") + ".o")
-        cmds.append(["g++", *CXX_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o])
+        o = os.path.join(bdir, s.replace(".", "_") + ".o")
+        cmds.append(["g++", *CXX_FLAGS, *extra, *inc, "-c", os.path.join(CSRC, s), "-o", o])
         objs.append(o)
     with ThreadPoolExecutor(max_workers=jobs) as ex:
         for r in ex.map(_run, cmds):
             if verbose and r.stderr.strip():
                 print(r.stderr, file=sys.stderr)
-    tmp = LIB + ".tmp"
+    tmp = lib_path + ".tmp"
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":

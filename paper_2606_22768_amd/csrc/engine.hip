@@ -45,7 +45,10 @@ int elem_size(int32_t dtype) { return dtype == FGD_BF16 ? 2 : 4; }
 // pinned host staging buffer and an event recorded after the last kernel
 // that read the slot, so a slot is refilled only once that kernel is done.
 constexpr int kTopoRing = 8;
-constexpr int kMaxBlocksPerCu = 8;
+#ifndef FGD_MAX_BLOCKS_PER_CU
+#define FGD_MAX_BLOCKS_PER_CU 8
+#endif
+constexpr int kMaxBlocksPerCu = FGD_MAX_BLOCKS_PER_CU;
 constexpr int kTimingPool = 4096;
 
 }  // namespace

@@ -75,30 +75,45 @@ constexpr int ilog2(int m) { return m <= 1 ? 0 : 1 + ilog2(m / 2); }
 
 // ------------------------------------------------------------ storage access
 
+// Streaming accesses carry the nontemporal hint unless FGD_NT is 0.
+#ifndef FGD_NT
+#define FGD_NT 1
+#endif
+template <class T>
+__device__ __forceinline__ T ld_stream(const T *p) {
+    if constexpr (FGD_NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+template <class T>
+__device__ __forceinline__ void st_stream(T v, T *p) {
+    if constexpr (FGD_NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
 // float32 storage, V in {1, 2, 4}.
 template <int V>
 struct F32Io {
     static constexpr int kElem = 4;
     __device__ static void load(const float *p, float (&o)[V]) {
         if constexpr (V == 4) {
-            f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(p));
+            f32x4 t = ld_stream(reinterpret_cast<const f32x4 *>(p));
             o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
         } else if constexpr (V == 2) {
-            f32x2 t = __builtin_nontemporal_load(reinterpret_cast<const f32x2 *>(p));
+            f32x2 t = ld_stream(reinterpret_cast<const f32x2 *>(p));
             o[0] = t.x; o[1] = t.y;
         } else {
-            o[0] = __builtin_nontemporal_load(p);
+            o[0] = ld_stream(p);
         }
     }
     __device__ static void store(float *p, const float (&i)[V]) {
         if constexpr (V == 4) {
             f32x4 t = {i[0], i[1], i[2], i[3]};
-            __builtin_nontemporal_store(t, reinterpret_cast<f32x4 *>(p));
+            st_stream(t, reinterpret_cast<f32x4 *>(p));
         } else if constexpr (V == 2) {
             f32x2 t = {i[0], i[1]};
-            __builtin_nontemporal_store(t, reinterpret_cast<f32x2 *>(p));
+            st_stream(t, reinterpret_cast<f32x2 *>(p));
         } else {
-            __builtin_nontemporal_store(i[0], p);
+            st_stream(i[0], p);
         }
     }
 };
@@ -155,25 +170,25 @@ struct ParamBF16 {
     __device__ static void load(const void *base, int64_t row, uint32_t lo, float (&o)[V]) {
         const uint16_t *p = static_cast<const uint16_t *>(base) + row + lo;
         if constexpr (V == 8) {
-            u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+            u32x4 t = ld_stream(reinterpret_cast<const u32x4 *>(p));
             uint32_t w[4] = {t.x, t.y, t.z, t.w};
 #pragma unroll
             for (int k = 0; k < 4; ++k) { o[2 * k] = bf16_lo(w[k]); o[2 * k + 1] = bf16_hi(w[k]); }
         } else if constexpr (V == 4) {
-            u32x2 t = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(p));
+            u32x2 t = ld_stream(reinterpret_cast<const u32x2 *>(p));
             o[0] = bf16_lo(t.x); o[1] = bf16_hi(t.x); o[2] = bf16_lo(t.y); o[3] = bf16_hi(t.y);
         } else if constexpr (V == 2) {
-            uint32_t t = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
+            uint32_t t = ld_stream(reinterpret_cast<const uint32_t *>(p));
             o[0] = bf16_lo(t); o[1] = bf16_hi(t);
         } else {
-            o[0] = __uint_as_float(static_cast<uint32_t>(__builtin_nontemporal_load(p)) << 16);
+            o[0] = __uint_as_float(static_cast<uint32_t>(ld_stream(p)) << 16);
         }
     }
     __device__ static void store(void *base, int64_t row, uint32_t lo, const float (&i)[V], float (&s)[V]) {
         uint16_t *p = static_cast<uint16_t *>(base) + row + lo;
         if constexpr (V == 1) {
             uint16_t h = to_bf16(i[0]);
-            __builtin_nontemporal_store(h, p);
+            st_stream(h, p);
             s[0] = __uint_as_float(static_cast<uint32_t>(h) << 16);
         } else {
             uint32_t w[V / 2];
@@ -185,12 +200,12 @@ struct ParamBF16 {
             }
             if constexpr (V == 8) {
                 u32x4 t = {w[0], w[1], w[2], w[3]};
-                __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(p));
+                st_stream(t, reinterpret_cast<u32x4 *>(p));
             } else if constexpr (V == 4) {
                 u32x2 t = {w[0], w[1]};
-                __builtin_nontemporal_store(t, reinterpret_cast<u32x2 *>(p));
+                st_stream(t, reinterpret_cast<u32x2 *>(p));
             } else {
-                __builtin_nontemporal_store(w[0], reinterpret_cast<uint32_t *>(p));
+                st_stream(w[0], reinterpret_cast<uint32_t *>(p));
             }
         }
     }
@@ -252,16 +267,15 @@ __device__ inline void row_mean(const float (&u)[MMAX][V], int M, float (&mean)[
     }
 }
 
-// Adds this lane-column's contribution to S_m(u) = sum_p (u_m - mean u)^2 into
-// the wave's double accumulators acc[m].  Workers are reduced in chunks of at
-// most 16 to bound register use.
+// Adds this lane-column's contribution to S_m(u) = sum_p (u_m - mean)^2 into
+// the wave's double accumulators acc[m], for a given per-element worker mean.
+// Workers are reduced in chunks of at most 16 to bound register use.
 template <int MMAX, bool EXACT, int V>
-__device__ inline void cd_accumulate(const float (&u)[MMAX][V], int M, double *acc, int lane) {
+__device__ inline void cd_accumulate_about(const float (&u)[MMAX][V], const float (&mean)[V], int M, double *acc,
+                                           int lane) {
     constexpr int MP = pow2_at_least(MMAX);
     constexpr int C = MP < 16 ? MP : 16;
     constexpr int kShift = 6 - ilog2(C);
-    float mean[V];
-    row_mean<MMAX, EXACT, V>(u, M, mean);
 #pragma unroll
     for (int c = 0; c < MP / C; ++c) {
         float part[C];
@@ -282,6 +296,14 @@ __device__ inline void cd_accumulate(const float (&u)[MMAX][V], int M, double *a
         const int m = c * C + (lane >> kShift);
         if ((lane & ((1 << kShift) - 1)) == 0 && m < M) acc[m] += static_cast<double>(tot);
     }
+}
+
+// S_m(u) contribution about the worker mean of u itself.
+template <int MMAX, bool EXACT, int V>
+__device__ inline void cd_accumulate(const float (&u)[MMAX][V], int M, double *acc, int lane) {
+    float mean[V];
+    row_mean<MMAX, EXACT, V>(u, M, mean);
+    cd_accumulate_about<MMAX, EXACT, V>(u, mean, M, acc, lane);
 }
 
 // ------------------------------------------------------------------ mixing
@@ -379,7 +401,129 @@ __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], f
 
 // Waves per SIMD the register allocator is asked to leave room for: enough
 // waves in flight to keep HBM busy while others mix.
-constexpr int waves_per_simd_target(int mmax) { return mmax <= 4 ? 4 : (mmax <= 8 ? 2 : 1); }
+#ifndef FGD_WAVES_M8
+#define FGD_WAVES_M8 2
+#endif
+constexpr int waves_per_simd_target(int mmax) { return mmax <= 4 ? 4 : (mmax <= 8 ? FGD_WAVES_M8 : 1); }
+
+// Per-tile state shared by the full-tile and ragged-tile paths.
+struct TileCtx {
+    float *rows;      // LDS rows (CSR mixes)
+    double *cd_acc;   // this wave's consensus accumulators, or nullptr
+    int M, tid, lane, n1, n2;
+};
+
+// One tile of kBlock * V parameters.  FULL: every lane's vector lies below P
+// (uniform; all tiles but the last), so no lane needs bounds logic.
+template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, bool FULL>
+__device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c, int64_t tb, uint32_t lo) {
+    constexpr int MP = pow2_at_least(MMAX);
+    constexpr int kCdStride = kWavesPerBlock * MP;  // doubles between consensus rows
+    const int M = c.M;
+    int nv = V;
+    if constexpr (!FULL) {
+        const int64_t rem = a.P - tb - lo;
+        nv = rem >= V ? V : (rem > 0 ? static_cast<int>(rem) : 0);
+    }
+
+    // Phase A: every row's loads are issued before the first use.  On the
+    // ragged tile a lane whose vector straddles P still loads the whole
+    // vector (the row's ld span covers it) and zeroes the elements at or
+    // beyond P; lanes entirely beyond P load nothing.
+    float u1[MMAX][V];  // theta_prev, then Mix1 output (unless global)
+    float u2[MMAX][V];  // theta_local, then g0, then Mix2 output (unless global)
+    if (FULL || nv > 0) {
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+            if (EXACT || m < M) {
+                PIO::load(a.theta_prev, m * a.ld + tb, lo, u1[m]);
+                PIO::load(a.theta_local, m * a.ld + tb, lo, u2[m]);
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            if ((EXACT || m < M) && (FULL || v < nv)) u2[m][v] = u1[m][v] - u2[m][v];
+            else { u1[m][v] = 0.0f; u2[m][v] = 0.0f; }
+        }
+    }
+
+    float xbar[V], gbar[V];
+    if (c.cd_acc) cd_accumulate<MMAX, EXACT, V>(u2, M, c.cd_acc, c.lane);
+    if constexpr (K1 == kGlobal) {
+        // The Mix1 output is the worker mean of theta_prev, which is also the
+        // mean the consensus row of theta_prev needs.
+        row_mean<MMAX, EXACT, V>(u1, M, xbar);
+        if (c.cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u1, xbar, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
+    } else {
+        if (c.cd_acc) cd_accumulate<MMAX, EXACT, V>(u1, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
+        mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, c.rows, c.tid,
+                                      c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane);
+    }
+    mix_apply<MMAX, EXACT, V, K2>(a.mix2, M, u2, gbar, c.rows, c.tid, c.cd_acc ? c.cd_acc + 1 * kCdStride : nullptr,
+                                  kCdStride, c.lane);
+
+    // Phase D: Nesterov (two-line form) and stores, a group of rows at a
+    // time.  The stored theta' replaces the row's dead input registers.
+    constexpr bool kStoreInU2 = K2 != kGlobal;
+    constexpr bool kStoreInU1 = !kStoreInU2 && K1 != kGlobal;
+    constexpr int kSep = (!kStoreInU2 && !kStoreInU1) ? MMAX : 1;
+    float sep[kSep][V];
+    constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
+    const float mu = a.mu, lr = a.lr;
+#pragma unroll
+    for (int m0 = 0; m0 < MMAX; m0 += G) {
+        float vm[G][V];
+        if (FULL || nv > 0) {
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                const int m = m0 + j;
+                if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(a.mom + (m * a.ld + tb) + lo, vm[j]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int m = m0 + j;
+            if (m >= MMAX) continue;
+            float stored[V];
+            if ((EXACT || m < M) && (FULL || nv > 0)) {
+                float t[V];
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    const float g = K2 == kGlobal ? gbar[e] : u2[m][e];
+                    const float x = K1 == kGlobal ? xbar[e] : u1[m][e];
+                    vm[j][e] = fmaf(mu, vm[j][e], g);
+                    t[e] = fmaf(-lr, fmaf(mu, vm[j][e], g), x);
+                }
+                const int64_t row = m * a.ld + tb;
+                if (FULL || nv == V) {
+                    F32Io<V>::store(a.mom + row + lo, vm[j]);
+                    PIO::store(a.theta_prev, row, lo, t, stored);
+                } else {
+                    tail_store(a.mom + row + lo, nv, vm[j]);
+                    PIO::store_part(a.theta_prev, row, lo, nv, t, stored);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < V; ++e) stored[e] = 0.0f;
+            }
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                if constexpr (kStoreInU2) u2[m][e] = stored[e];
+                else if constexpr (kStoreInU1) u1[m][e] = stored[e];
+                else sep[kSep == 1 ? 0 : m][e] = stored[e];
+            }
+        }
+    }
+    if (c.cd_acc) {
+        double *acc = c.cd_acc + (c.n2 + c.n1 + 2) * kCdStride;
+        if constexpr (kStoreInU2) cd_accumulate<MMAX, EXACT, V>(u2, M, acc, c.lane);
+        else if constexpr (kStoreInU1) cd_accumulate<MMAX, EXACT, V>(u1, M, acc, c.lane);
+        else cd_accumulate<MMAX, EXACT, V>(sep, M, acc, c.lane);
+    }
+}
 
 // K1, K2: compile-time kinds of Mix1 and Mix2 (kAny = decided at run time).
 template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2>
@@ -387,134 +531,45 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(waves_pe
 void outer_step_kernel(StepParams a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     constexpr int MP = pow2_at_least(MMAX);
-    constexpr int kCdStride = kWavesPerBlock * MP;  // doubles between consensus rows
-    const int M = EXACT ? MMAX : a.M;
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    constexpr int kCdStride = kWavesPerBlock * MP;
+    TileCtx c;
+    c.M = EXACT ? MMAX : a.M;
+    c.tid = threadIdx.x;
+    c.lane = c.tid & (kWave - 1);
+    const int wave = c.tid / kWave;
     const bool tables = (K1 == kTable || K2 == kTable) ||
                         ((K1 == kAny || K2 == kAny) && (a.mix1.kind == kTable || a.mix2.kind == kTable));
-    float *rows = reinterpret_cast<float *>(smem);
-    const int64_t rows_bytes = tables ? static_cast<int64_t>(M + 1) * kBlock * V * 4 : 0;
-    double *cd_acc = a.cd_partials ? reinterpret_cast<double *>(smem + rows_bytes) + wave * MP : nullptr;
-    const int n2 = a.mix2.kind == kTable ? a.mix2.rounds : (a.mix2.kind == kGlobal ? 1 : 0);
-    const int n1 = a.mix1.kind == kTable ? a.mix1.rounds : (a.mix1.kind == kGlobal ? 1 : 0);
+    c.rows = reinterpret_cast<float *>(smem);
+    const int64_t rows_bytes = tables ? static_cast<int64_t>(c.M + 1) * kBlock * V * 4 : 0;
+    c.cd_acc = a.cd_partials ? reinterpret_cast<double *>(smem + rows_bytes) + wave * MP : nullptr;
+    c.n2 = a.mix2.kind == kTable ? a.mix2.rounds : (a.mix2.kind == kGlobal ? 1 : 0);
+    c.n1 = a.mix1.kind == kTable ? a.mix1.rounds : (a.mix1.kind == kGlobal ? 1 : 0);
 
     if (tables) {
-        float *z = rows + (static_cast<int64_t>(M) * kBlock + tid) * V;
+        float *z = c.rows + (static_cast<int64_t>(c.M) * kBlock + c.tid) * V;
 #pragma unroll
         for (int v = 0; v < V; ++v) z[v] = 0.0f;
     }
-    if (cd_acc) {
-        for (int i = lane; i < a.n_cd * MP; i += kWave) cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
+    if (c.cd_acc) {
+        for (int i = c.lane; i < a.n_cd * MP; i += kWave) c.cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
     }
 
-    const uint32_t lo = static_cast<uint32_t>(tid) * V;  // lane offset inside a tile
+    const uint32_t lo = static_cast<uint32_t>(c.tid) * V;  // lane offset inside a tile
     for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
         const int64_t tb = tile * (kBlock * V);  // first parameter of the tile (uniform)
-        const int64_t rem = a.P - tb - lo;
-        const int nv = rem >= V ? V : (rem > 0 ? static_cast<int>(rem) : 0);
-
-        // Phase A: every row's loads are issued before the first use.  A lane
-        // whose vector straddles P still loads the whole vector (the row's ld
-        // span covers it) and zeroes the elements at or beyond P.
-        float u1[MMAX][V];  // theta_prev, then Mix1 output (unless global)
-        float u2[MMAX][V];  // theta_local, then g0, then Mix2 output (unless global)
-        if (nv > 0) {
-#pragma unroll
-            for (int m = 0; m < MMAX; ++m) {
-                if (EXACT || m < M) {
-                    PIO::load(a.theta_prev, m * a.ld + tb, lo, u1[m]);
-                    PIO::load(a.theta_local, m * a.ld + tb, lo, u2[m]);
-                }
-            }
-        }
-#pragma unroll
-        for (int m = 0; m < MMAX; ++m) {
-#pragma unroll
-            for (int v = 0; v < V; ++v) {
-                if ((EXACT || m < M) && v < nv) u2[m][v] = u1[m][v] - u2[m][v];
-                else { u1[m][v] = 0.0f; u2[m][v] = 0.0f; }
-            }
-        }
-        if (cd_acc) {
-            cd_accumulate<MMAX, EXACT, V>(u2, M, cd_acc, lane);
-            cd_accumulate<MMAX, EXACT, V>(u1, M, cd_acc + (n2 + 1) * kCdStride, lane);
-        }
-
-        float xbar[V], gbar[V];
-        mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, rows, tid, cd_acc ? cd_acc + (n2 + 2) * kCdStride : nullptr,
-                                      kCdStride, lane);
-        mix_apply<MMAX, EXACT, V, K2>(a.mix2, M, u2, gbar, rows, tid, cd_acc ? cd_acc + 1 * kCdStride : nullptr,
-                                      kCdStride, lane);
-
-        // Phase D: Nesterov (two-line form) and stores, a group of rows at a
-        // time.  The stored theta' replaces the row's dead input registers.
-        constexpr bool kStoreInU2 = K2 != kGlobal;
-        constexpr bool kStoreInU1 = !kStoreInU2 && K1 != kGlobal;
-        constexpr int kSep = (!kStoreInU2 && !kStoreInU1) ? MMAX : 1;
-        float sep[kSep][V];
-        constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
-        const float mu = a.mu, lr = a.lr;
-#pragma unroll
-        for (int m0 = 0; m0 < MMAX; m0 += G) {
-            float vm[G][V];
-            if (nv > 0) {
-#pragma unroll
-                for (int j = 0; j < G; ++j) {
-                    const int m = m0 + j;
-                    if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(a.mom + (m * a.ld + tb) + lo, vm[j]);
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < G; ++j) {
-                const int m = m0 + j;
-                if (m >= MMAX) continue;
-                float stored[V];
-                if ((EXACT || m < M) && nv > 0) {
-                    float t[V];
-#pragma unroll
-                    for (int e = 0; e < V; ++e) {
-                        const float g = K2 == kGlobal ? gbar[e] : u2[m][e];
-                        const float x = K1 == kGlobal ? xbar[e] : u1[m][e];
-                        vm[j][e] = fmaf(mu, vm[j][e], g);
-                        t[e] = fmaf(-lr, fmaf(mu, vm[j][e], g), x);
-                    }
-                    const int64_t row = m * a.ld + tb;
-                    if (nv == V) {
-                        F32Io<V>::store(a.mom + row + lo, vm[j]);
-                        PIO::store(a.theta_prev, row, lo, t, stored);
-                    } else {
-                        tail_store(a.mom + row + lo, nv, vm[j]);
-                        PIO::store_part(a.theta_prev, row, lo, nv, t, stored);
-                    }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < V; ++e) stored[e] = 0.0f;
-                }
-#pragma unroll
-                for (int e = 0; e < V; ++e) {
-                    if constexpr (kStoreInU2) u2[m][e] = stored[e];
-                    else if constexpr (kStoreInU1) u1[m][e] = stored[e];
-                    else sep[kSep == 1 ? 0 : m][e] = stored[e];
-                }
-            }
-        }
-        if (cd_acc) {
-            double *acc = cd_acc + (n2 + n1 + 2) * kCdStride;
-            if constexpr (kStoreInU2) cd_accumulate<MMAX, EXACT, V>(u2, M, acc, lane);
-            else if constexpr (kStoreInU1) cd_accumulate<MMAX, EXACT, V>(u1, M, acc, lane);
-            else cd_accumulate<MMAX, EXACT, V>(sep, M, acc, lane);
-        }
+        if (tb + kBlock * V <= a.P) step_tile<MMAX, EXACT, V, PIO, K1, K2, true>(a, c, tb, lo);
+        else step_tile<MMAX, EXACT, V, PIO, K1, K2, false>(a, c, tb, lo);
     }
 
-    if (cd_acc) {
+    if (c.cd_acc) {
         __syncthreads();
         const double *base = reinterpret_cast<const double *>(smem + rows_bytes);
-        for (int i = tid; i < a.n_cd * M; i += kBlock) {
-            const int r = i / M, m = i % M;
+        for (int i = c.tid; i < a.n_cd * c.M; i += kBlock) {
+            const int r = i / c.M, m = i % c.M;
             double s = 0.0;
 #pragma unroll
             for (int w = 0; w < kWavesPerBlock; ++w) s += base[r * kCdStride + w * MP + m];
-            a.cd_partials[(static_cast<int64_t>(blockIdx.x) * a.n_cd + r) * M + m] = s;
+            a.cd_partials[(static_cast<int64_t>(blockIdx.x) * a.n_cd + r) * c.M + m] = s;
         }
     }
 }
@@ -600,8 +655,16 @@ KernelSet make_kernel_set(int k1, int k2) {
 // Elements per lane per row: 16-byte float32 accesses up to 16 workers; bf16
 // parameters use 8-byte accesses (4 elements) so that momentum still moves in
 // 16-byte accesses and the register and LDS footprint per lane stays small.
-constexpr int lanes_v_f32(int mmax) { return mmax <= 16 ? 4 : (mmax == 32 ? 2 : 1); }
-constexpr int lanes_v_bf16(int mmax) { return mmax <= 16 ? 4 : (mmax == 32 ? 2 : 1); }
+#ifndef FGD_V_F32_M16
+#define FGD_V_F32_M16 4
+#endif
+#ifndef FGD_V_BF16_M8
+#define FGD_V_BF16_M8 4
+#endif
+constexpr int lanes_v_f32(int mmax) { return mmax <= 8 ? 4 : (mmax == 16 ? FGD_V_F32_M16 : (mmax == 32 ? 2 : 1)); }
+constexpr int lanes_v_bf16(int mmax) {
+    return mmax <= 8 ? FGD_V_BF16_M8 : (mmax == 16 ? 4 : (mmax == 32 ? 2 : 1));
+}
 
 // Defined per storage type.  k1, k2: Mix kinds (kIdentity, kGlobal, kTable);
 // a specialised step kernel is returned when one exists, else the one that
