@@ -1,0 +1,137 @@
+"""Full-size parity at the benchmark's launch configuration, for the four
+large workloads (8x150M f32, 16x500M f32, 8x1.1e9 bf16, 64x124M f32).
+
+Outputs are checked element by element against the oracle on sampled
+parameter columns (every column is independent given W, so the oracle run on
+the gathered columns is exact parity for them): the first and last columns
+(ragged end of the tiles) and seeded random ones.  The consensus rows, which
+the oracle cannot recompute at this size, are checked through properties that
+hold at any size:
+  - x^0 row = standalone consensus kernel on theta_prev before the step;
+  - g^0 row = standalone consensus kernel on theta_prev - theta_local
+    (formed by torch in float32, the same single rounding the kernel does);
+  - theta' row = standalone consensus kernel on the stored output;
+  - a global-mean round leaves an exactly zero row;
+  - each CSR round contracts: S(W u) <= sigma_2(W)^2 S(u), sigma_2 from the
+    round's effective weights (Sec. 3 contraction factor).
+"""
+
+import gc
+
+import numpy as np
+import pytest
+import scipy.sparse
+
+import oracle
+from synth import configs, tensors
+from tests import _parity as pa
+
+pytestmark = pytest.mark.gpu
+
+WORKLOADS = ["m8_p150m_f32", "m16_p500m_f32", "m8_p1100m_bf16", "m64_p124m_f32"]
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2606_22768_amd as fgd
+
+    return fgd, torch
+
+
+def _sample_columns(P, seed, n_edge=2048, n_random=8192):
+    rng = np.random.default_rng(seed)
+    cols = set(range(min(n_edge, P)))
+    cols |= set(range(max(0, P - n_edge), P))
+    cols |= set(rng.integers(0, P, n_random).tolist())
+    return np.array(sorted(cols), dtype=np.int64)
+
+
+def _host(t, dtype):
+    import torch
+
+    t = t.contiguous()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16) if dtype == "bf16" else t.cpu().numpy()
+
+
+def _sigma2(row_ptr, col_idx, w):
+    M = len(row_ptr) - 1
+    W = scipy.sparse.csr_matrix((np.asarray(w, np.float64), col_idx, row_ptr), shape=(M, M)).toarray()
+    s = np.linalg.svd(W, compute_uv=False)
+    return sorted(s)[-2]
+
+
+@pytest.mark.parametrize("workload", WORKLOADS)
+def test_fullsize_step(env, workload):
+    fgd, torch = env
+    w = configs.WORKLOADS[workload]
+    M, P, dtype = w["M"], w["P"], w["dtype"]
+    ld = pa.aligned_ld(P)
+    print(f"[fullsize] {workload}: generating inputs", flush=True)
+    tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
+                                     mom_std=w["mom_std"], seed=w["seed"], device="cuda")
+    cols = _sample_columns(P, w["seed"])
+    icol = torch.from_numpy(cols).cuda()
+    s_tp, s_tl, s_v = (_host(t.index_select(1, icol), d) for t, d in ((tp, dtype), (tl, dtype), (v, "f32")))
+
+    t1 = configs.topology(w["mix1"], M, w["k1"], w["seed"])
+    t2 = configs.topology(w["mix2"], M, w["k2"], w["seed"], step=0)
+    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0)
+    eng.set_topology_dict("mix1", t1)
+    eng.set_topology_dict("mix2", t2)
+    n_rows = eng.num_cd_rows()
+
+    # Standalone consensus of the inputs, by a different kernel.
+    cd_x0 = torch.zeros(M, dtype=torch.float64, device="cuda")
+    eng.consensus_distance(tp, cd_x0)
+    g0 = tp[:, :P].float() - tl[:, :P].float()
+    g0_full = torch.zeros((M, ld), dtype=torch.float32, device="cuda")
+    g0_full[:, :P] = g0
+    del g0
+    cd_g0 = torch.zeros(M, dtype=torch.float64, device="cuda")
+    eng.consensus_distance(g0_full, cd_g0, dtype="f32")
+    torch.cuda.synchronize()
+    del g0_full
+    gc.collect()
+    torch.cuda.empty_cache()
+
+    print(f"[fullsize] {workload}: step", flush=True)
+    cd = torch.full((n_rows, M), float("nan"), dtype=torch.float64, device="cuda")
+    eng.outer_step(tp, tl, v, cd)
+    cd_out = torch.zeros(M, dtype=torch.float64, device="cuda")
+    eng.consensus_distance(tp, cd_out)
+    torch.cuda.synchronize()
+    got_t = _host(tp.index_select(1, icol), dtype)
+    got_v = _host(v.index_select(1, icol), "f32")
+    cd = cd.cpu().numpy()
+
+    # Element-by-element parity on the sampled columns.
+    ref_t, ref_v, _ = oracle.outer_step(s_tp, s_tl, s_v, oracle.Mix.from_topology(t1), oracle.Mix.from_topology(t2),
+                                        lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=dtype)
+    scale = float(np.abs(tensors.bf16_bits_to_f32(s_tp) if dtype == "bf16" else s_tp).max())
+    pa.compare_outputs(dtype, got_t, ref_t, got_v, ref_v, len(cols), scale)
+
+    # Consensus rows.
+    k2 = 1 if t2["kind"] == "global" else t2["rounds"]
+    k1 = 1 if t1["kind"] == "global" else t1["rounds"]
+    assert n_rows == k2 + k1 + 3
+    np.testing.assert_allclose(cd[0], cd_g0.cpu().numpy(), rtol=1e-9)
+    np.testing.assert_allclose(cd[k2 + 1], cd_x0.cpu().numpy(), rtol=1e-9)
+    np.testing.assert_allclose(cd[-1], cd_out.cpu().numpy(), rtol=1e-9)
+    for t, first in ((t2, 0), (t1, k2 + 1)):
+        K = 1 if t["kind"] == "global" else t["rounds"]
+        for k in range(K):
+            before, after = cd[first + k].sum(), cd[first + k + 1].sum()
+            if t["kind"] == "global":
+                assert np.all(cd[first + k + 1] == 0.0)
+                continue
+            which = "mix2" if t is t2 else "mix1"
+            s2 = _sigma2(t["row_ptr"], t["col_idx"], eng.effective_weights(which, k))
+            assert after <= s2 ** 2 * before * (1 + 1e-5), (workload, which, k, after / before, s2 ** 2)
+    print(f"[fullsize] {workload}: ok, consensus rows {np.round(cd.mean(axis=1), 6).tolist()}", flush=True)
+    eng.close()
+    del tp, tl, v, cd_x0, cd_g0, cd_out
+    gc.collect()
+    torch.cuda.empty_cache()
