@@ -376,8 +376,10 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
 
     fgd::StepParams p{};
     p.theta_prev = theta_prev;
+    p.theta_out = theta_prev;
     p.theta_local = theta_local;
     p.mom = momentum;
+    p.mom_out = momentum;
     p.P = c.num_params;
     p.ld = c.ld;
     p.ntiles = tiles_of(c.num_params, ks.v);
@@ -390,7 +392,9 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     p.mix1 = mix_dev(e->slot[0], t1);
     p.mix2 = mix_dev(e->slot[1], t2);
     const bool tables = e->slot[0].kind == 2 || e->slot[1].kind == 2;
-    size_t lds = tables ? static_cast<size_t>(c.num_workers + 1) * fgd::kBlock * ks.v * sizeof(float) : 0;
+    const bool padded = (e->slot[0].kind == 2 && e->slot[0].padded) || (e->slot[1].kind == 2 && e->slot[1].padded);
+    p.lds_rows = tables ? c.num_workers + (padded ? 1 : 0) : 0;
+    size_t lds = static_cast<size_t>(p.lds_rows) * fgd::kBlock * ks.v * sizeof(float);
     if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
 
     int grid = 0;

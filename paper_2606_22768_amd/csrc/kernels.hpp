@@ -5,25 +5,28 @@
 // rows.  Every parameter index p is independent given W, so one lane owns V
 // consecutive parameters of *all* M workers and keeps them in registers:
 //
-//   phase A  load theta_prev and theta_local rows (16-byte nontemporal loads
-//            where V allows), g0 = theta_prev - theta_local
+//   phase A  load theta_prev and theta_local rows (nontemporal buffer loads,
+//            16 bytes per lane where V allows), g0 = theta_prev - theta_local
 //   mix      Mix2 on g and Mix1 on x = theta_prev: a global mean in registers,
-//            or CSR rounds.  A CSR round needs u[col] for a run-time col, so
-//            the lane parks its M values in its own column of an LDS array
-//            [M+1][block][V] (row M is all zero and pads short rows) and
-//            gathers neighbours from there.  Each lane touches only its own
-//            column, so no barrier is needed.  Per round the host supplies a
-//            padded table [width][M] of (column, weight): the d-th live entry
-//            of every row, in ascending column order, so the sum runs in the
-//            same order as the CSR row.
+//            or CSR rounds.  A CSR round needs u[col] for a run-time col that
+//            is the same for the whole wave, so the lane parks its M values
+//            in its own column of an LDS array [M][block][V] (plus a zero
+//            row M when some table pads a short row) and gathers from there
+//            (no barrier: a lane touches only its own column).
+//            Per round the host supplies a padded table [width][M] of
+//            (column, weight): the d-th live entry of every row, in ascending
+//            column order, so the sum runs in the CSR row's order.
 //   phase D  load momentum rows, v' = mu v + g, theta' = x - lr (g + mu v'),
 //            store theta' (RNE to bf16 for bf16 storage) and v'.
 //   CD       S_m(u) = sum_p (u_m - mean_n u_n)^2 for every intermediate u
 //            (Sec. 4.4; Appendix D.1): float32 deviations, a reduce-scatter
-//            across the wave's lanes, double accumulation per (row, worker)
-//            in LDS, per-block partials and a fixed-order finalize kernel, so
-//            results are deterministic.
+//            across the wave's lanes (cross-row lane swaps, then DPP),
+//            double accumulation per (row, worker) in LDS, per-block partials
+//            and a fixed-order finalize kernel, so results are deterministic.
 //
+// Global memory is addressed through buffer descriptors: each row's address
+// is formed in scalar registers and every lane adds one 32-bit byte offset,
+// so a lane needs a single address register however many rows it streams.
 // No matrix cores: the work is a sparse weighted reduction across rows.
 #pragma once
 
@@ -37,6 +40,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr int kBlock = 256;
 constexpr int kWave = 64;
@@ -53,12 +57,19 @@ struct MixDev {
 };
 
 struct StepParams {
-    void *theta_prev;         // [M][ld] storage type, in/out
+    const void *theta_prev;   // [M][ld] storage type, read
+    void *theta_out;          // the same array, written (a separate argument so the
+                              // row descriptors of the loads and of the stores are
+                              // formed independently and none stays live across the tile)
     const void *theta_local;  // [M][ld] storage type
-    float *mom;               // [M][ld] float32, in/out
+    const float *mom;         // [M][ld] float32, read
+    float *mom_out;           // the same array, written (separate for the same reason)
     double *cd_partials;      // [gridDim.x][n_cd][M] or nullptr
     int64_t P, ld, ntiles;
     int32_t M, n_cd;
+    int32_t lds_rows;         // rows of the LDS gather array: 0 (no CSR mix), M, or M + 1
+                              // when some table pads a short row (row M is then zero)
+    int32_t pad_;
     float lr, mu;
     MixDev mix1, mix2;
 };
@@ -73,84 +84,85 @@ struct ConsensusParams {
 constexpr int pow2_at_least(int m) { return m <= 1 ? 1 : 2 * pow2_at_least((m + 1) / 2); }
 constexpr int ilog2(int m) { return m <= 1 ? 0 : 1 + ilog2(m / 2); }
 
+// ------------------------------------------------------------ tuning knobs
+// Defaults are the shipped configuration; variants are built with -D.
+
+#ifndef FGD_NT
+#define FGD_NT 1  // nontemporal hint on the streaming accesses
+#endif
+#ifndef FGD_WAVES_M8
+#define FGD_WAVES_M8 2  // occupancy hint for up to 8 workers
+#endif
+#ifndef FGD_V_F32_M16
+#define FGD_V_F32_M16 4  // float32 parameters per lane at 16 workers
+#endif
+#ifndef FGD_V_BF16_M8
+#define FGD_V_BF16_M8 4  // bf16 parameters per lane up to 8 workers
+#endif
+
 // ------------------------------------------------------------ storage access
 
-// Streaming accesses carry the nontemporal hint unless FGD_NT is 0.
-#ifndef FGD_NT
-#define FGD_NT 1
-#endif
-template <class T>
-__device__ __forceinline__ T ld_stream(const T *p) {
-    if constexpr (FGD_NT) return __builtin_nontemporal_load(p);
-    else return *p;
-}
-template <class T>
-__device__ __forceinline__ void st_stream(T v, T *p) {
-    if constexpr (FGD_NT) __builtin_nontemporal_store(v, p);
-    else *p = v;
+constexpr int kCachePolicy = FGD_NT ? 2 : 0;  // buffer-instruction cache bits: nontemporal
+constexpr int kRawBufferFlags = 0x00020000;   // raw (untyped) buffer descriptor, dword 3
+
+// Descriptor of the row that starts `elem` elements (of `es` bytes) past
+// `base`.  Offsets used with it stay far below the 2^31-byte record count.
+__device__ __forceinline__ rsrc_t row_rsrc(const void *base, int64_t elem, int es) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(static_cast<const char *>(base)) + elem * es,
+                                             static_cast<short>(0), 0x7fffffff, kRawBufferFlags);
 }
 
-// float32 storage, V in {1, 2, 4}.
+// float32 values, V in {1, 2, 4}; `off` is the lane's byte offset in the row.
 template <int V>
 struct F32Io {
-    static constexpr int kElem = 4;
-    __device__ static void load(const float *p, float (&o)[V]) {
+    __device__ static void load(rsrc_t r, uint32_t off, float (&o)[V]) {
         if constexpr (V == 4) {
-            f32x4 t = ld_stream(reinterpret_cast<const f32x4 *>(p));
-            o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
+            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCachePolicy);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = __uint_as_float(t[v]);
         } else if constexpr (V == 2) {
-            f32x2 t = ld_stream(reinterpret_cast<const f32x2 *>(p));
-            o[0] = t.x; o[1] = t.y;
+            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCachePolicy);
+            o[0] = __uint_as_float(t[0]);
+            o[1] = __uint_as_float(t[1]);
         } else {
-            o[0] = ld_stream(p);
+            o[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCachePolicy));
         }
     }
-    __device__ static void store(float *p, const float (&i)[V]) {
+    __device__ static void store(rsrc_t r, uint32_t off, const float (&i)[V]) {
         if constexpr (V == 4) {
-            f32x4 t = {i[0], i[1], i[2], i[3]};
-            st_stream(t, reinterpret_cast<f32x4 *>(p));
+            const u32x4 t = {__float_as_uint(i[0]), __float_as_uint(i[1]), __float_as_uint(i[2]), __float_as_uint(i[3])};
+            __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kCachePolicy);
         } else if constexpr (V == 2) {
-            f32x2 t = {i[0], i[1]};
-            st_stream(t, reinterpret_cast<f32x2 *>(p));
+            const u32x2 t = {__float_as_uint(i[0]), __float_as_uint(i[1])};
+            __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kCachePolicy);
         } else {
-            st_stream(i[0], p);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(i[0]), r, off, 0, kCachePolicy);
         }
+    }
+    // Writes only the first n < V values (ragged end of a row).
+    __device__ static void store_part(rsrc_t r, uint32_t off, int n, const float (&i)[V]) {
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            if (v < n) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(i[v]), r, off + 4 * v, 0, kCachePolicy);
     }
 };
 
-// Elementwise store of the first n < V values (ragged tail of a row).
-template <int V>
-__device__ inline void tail_store(float *p, int n, const float (&i)[V]) {
-#pragma unroll
-    for (int v = 0; v < V; ++v)
-        if (v < n) p[v] = i[v];
-}
-
-// Parameter storage: float32 or bf16 bit patterns.  load/store of a full
-// vector of V elements at element index row + lo of `base`, where `row` is
-// wave-uniform (row start plus tile start, kept in scalar registers) and `lo`
-// the lane's offset inside the tile; store_part writes only the first n < V
-// elements (ragged tail of a row).
+// Parameter storage: float32 (ParamF32) or bf16 bit patterns (ParamBF16).
+// store() writes the values in the storage type and returns, in `s`, what
+// was stored, widened back to float.
 template <int V>
 struct ParamF32 {
     static constexpr int kElem = 4;
-    __device__ static void load(const void *base, int64_t row, uint32_t lo, float (&o)[V]) {
-        F32Io<V>::load(static_cast<const float *>(base) + row + lo, o);
-    }
-    // Stores and returns the stored values in `s`.
-    __device__ static void store(void *base, int64_t row, uint32_t lo, const float (&i)[V], float (&s)[V]) {
-        F32Io<V>::store(static_cast<float *>(base) + row + lo, i);
+    __device__ static void load(rsrc_t r, uint32_t off, float (&o)[V]) { F32Io<V>::load(r, off, o); }
+    __device__ static void store(rsrc_t r, uint32_t off, const float (&i)[V], float (&s)[V]) {
+        F32Io<V>::store(r, off, i);
 #pragma unroll
         for (int v = 0; v < V; ++v) s[v] = i[v];
     }
-    __device__ static void store_part(void *base, int64_t row, uint32_t lo, int n, const float (&i)[V],
-                                      float (&s)[V]) {
-        float *p = static_cast<float *>(base) + row + lo;
+    __device__ static void store_part(rsrc_t r, uint32_t off, int n, const float (&i)[V], float (&s)[V]) {
+        F32Io<V>::store_part(r, off, n, i);
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-            if (v < n) p[v] = i[v];
-            s[v] = v < n ? i[v] : 0.0f;
-        }
+        for (int v = 0; v < V; ++v) s[v] = v < n ? i[v] : 0.0f;
     }
 };
 
@@ -161,35 +173,31 @@ __device__ inline uint32_t pack_bf16(float a, float b) {
     f32x2 f = {a, b};
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
-__device__ inline uint16_t to_bf16(float a) { return static_cast<uint16_t>(pack_bf16(a, 0.0f) & 0xFFFFu); }
 
-// bf16 storage, V in {1, 2, 4, 8}.
 template <int V>
 struct ParamBF16 {
     static constexpr int kElem = 2;
-    __device__ static void load(const void *base, int64_t row, uint32_t lo, float (&o)[V]) {
-        const uint16_t *p = static_cast<const uint16_t *>(base) + row + lo;
+    __device__ static void load(rsrc_t r, uint32_t off, float (&o)[V]) {
         if constexpr (V == 8) {
-            u32x4 t = ld_stream(reinterpret_cast<const u32x4 *>(p));
-            uint32_t w[4] = {t.x, t.y, t.z, t.w};
+            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCachePolicy);
 #pragma unroll
-            for (int k = 0; k < 4; ++k) { o[2 * k] = bf16_lo(w[k]); o[2 * k + 1] = bf16_hi(w[k]); }
+            for (int k = 0; k < 4; ++k) { o[2 * k] = bf16_lo(t[k]); o[2 * k + 1] = bf16_hi(t[k]); }
         } else if constexpr (V == 4) {
-            u32x2 t = ld_stream(reinterpret_cast<const u32x2 *>(p));
-            o[0] = bf16_lo(t.x); o[1] = bf16_hi(t.x); o[2] = bf16_lo(t.y); o[3] = bf16_hi(t.y);
+            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCachePolicy);
+            o[0] = bf16_lo(t[0]); o[1] = bf16_hi(t[0]); o[2] = bf16_lo(t[1]); o[3] = bf16_hi(t[1]);
         } else if constexpr (V == 2) {
-            uint32_t t = ld_stream(reinterpret_cast<const uint32_t *>(p));
+            const uint32_t t = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCachePolicy);
             o[0] = bf16_lo(t); o[1] = bf16_hi(t);
         } else {
-            o[0] = __uint_as_float(static_cast<uint32_t>(ld_stream(p)) << 16);
+            const uint16_t t = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kCachePolicy);
+            o[0] = __uint_as_float(static_cast<uint32_t>(t) << 16);
         }
     }
-    __device__ static void store(void *base, int64_t row, uint32_t lo, const float (&i)[V], float (&s)[V]) {
-        uint16_t *p = static_cast<uint16_t *>(base) + row + lo;
+    __device__ static void store(rsrc_t r, uint32_t off, const float (&i)[V], float (&s)[V]) {
         if constexpr (V == 1) {
-            uint16_t h = to_bf16(i[0]);
-            st_stream(h, p);
-            s[0] = __uint_as_float(static_cast<uint32_t>(h) << 16);
+            const uint32_t w = pack_bf16(i[0], 0.0f);
+            __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(w & 0xFFFFu), r, off, 0, kCachePolicy);
+            s[0] = bf16_lo(w);
         } else {
             uint32_t w[V / 2];
 #pragma unroll
@@ -199,58 +207,105 @@ struct ParamBF16 {
                 s[2 * k + 1] = bf16_hi(w[k]);
             }
             if constexpr (V == 8) {
-                u32x4 t = {w[0], w[1], w[2], w[3]};
-                st_stream(t, reinterpret_cast<u32x4 *>(p));
+                const u32x4 t = {w[0], w[1], w[2], w[3]};
+                __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kCachePolicy);
             } else if constexpr (V == 4) {
-                u32x2 t = {w[0], w[1]};
-                st_stream(t, reinterpret_cast<u32x2 *>(p));
+                const u32x2 t = {w[0], w[1]};
+                __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kCachePolicy);
             } else {
-                st_stream(w[0], reinterpret_cast<uint32_t *>(p));
+                __builtin_amdgcn_raw_buffer_store_b32(w[0], r, off, 0, kCachePolicy);
             }
         }
     }
-    __device__ static void store_part(void *base, int64_t row, uint32_t lo, int n, const float (&i)[V],
-                                      float (&s)[V]) {
-        uint16_t *p = static_cast<uint16_t *>(base) + row + lo;
+    __device__ static void store_part(rsrc_t r, uint32_t off, int n, const float (&i)[V], float (&s)[V]) {
 #pragma unroll
         for (int v = 0; v < V; ++v) {
-            uint16_t h = to_bf16(i[v]);
-            if (v < n) p[v] = h;
-            s[v] = v < n ? __uint_as_float(static_cast<uint32_t>(h) << 16) : 0.0f;
+            const uint32_t w = pack_bf16(i[v], 0.0f);
+            if (v < n) __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(w & 0xFFFFu), r, off + 2 * v, 0,
+                                                             kCachePolicy);
+            s[v] = v < n ? bf16_lo(w) : 0.0f;
         }
     }
 };
 
 // ------------------------------------------------------- consensus pieces
 
+// Cross-lane moves used by the reduce-scatter.  swap32 / swap16 exchange the
+// upper half of `a` with the lower half of `b` across the two 32-lane halves
+// (v_permlane32_swap) or across adjacent 16-lane rows (v_permlane16_swap).
+__device__ __forceinline__ void swap32(float &a, float &b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void swap16(float &a, float &b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+}
+// DPP lane permutations inside a 16-lane row; each pairs lanes whose bit
+// 3, 2, 1 or 0 differs and keeps the higher bits.
+constexpr int kDppRowMirror = 0x140;      // l <-> 15 - l
+constexpr int kDppRowHalfMirror = 0x141;  // l <-> 7 - l inside each 8
+constexpr int kDppQuadXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppQuadXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// One step of the reduce-scatter on lane bit B: with n values left, lanes
+// whose bit B is clear keep the lower n/2 values and lanes whose bit is set
+// keep the upper n/2, each summed with its partner's copy; with one value
+// left it is a plain all-reduce step.
+template <int B, int C>
+__device__ __forceinline__ void rs_step(float (&part)[C], int &n, int lane) {
+    constexpr int ctrl = B == 3 ? kDppRowMirror : (B == 2 ? kDppRowHalfMirror : (B == 1 ? kDppQuadXor2 : kDppQuadXor1));
+    if (n > 1) {
+        n >>= 1;
+#pragma unroll
+        for (int i = 0; i < C / 2; ++i) {
+            if (i < n) {
+                // Read both values first: a select between two array lvalues
+                // would index the register array dynamically.
+                float lower_half = part[i], upper_half = part[i + n];
+                if constexpr (B == 5 || B == 4) {
+                    if constexpr (B == 5) swap32(lower_half, upper_half);
+                    else swap16(lower_half, upper_half);
+                    part[i] = lower_half + upper_half;
+                } else {
+                    const bool upper = (lane >> B) & 1;
+                    const float send = upper ? lower_half : upper_half;
+                    const float keep = upper ? upper_half : lower_half;
+                    part[i] = keep + dpp<ctrl>(send);
+                }
+            }
+        }
+    } else {
+        if constexpr (B == 5 || B == 4) {
+            float a = part[0], b = part[0];
+            if constexpr (B == 5) swap32(a, b);
+            else swap16(a, b);
+            part[0] = a + b;
+        } else {
+            part[0] += dpp<ctrl>(part[0]);
+        }
+    }
+}
+
 // Sum over the wave of part[j] for every j < C, scattered so that lane l ends
 // up with the total of j = l >> (6 - log2 C) (every lane of that group of
-// 64 / C lanes holds it).  Halving steps swap half of the remaining values
-// with the partner lane (lane ^ s) and add; the rest is a butterfly.  The
-// order of additions is fixed, so results are deterministic.
+// 64 / C lanes holds it).  The order of additions is fixed, so results are
+// deterministic.  Needs all 64 lanes active.
 template <int C>
 __device__ inline float wave_reduce_scatter(float (&part)[C], int lane) {
     int n = C;
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) {
-        if (n > 1) {
-            n >>= 1;
-            const bool upper = (lane & s) != 0;
-#pragma unroll
-            for (int i = 0; i < C / 2; ++i) {
-                if (i < n) {
-                    // Read both values first: a select between two array
-                    // lvalues would index the register array dynamically.
-                    const float lower_half = part[i], upper_half = part[i + n];
-                    const float send = upper ? lower_half : upper_half;
-                    const float keep = upper ? upper_half : lower_half;
-                    part[i] = keep + __shfl_xor(send, s);
-                }
-            }
-        } else {
-            part[0] += __shfl_xor(part[0], s);
-        }
-    }
+    rs_step<5>(part, n, lane);
+    rs_step<4>(part, n, lane);
+    rs_step<3>(part, n, lane);
+    rs_step<2>(part, n, lane);
+    rs_step<1>(part, n, lane);
+    rs_step<0>(part, n, lane);
     return part[0];
 }
 
@@ -316,11 +371,11 @@ constexpr int kAny = 3;
 // scalar registers, shared by the wave.
 typedef const __attribute__((address_space(4))) int32_t *const_table_ptr;
 
-// One table round applied in place: u_m <- sum_d w[d][m] * u_{col[d][m]}.
-// The lane parks u in its column of the LDS rows, then gathers from there.
+// One table round applied in place, u_m <- sum_d w[d][m] * u_{col[d][m]},
+// gathering through the lane's LDS column.
 template <int MMAX, bool EXACT, int V>
-__device__ inline void table_round(const_table_ptr tab, int width, int M, float (&u)[MMAX][V], float *rows,
-                                   int tid) {
+__device__ inline void table_round_lds(const_table_ptr tab, int width, int M, float (&u)[MMAX][V], float *rows,
+                                       int tid) {
     const int Mr = EXACT ? MMAX : M;
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
@@ -367,20 +422,26 @@ __device__ inline void table_round(const_table_ptr tab, int width, int M, float 
     }
 }
 
-// Applies one Mix slot.  For a global mean the result is written to `mean`
-// only (KIND == kGlobal) or to every row (KIND == kAny).  cd_acc: the wave's
-// accumulators of the slot's first round-output row (nullptr: no consensus);
-// consecutive rounds use consecutive rows, `cd_stride` doubles apart.
+template <int MMAX, bool EXACT, int V>
+__device__ __forceinline__ void table_round(const_table_ptr tab, int width, int M, float (&u)[MMAX][V], float *rows,
+                                            int tid) {
+    table_round_lds<MMAX, EXACT, V>(tab, width, M, u, rows, tid);
+}
+
+// Applies one Mix slot to u.  `mean` holds the worker mean of u on entry.
+// A global mean leaves the result in `mean` (KIND == kGlobal) or in every row
+// (KIND == kAny).  cd_acc: the wave's accumulators of the slot's first
+// round-output row (nullptr: no consensus); consecutive rounds use
+// consecutive rows, `cd_stride` doubles apart.  A doubly-stochastic W keeps
+// the worker mean (Sec. 3), so every round's consensus row is taken about
+// the input mean.
 template <int MMAX, bool EXACT, int V, int KIND>
-__device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], float (&mean)[V], float *rows,
+__device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], const float (&mean)[V], float *rows,
                                  int tid, double *cd_acc, int cd_stride, int lane) {
-    if constexpr (KIND == kIdentity) {
+    if constexpr (KIND == kIdentity || KIND == kGlobal) {
         return;
-    } else if constexpr (KIND == kGlobal) {
-        row_mean<MMAX, EXACT, V>(u, M, mean);
     } else {
         if (KIND == kAny && mx.kind == kGlobal) {
-            row_mean<MMAX, EXACT, V>(u, M, mean);
 #pragma unroll
             for (int m = 0; m < MMAX; ++m)
 #pragma unroll
@@ -392,7 +453,7 @@ __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], f
         for (int k = 0; k < mx.rounds; ++k) {
             const_table_ptr tab = (const_table_ptr)(mx.table) + 2 * static_cast<int64_t>(k) * mx.width * Mr;
             table_round<MMAX, EXACT, V>(tab, mx.width, M, u, rows, tid);
-            if (cd_acc) cd_accumulate<MMAX, EXACT, V>(u, M, cd_acc + k * cd_stride, lane);
+            if (cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u, mean, M, cd_acc + k * cd_stride, lane);
         }
     }
 }
@@ -401,14 +462,11 @@ __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], f
 
 // Waves per SIMD the register allocator is asked to leave room for: enough
 // waves in flight to keep HBM busy while others mix.
-#ifndef FGD_WAVES_M8
-#define FGD_WAVES_M8 2
-#endif
 constexpr int waves_per_simd_target(int mmax) { return mmax <= 4 ? 4 : (mmax <= 8 ? FGD_WAVES_M8 : 1); }
 
 // Per-tile state shared by the full-tile and ragged-tile paths.
 struct TileCtx {
-    float *rows;      // LDS rows (CSR mixes)
+    float *rows;      // LDS rows (CSR mixes gathered through LDS)
     double *cd_acc;   // this wave's consensus accumulators, or nullptr
     int M, tid, lane, n1, n2;
 };
@@ -419,12 +477,14 @@ template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, bool FULL>
 __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c, int64_t tb, uint32_t lo) {
     constexpr int MP = pow2_at_least(MMAX);
     constexpr int kCdStride = kWavesPerBlock * MP;  // doubles between consensus rows
+    constexpr int kE = PIO::kElem;
     const int M = c.M;
     int nv = V;
     if constexpr (!FULL) {
         const int64_t rem = a.P - tb - lo;
         nv = rem >= V ? V : (rem > 0 ? static_cast<int>(rem) : 0);
     }
+    const uint32_t off_p = lo * kE, off_v = lo * 4;  // lane byte offsets in parameter / momentum rows
 
     // Phase A: every row's loads are issued before the first use.  On the
     // ragged tile a lane whose vector straddles P still loads the whole
@@ -436,8 +496,8 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
 #pragma unroll
         for (int m = 0; m < MMAX; ++m) {
             if (EXACT || m < M) {
-                PIO::load(a.theta_prev, m * a.ld + tb, lo, u1[m]);
-                PIO::load(a.theta_local, m * a.ld + tb, lo, u2[m]);
+                PIO::load(row_rsrc(a.theta_prev, m * a.ld + tb, kE), off_p, u1[m]);
+                PIO::load(row_rsrc(a.theta_local, m * a.ld + tb, kE), off_p, u2[m]);
             }
         }
     }
@@ -450,18 +510,17 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
         }
     }
 
+    // Worker means of the mix inputs: the global-mean outputs themselves and
+    // the centres of every consensus row of the slot.
     float xbar[V], gbar[V];
-    if (c.cd_acc) cd_accumulate<MMAX, EXACT, V>(u2, M, c.cd_acc, c.lane);
-    if constexpr (K1 == kGlobal) {
-        // The Mix1 output is the worker mean of theta_prev, which is also the
-        // mean the consensus row of theta_prev needs.
-        row_mean<MMAX, EXACT, V>(u1, M, xbar);
-        if (c.cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u1, xbar, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
-    } else {
-        if (c.cd_acc) cd_accumulate<MMAX, EXACT, V>(u1, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
-        mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, c.rows, c.tid,
-                                      c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane);
+    row_mean<MMAX, EXACT, V>(u2, M, gbar);
+    row_mean<MMAX, EXACT, V>(u1, M, xbar);
+    if (c.cd_acc) {
+        cd_accumulate_about<MMAX, EXACT, V>(u2, gbar, M, c.cd_acc, c.lane);
+        cd_accumulate_about<MMAX, EXACT, V>(u1, xbar, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
     }
+    mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, c.rows, c.tid,
+                                  c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane);
     mix_apply<MMAX, EXACT, V, K2>(a.mix2, M, u2, gbar, c.rows, c.tid, c.cd_acc ? c.cd_acc + 1 * kCdStride : nullptr,
                                   kCdStride, c.lane);
 
@@ -480,7 +539,7 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
 #pragma unroll
             for (int j = 0; j < G; ++j) {
                 const int m = m0 + j;
-                if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(a.mom + (m * a.ld + tb) + lo, vm[j]);
+                if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[j]);
             }
         }
 #pragma unroll
@@ -497,13 +556,14 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
                     vm[j][e] = fmaf(mu, vm[j][e], g);
                     t[e] = fmaf(-lr, fmaf(mu, vm[j][e], g), x);
                 }
-                const int64_t row = m * a.ld + tb;
+                const rsrc_t rv = row_rsrc(a.mom_out, m * a.ld + tb, 4);
+                const rsrc_t rp = row_rsrc(a.theta_out, m * a.ld + tb, kE);
                 if (FULL || nv == V) {
-                    F32Io<V>::store(a.mom + row + lo, vm[j]);
-                    PIO::store(a.theta_prev, row, lo, t, stored);
+                    F32Io<V>::store(rv, off_v, vm[j]);
+                    PIO::store(rp, off_p, t, stored);
                 } else {
-                    tail_store(a.mom + row + lo, nv, vm[j]);
-                    PIO::store_part(a.theta_prev, row, lo, nv, t, stored);
+                    F32Io<V>::store_part(rv, off_v, nv, vm[j]);
+                    PIO::store_part(rp, off_p, nv, t, stored);
                 }
             } else {
 #pragma unroll
@@ -537,15 +597,13 @@ void outer_step_kernel(StepParams a) {
     c.tid = threadIdx.x;
     c.lane = c.tid & (kWave - 1);
     const int wave = c.tid / kWave;
-    const bool tables = (K1 == kTable || K2 == kTable) ||
-                        ((K1 == kAny || K2 == kAny) && (a.mix1.kind == kTable || a.mix2.kind == kTable));
     c.rows = reinterpret_cast<float *>(smem);
-    const int64_t rows_bytes = tables ? static_cast<int64_t>(c.M + 1) * kBlock * V * 4 : 0;
+    const int64_t rows_bytes = static_cast<int64_t>(a.lds_rows) * kBlock * V * 4;
     c.cd_acc = a.cd_partials ? reinterpret_cast<double *>(smem + rows_bytes) + wave * MP : nullptr;
     c.n2 = a.mix2.kind == kTable ? a.mix2.rounds : (a.mix2.kind == kGlobal ? 1 : 0);
     c.n1 = a.mix1.kind == kTable ? a.mix1.rounds : (a.mix1.kind == kGlobal ? 1 : 0);
 
-    if (tables) {
+    if (a.lds_rows > c.M) {
         float *z = c.rows + (static_cast<int64_t>(c.M) * kBlock + c.tid) * V;
 #pragma unroll
         for (int v = 0; v < V; ++v) z[v] = 0.0f;
@@ -554,7 +612,7 @@ void outer_step_kernel(StepParams a) {
         for (int i = c.lane; i < a.n_cd * MP; i += kWave) c.cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
     }
 
-    const uint32_t lo = static_cast<uint32_t>(c.tid) * V;  // lane offset inside a tile
+    const uint32_t lo = static_cast<uint32_t>(c.tid) * V;  // lane offset inside a tile, in elements
     for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
         const int64_t tb = tile * (kBlock * V);  // first parameter of the tile (uniform)
         if (tb + kBlock * V <= a.P) step_tile<MMAX, EXACT, V, PIO, K1, K2, true>(a, c, tb, lo);
@@ -579,6 +637,7 @@ void outer_step_kernel(StepParams a) {
 template <int MMAX, bool EXACT, int V, class PIO>
 __global__ __launch_bounds__(kBlock) void consensus_kernel(ConsensusParams a) {
     constexpr int MP = pow2_at_least(MMAX);
+    constexpr int kE = PIO::kElem;
     __shared__ double acc[kWavesPerBlock * MP];
     const int M = EXACT ? MMAX : a.M;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -593,7 +652,7 @@ __global__ __launch_bounds__(kBlock) void consensus_kernel(ConsensusParams a) {
         if (nv > 0) {
 #pragma unroll
             for (int m = 0; m < MMAX; ++m)
-                if (EXACT || m < M) PIO::load(a.x, m * a.ld + tb, lo, u[m]);
+                if (EXACT || m < M) PIO::load(row_rsrc(a.x, m * a.ld + tb, kE), lo * kE, u[m]);
         }
 #pragma unroll
         for (int m = 0; m < MMAX; ++m)
@@ -652,15 +711,9 @@ KernelSet make_kernel_set(int k1, int k2) {
     return ks;
 }
 
-// Elements per lane per row: 16-byte float32 accesses up to 16 workers; bf16
+// Elements per lane per row: 16-byte float32 accesses up to 8 workers; bf16
 // parameters use 8-byte accesses (4 elements) so that momentum still moves in
 // 16-byte accesses and the register and LDS footprint per lane stays small.
-#ifndef FGD_V_F32_M16
-#define FGD_V_F32_M16 4
-#endif
-#ifndef FGD_V_BF16_M8
-#define FGD_V_BF16_M8 4
-#endif
 constexpr int lanes_v_f32(int mmax) { return mmax <= 8 ? 4 : (mmax == 16 ? FGD_V_F32_M16 : (mmax == 32 ? 2 : 1)); }
 constexpr int lanes_v_bf16(int mmax) {
     return mmax <= 8 ? FGD_V_BF16_M8 : (mmax == 16 ? 4 : (mmax == 32 ? 2 : 1));

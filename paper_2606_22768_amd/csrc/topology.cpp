@@ -267,6 +267,16 @@ TopoStatus build_mix_topology(int32_t M, int32_t kind, const int32_t *row_ptr, c
             }
         }
     }
+    for (int32_t k = 0; k < rounds && !t.padded; ++k) {
+        for (int32_t i = 0; i < M; ++i) {
+            int32_t nlive = 0;
+            for (int32_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) nlive += t.live[static_cast<size_t>(k) * nnz + e];
+            if (nlive < t.width) {
+                t.padded = true;
+                break;
+            }
+        }
+    }
     out = std::move(t);
     return TopoStatus::ok;
 }

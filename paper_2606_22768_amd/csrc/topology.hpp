@@ -26,6 +26,7 @@ struct MixTopology {
     std::vector<float> eff;            // [rounds][nnz], 0 where dropped
     std::vector<uint8_t> live;         // [rounds][nnz]
     int32_t width = 0;                 // max live entries of a row over all rounds
+    bool padded = false;               // some row of some round has fewer than `width` live entries
 
     // Rounds of this slot as the kernel counts them (global mean = 1).
     int32_t effective_rounds() const { return kind == 0 ? 0 : (kind == 1 ? 1 : rounds); }
