@@ -44,6 +44,11 @@ class _Mix(ctypes.Structure):
                 ("reweight", ctypes.c_int32)]
 
 
+class _Opts(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("mu", ctypes.c_float), ("nesterov", ctypes.c_int32),
+                ("mix1_state", ctypes.c_int32), ("n_seg", ctypes.c_int32), ("seg", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -66,8 +71,8 @@ def lib():
         L.fgdo_outer_step.restype = ctypes.c_int
         L.fgdo_outer_step.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                      ctypes.POINTER(_Mix), ctypes.POINTER(_Mix), ctypes.c_float,
-                                      ctypes.c_float, ctypes.c_void_p]
+                                      ctypes.POINTER(_Mix), ctypes.POINTER(_Mix), ctypes.POINTER(_Opts),
+                                      ctypes.c_void_p]
         L.fgdo_consensus.restype = ctypes.c_int
         L.fgdo_consensus.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                      ctypes.c_void_p, ctypes.c_void_p]
@@ -141,10 +146,22 @@ def num_cd(mix1: Mix, mix2: Mix) -> int:
     return mix2.effective_rounds() + 1 + mix1.effective_rounds() + 1 + 1
 
 
-def outer_step(theta_prev, theta_local, mom, mix1: Mix, mix2: Mix, lr=0.7, mu=0.9, P=None, dtype=None):
+def subset_array(segments):
+    """[n][2] int64 array of half-open Mix2 subset segments (None: no subset)."""
+    if segments is None:
+        return None
+    return np.ascontiguousarray(np.asarray(segments, dtype=np.int64).reshape(-1, 2))
+
+
+def outer_step(theta_prev, theta_local, mom, mix1: Mix, mix2: Mix, lr=0.7, mu=0.9, P=None, dtype=None,
+               nesterov=True, mix1_state=False, subset=None):
     """One outer step.  Inputs are numpy [M][ld] arrays (float32, or uint16 bf16
     bits for the parameter tensors).  Returns new copies
-    (theta_prev', mom', cd[n_cd, M]); the inputs are left untouched."""
+    (theta_prev', mom', cd[n_cd, M]); the inputs are left untouched.
+
+    nesterov: Nesterov (App. B two-line form) or plain momentum.
+    mix1_state: Mix1 also mixes the momentum (App. B, GlobalM1S).
+    subset: Mix2 acts only on these [begin, end) parameter segments."""
     tp = np.array(theta_prev, copy=True, order="C")
     tl = np.ascontiguousarray(theta_local)
     v = np.array(mom, dtype=np.float32, copy=True, order="C")
@@ -157,8 +174,11 @@ def outer_step(theta_prev, theta_local, mom, mix1: Mix, mix2: Mix, lr=0.7, mu=0.
     P = ld if P is None else P
     cd = np.zeros((num_cd(mix1, mix2), M), dtype=np.float64)
     c1, c2 = mix1.c(), mix2.c()
+    seg = subset_array(subset)
+    opts = _Opts(float(lr), float(mu), 1 if nesterov else 0, 1 if mix1_state else 0,
+                 0 if seg is None else seg.shape[0], _ptr(seg))
     rc = lib().fgdo_outer_step(M, P, ld, 1 if dtype == "bf16" else 0, _ptr(tp), _ptr(tl), _ptr(v),
-                               ctypes.byref(c1), ctypes.byref(c2), float(lr), float(mu), _ptr(cd))
+                               ctypes.byref(c1), ctypes.byref(c2), ctypes.byref(opts), _ptr(cd))
     if rc:
         raise ValueError(f"oracle outer step failed (rc={rc})")
     return tp, v, cd

@@ -19,7 +19,16 @@
  *   3. Mix1 of the previous outer parameters, K1 rounds, or the exact global
  *      mean (same operator; global averaging is W = 11^T / M).
  *   4. Nesterov outer update in the two-line implementation form of
- *      Appendix B: v' = mu v + g;  theta' = x - lr (g + mu v').
+ *      Appendix B: v' = mu v + g;  theta' = x - lr (g + mu v').  With
+ *      Nesterov off, the plain momentum form of the same optimizer:
+ *      v' = mu v + g;  theta' = x - lr v'.
+ *      Variants (Appendix B, GlobalM1S; Sec. 4.1 and Appendix C, the
+ *      Mix2-subset configuration):
+ *        - mix1_state: Mix1 is also applied to the momentum v (the outer
+ *          optimizer state) before the momentum update.
+ *        - Mix2 subset: Mix2 acts only on the parameter indices inside a
+ *          list of half-open segments [begin, end); elsewhere it is the
+ *          identity, in every round.
  *   5. Consensus distance S_m(u) = sum_p (u_m - mean_n u_n)^2 for every
  *      intermediate u (Sec. 4.4 L2 consensus distance; Appendix D.1 uses the
  *      mean of the squared norms, Sec. 4.4 the mean of the norms; both follow
@@ -52,6 +61,16 @@
 enum { FGDO_OK = 0, FGDO_BAD_ARG = -1, FGDO_NO_MEM = -2 };
 enum { FGDO_IDENTITY = 0, FGDO_GLOBAL = 1, FGDO_CSR = 2 };
 enum { FGDO_RW_NONE = 0, FGDO_RW_METROPOLIS = 1, FGDO_RW_SELF = 2 };
+
+/* Outer-optimizer settings and step variants. */
+typedef struct {
+    float lr;              /* outer learning rate gamma */
+    float mu;              /* momentum */
+    int32_t nesterov;      /* 1: Nesterov form, 0: plain momentum */
+    int32_t mix1_state;    /* 1: Mix1 also mixes the momentum before its update */
+    int32_t n_seg;         /* Mix2 subset segments (0: Mix2 acts on every index) */
+    const int64_t *seg;    /* [n_seg][2] half-open [begin, end), ascending, disjoint */
+} fgdo_opts;
 
 typedef struct {
     int32_t kind;           /* FGDO_IDENTITY, FGDO_GLOBAL or FGDO_CSR */
@@ -263,7 +282,21 @@ static int check_mix(int32_t M, const fgdo_mix *mx)
 /* Applies all rounds of one Mix to src (double [M][P]) into dst.  cd, when
  * not NULL, receives S_m of the input and of every round's output:
  * [(rounds_eff + 1) * M].  Returns FGDO_OK or an error. */
-int fgdo_mix_apply(int32_t M, int64_t P, const fgdo_mix *mx, const double *src, double *dst, double *cd)
+/* Puts back the input value at every index outside the subset: there the
+ * Mix is the identity, in every round. */
+static void restore_outside(int32_t M, int64_t P, const uint8_t *inset, const double *src, double *dst)
+{
+    if (!inset) return;
+    for (int32_t m = 0; m < M; ++m)
+        for (int64_t p = 0; p < P; ++p)
+            if (!inset[p]) dst[(int64_t)m * P + p] = src[(int64_t)m * P + p];
+}
+
+/* One Mix slot on src [M][P] into dst, with consensus rows cd[(K+1)][M]
+ * (input, then every round's output; NULL: none).  inset[P] (NULL: every
+ * index) marks the indices the Mix acts on. */
+int fgdo_mix_apply_subset(int32_t M, int64_t P, const fgdo_mix *mx, const uint8_t *inset, const double *src,
+                          double *dst, double *cd)
 {
     if (M <= 0 || P < 0 || !src || !dst) return FGDO_BAD_ARG;
     int rc = check_mix(M, mx);
@@ -277,6 +310,7 @@ int fgdo_mix_apply(int32_t M, int64_t P, const fgdo_mix *mx, const double *src, 
     if (!tmp) return FGDO_NO_MEM;
     if (mx->kind == FGDO_GLOBAL) {
         mix_global(M, P, dst, tmp);
+        restore_outside(M, P, inset, src, tmp);
         memcpy(dst, tmp, (size_t)n * sizeof(double));
         if (cd) consensus_sq(M, P, dst, cd + M);
         free(tmp);
@@ -293,6 +327,7 @@ int fgdo_mix_apply(int32_t M, int64_t P, const fgdo_mix *mx, const double *src, 
         rc = fgdo_round_weights(M, mx->row_ptr, mx->col_idx, mx->weights, mask, mx->reweight, w);
         if (rc) break;
         mix_csr_round(M, P, mx->row_ptr, mx->col_idx, w, mask, dst, tmp);
+        restore_outside(M, P, inset, src, tmp);
         memcpy(dst, tmp, (size_t)n * sizeof(double));
         if (cd) consensus_sq(M, P, dst, cd + (int64_t)(k + 1) * M);
     }
@@ -301,8 +336,11 @@ int fgdo_mix_apply(int32_t M, int64_t P, const fgdo_mix *mx, const double *src, 
     return rc;
 }
 
-/* Number of consensus-distance rows the outer step reports:
- * g^0..g^K2, x^0..x^K1, theta'. */
+int fgdo_mix_apply(int32_t M, int64_t P, const fgdo_mix *mx, const double *src, double *dst, double *cd)
+{
+    return fgdo_mix_apply_subset(M, P, mx, NULL, src, dst, cd);
+}
+
 int fgdo_num_cd(const fgdo_mix *mix1, const fgdo_mix *mix2)
 {
     return effective_rounds(mix2) + 1 + effective_rounds(mix1) + 1 + 1;
@@ -316,12 +354,28 @@ int fgdo_num_cd(const fgdo_mix *mix1, const fgdo_mix *mix2)
  *   mom         [M][ld] float32, in/out
  *   cd          [fgdo_num_cd * M] double or NULL
  */
+/* Index flags of a Mix2 subset: 1 inside some segment.  Segments must be
+ * ascending, disjoint, non-empty and inside [0, P). */
+static int subset_flags(int64_t P, int32_t n_seg, const int64_t *seg, uint8_t *inset)
+{
+    if (n_seg < 0 || (n_seg > 0 && !seg)) return FGDO_BAD_ARG;
+    memset(inset, 0, (size_t)(P > 0 ? P : 1));
+    int64_t prev_end = 0;
+    for (int32_t i = 0; i < n_seg; ++i) {
+        int64_t b = seg[2 * i], e = seg[2 * i + 1];
+        if (b < prev_end || e <= b || e > P) return FGDO_BAD_ARG;
+        for (int64_t p = b; p < e; ++p) inset[p] = 1;
+        prev_end = e;
+    }
+    return FGDO_OK;
+}
+
 int fgdo_outer_step(int32_t M, int64_t P, int64_t ld, int32_t dtype, void *theta_prev,
                     const void *theta_local, float *mom, const fgdo_mix *mix1, const fgdo_mix *mix2,
-                    float lr, float mu, double *cd)
+                    const fgdo_opts *opt, double *cd)
 {
     if (M <= 0 || P < 0 || ld < P || (dtype != 0 && dtype != 1)) return FGDO_BAD_ARG;
-    if (!theta_prev || !theta_local || !mom) return FGDO_BAD_ARG;
+    if (!theta_prev || !theta_local || !mom || !opt) return FGDO_BAD_ARG;
     if (check_mix(M, mix1) || check_mix(M, mix2)) return FGDO_BAD_ARG;
     int64_t n = (int64_t)M * P;
     size_t bytes = (size_t)(n > 0 ? n : 1) * sizeof(double);
@@ -329,14 +383,21 @@ int fgdo_outer_step(int32_t M, int64_t P, int64_t ld, int32_t dtype, void *theta
     double *ghat = (double *)malloc(bytes);
     double *x0 = (double *)malloc(bytes);
     double *x = (double *)malloc(bytes);
+    double *v0 = (double *)malloc(bytes);
+    double *v = (double *)malloc(bytes);
     double *theta_new = (double *)malloc(bytes);
+    uint8_t *inset = opt->n_seg > 0 ? (uint8_t *)malloc((size_t)(P > 0 ? P : 1)) : NULL;
     int K2 = effective_rounds(mix2), K1 = effective_rounds(mix1);
     double *cd2 = (double *)malloc((size_t)(K2 + 1) * M * sizeof(double));
     double *cd1 = (double *)malloc((size_t)(K1 + 1) * M * sizeof(double));
     int rc = FGDO_OK;
-    if (!g0 || !ghat || !x0 || !x || !theta_new || !cd2 || !cd1) {
+    if (!g0 || !ghat || !x0 || !x || !v0 || !v || !theta_new || !cd2 || !cd1 || (opt->n_seg > 0 && !inset)) {
         rc = FGDO_NO_MEM;
         goto done;
+    }
+    if (inset) {
+        rc = subset_flags(P, opt->n_seg, opt->seg, inset);
+        if (rc) goto done;
     }
 
     /* 1. Outer gradient g0 = theta_prev - theta_local (negated paper Delta). */
@@ -346,25 +407,31 @@ int fgdo_outer_step(int32_t M, int64_t P, int64_t ld, int32_t dtype, void *theta
             double tl = load_param(theta_local, dtype, (int64_t)m * ld + p);
             x0[(int64_t)m * P + p] = tp;
             g0[(int64_t)m * P + p] = tp - tl;
+            v0[(int64_t)m * P + p] = (double)mom[(int64_t)m * ld + p];
         }
 
-    /* 2. Mix2 on the outer gradient (blocking mix). */
-    rc = fgdo_mix_apply(M, P, mix2, g0, ghat, cd2);
+    /* 2. Mix2 on the outer gradient (blocking mix), on the subset if any. */
+    rc = fgdo_mix_apply_subset(M, P, mix2, inset, g0, ghat, cd2);
     if (rc) goto done;
 
-    /* 3. Mix1 on the previous outer parameters (non-blocking mix). */
+    /* 3. Mix1 on the previous outer parameters (non-blocking mix), and on
+     *    the momentum too when the optimizer state is mixed. */
     rc = fgdo_mix_apply(M, P, mix1, x0, x, cd1);
     if (rc) goto done;
+    if (opt->mix1_state) rc = fgdo_mix_apply(M, P, mix1, v0, v, NULL);
+    else memcpy(v, v0, bytes);
+    if (rc) goto done;
 
-    /* 4. Nesterov, two-line form: v' = mu v + g ; theta' = x - lr (g + mu v'). */
+    /* 4. Outer optimizer.  Nesterov, two-line form: v' = mu v + g ;
+     *    theta' = x - lr (g + mu v').  Plain momentum: theta' = x - lr v'. */
     {
-        double dmu = (double)mu, dlr = (double)lr;
+        double dmu = (double)opt->mu, dlr = (double)opt->lr;
         for (int32_t m = 0; m < M; ++m)
             for (int64_t p = 0; p < P; ++p) {
                 int64_t i = (int64_t)m * P + p, j = (int64_t)m * ld + p;
                 double g = ghat[i];
-                double v_new = dmu * (double)mom[j] + g;
-                double t_new = x[i] - dlr * (g + dmu * v_new);
+                double v_new = dmu * v[i] + g;
+                double t_new = opt->nesterov ? x[i] - dlr * (g + dmu * v_new) : x[i] - dlr * v_new;
                 mom[j] = (float)v_new;
                 store_param(theta_prev, dtype, j, t_new);
                 theta_new[i] = load_param(theta_prev, dtype, j); /* as stored */
@@ -383,7 +450,10 @@ done:
     free(ghat);
     free(x0);
     free(x);
+    free(v0);
+    free(v);
     free(theta_new);
+    free(inset);
     free(cd2);
     free(cd1);
     return rc;

@@ -1,0 +1,209 @@
+"""Pins for the oracle's step variants, each against something other than the
+oracle itself (torch's optimizer, scipy dense products, brute-force sums):
+
+  - plain momentum (the optimizer with Nesterov off);
+  - Mix1 also applied to the outer-optimizer state (Appendix B, GlobalM1S and
+    GlobalM1SLocalM2 in the further-ablations table);
+  - Mix2 restricted to a subset of parameter segments (Sec. 4.1 and Appendix
+    C, the GlobalM1LocalM2-subset configuration; identity elsewhere).
+
+Runs on the CPU only.
+"""
+
+import numpy as np
+import pytest
+import scipy.sparse
+import torch
+
+import oracle
+from synth import graphs, tensors
+
+LR, MU = np.float32(0.7), np.float32(0.9)
+
+
+def dense_W(row_ptr, col_idx, w):
+    M = len(row_ptr) - 1
+    return scipy.sparse.csr_matrix((np.asarray(w, np.float64), col_idx, row_ptr), shape=(M, M)).toarray()
+
+
+def torch_sgd(param, grad, buf, nesterov):
+    """One torch.optim.SGD step (float64) with a preloaded momentum buffer."""
+    p = torch.nn.Parameter(torch.from_numpy(np.array(param, np.float64)))
+    opt = torch.optim.SGD([p], lr=float(LR), momentum=float(MU), nesterov=nesterov)
+    p.grad = torch.from_numpy(np.array(grad, np.float64))
+    opt.state[p]["momentum_buffer"] = torch.from_numpy(np.array(buf, np.float64)).clone()
+    opt.step()
+    return p.detach().numpy(), opt.state[p]["momentum_buffer"].numpy()
+
+
+def close(got, want, ulps=2):
+    np.testing.assert_allclose(got, want, rtol=0, atol=np.abs(want).max() * ulps * 2.0 ** -24 + 1e-30)
+
+
+# ------------------------------------------------------------ plain momentum
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_plain_momentum_m1_matches_torch_sgd(dtype):
+    """M = 1, Nesterov off: torch's SGD with momentum (no Nesterov), gradient
+    theta_prev - theta_local, buffer preloaded with v."""
+    P = 3001
+    tp, tl, v = tensors.numpy_inputs(1, P, dtype=dtype, mom_std=1e-4, seed=21)
+    out_t, out_v, _ = oracle.outer_step(tp, tl, v, oracle.Mix("identity"), oracle.Mix("identity"), lr=LR, mu=MU,
+                                        nesterov=False)
+    f = tensors.bf16_bits_to_f32 if dtype == "bf16" else (lambda a: a)
+    want_t, want_v = torch_sgd(f(tp[0]), f(tp[0]).astype(np.float64) - f(tl[0]), v[0], nesterov=False)
+    close(out_v[0], want_v)
+    if dtype == "bf16":
+        want_bits = np.array([oracle.bf16_from_double(x) for x in want_t], dtype=np.uint16)
+        # Double rounding aside (torch rounds nothing here), the stored value is
+        # the nearest bf16 of the double result.
+        assert np.array_equal(out_t[0], want_bits)
+    else:
+        close(out_t[0], want_t)
+
+
+def test_plain_momentum_diloco_reduction():
+    """Equal theta_prev and v everywhere, global Mix2, Nesterov off: every
+    worker takes torch's momentum-SGD step on the mean outer gradient."""
+    M, P = 6, 513
+    rng = np.random.default_rng(4)
+    base = (rng.standard_normal(P) * 0.02).astype(np.float32)
+    tp = np.tile(base, (M, 1))
+    tl = (tp + rng.standard_normal((M, P)).astype(np.float32) * np.float32(1e-3)).astype(np.float32)
+    vb = (rng.standard_normal(P) * 1e-4).astype(np.float32)
+    out_t, out_v, cd = oracle.outer_step(tp, tl, np.tile(vb, (M, 1)), oracle.Mix("global"), oracle.Mix("global"),
+                                         lr=LR, mu=MU, nesterov=False)
+    gbar = (tp.astype(np.float64) - tl.astype(np.float64)).mean(axis=0)
+    want_t, want_v = torch_sgd(base, gbar, vb, nesterov=False)
+    for m in range(M):
+        close(out_t[m], want_t, ulps=4)
+        close(out_v[m], want_v, ulps=4)
+    assert np.all(cd[-1] == 0.0)
+
+
+def test_plain_momentum_differs_from_nesterov_by_closed_form():
+    """Both forms from the same inputs with a ring Mix2: x - lr (g + mu v')
+    (Nesterov) and x - lr v' (plain), g and v' built from a dense scipy
+    product; the momentum update itself is common to both forms."""
+    M, P = 3, 400
+    tp, tl, v = tensors.numpy_inputs(M, P, mom_std=1e-3, seed=8)
+    m2 = oracle.Mix("csr", *graphs.ring_weights(M), rounds=1)
+    tn, vn, _ = oracle.outer_step(tp, tl, v, oracle.Mix("identity"), m2, lr=LR, mu=MU, nesterov=True)
+    tq, vq, _ = oracle.outer_step(tp, tl, v, oracle.Mix("identity"), m2, lr=LR, mu=MU, nesterov=False)
+    assert np.array_equal(vn, vq)  # the momentum update does not depend on the form
+    W = dense_W(*graphs.ring_weights(M))
+    g = W @ (tp.astype(np.float64) - tl.astype(np.float64))
+    vnew = float(MU) * v.astype(np.float64) + g
+    close(tn, tp - float(LR) * (g + float(MU) * vnew), ulps=4)
+    close(tq, tp - float(LR) * vnew, ulps=4)
+
+
+# ------------------------------------------------------ Mix1 over the state
+
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_global_state_mix_matches_torch_on_mean_buffer(nesterov):
+    """GlobalM1S with ring Mix2 (GlobalM1SLocalM2): worker m's result is
+    torch's SGD step from the worker-mean parameters with gradient (W2 g0)_m
+    and the momentum buffer preloaded with the worker mean of v."""
+    M, P = 8, 700
+    tp, tl, v = tensors.numpy_inputs(M, P, mom_std=1e-3, seed=13)
+    rp, ci, w = graphs.ring_weights(M)
+    out_t, out_v, _ = oracle.outer_step(tp, tl, v, oracle.Mix("global"), oracle.Mix("csr", rp, ci, w, rounds=1),
+                                        lr=LR, mu=MU, nesterov=nesterov, mix1_state=True)
+    W2 = dense_W(rp, ci, w)
+    g = W2 @ (tp.astype(np.float64) - tl.astype(np.float64))
+    xbar = tp.astype(np.float64).mean(axis=0)
+    vbar = v.astype(np.float64).mean(axis=0)
+    for m in range(M):
+        want_t, want_v = torch_sgd(xbar, g[m], vbar, nesterov)
+        close(out_t[m], want_t, ulps=4)
+        close(out_v[m], want_v, ulps=4)
+
+
+def test_csr_state_mix_matches_dense_products():
+    """Mix1 over a CSR W1 (two rounds, directed exponential graph) applied to
+    both theta_prev and v: worker m steps from (W1^2 theta)_m with buffer
+    (W1^2 v)_m, via torch's SGD."""
+    M, P = 16, 300
+    tp, tl, v = tensors.numpy_inputs(M, P, mom_std=1e-3, seed=17)
+    rp, ci, w = graphs.exponential_weights(M)
+    m1 = oracle.Mix("csr", rp, ci, w, rounds=2)
+    out_t, out_v, _ = oracle.outer_step(tp, tl, v, m1, oracle.Mix("identity"), lr=LR, mu=MU, mix1_state=True)
+    W1 = dense_W(rp, ci, w)
+    x = W1 @ (W1 @ tp.astype(np.float64))
+    vb = W1 @ (W1 @ v.astype(np.float64))
+    g = tp.astype(np.float64) - tl.astype(np.float64)
+    for m in range(M):
+        want_t, want_v = torch_sgd(x[m], g[m], vb[m], True)
+        close(out_t[m], want_t, ulps=4)
+        close(out_v[m], want_v, ulps=4)
+
+
+def test_state_mix_off_leaves_momentum_per_worker():
+    """Without state mixing the new momentum is mu v_m + g_m per worker, with
+    the same Mix1 (the state is not mixed unless asked)."""
+    M, P = 4, 64
+    tp, tl, v = tensors.numpy_inputs(M, P, mom_std=1e-3, seed=2)
+    _, out_v, _ = oracle.outer_step(tp, tl, v, oracle.Mix("global"), oracle.Mix("identity"), lr=LR, mu=MU)
+    close(out_v, float(MU) * v.astype(np.float64) + (tp.astype(np.float64) - tl.astype(np.float64)))
+
+
+# -------------------------------------------------------------- Mix2 subset
+
+SEGMENT_CASES = [
+    [(0, 100)],
+    [(37, 38), (200, 257), (511, 600)],
+    [(0, 600)],
+    [(599, 600)],
+]
+
+
+@pytest.mark.parametrize("segs", SEGMENT_CASES)
+def test_subset_plain_sgd_factored_form(segs):
+    """lr = 1, mu = 0: theta' = Mix1(theta) + Mix2_S(Delta), where Mix2_S is K2
+    rounds of W2 on the subset columns and the identity elsewhere, built here
+    as dense scipy products column by column."""
+    M, P = 6, 600
+    tp, tl, v = tensors.numpy_inputs(M, P, mom_std=0.0, seed=23)
+    rp, ci, w = graphs.ring_weights(M)
+    W = dense_W(rp, ci, w)
+    out_t, _, cd = oracle.outer_step(tp, tl, np.zeros_like(v), oracle.Mix("global"),
+                                     oracle.Mix("csr", rp, ci, w, rounds=2), lr=1.0, mu=0.0, subset=segs)
+    inset = np.zeros(P, bool)
+    for b, e in segs:
+        inset[b:e] = True
+    d = tl.astype(np.float64) - tp.astype(np.float64)
+    dm = np.where(inset[None, :], W @ (W @ d), d)
+    want = tp.astype(np.float64).mean(axis=0)[None, :] + dm
+    close(out_t, want, ulps=4)
+    # Consensus rows of the Mix2 rounds: brute-force sums over both parts.
+    g0 = -d
+    for k, gk in enumerate([g0, np.where(inset, W @ g0, g0), np.where(inset, W @ (W @ g0), g0)]):
+        S = ((gk - gk.mean(axis=0)) ** 2).sum(axis=1)
+        np.testing.assert_allclose(cd[k], S, rtol=1e-12, atol=1e-300)
+
+
+def test_subset_segments_match_full_and_no_mix2():
+    """Inside the subset the result equals the full-Mix2 step, outside it the
+    step with Mix2 the identity (Nesterov, random momentum)."""
+    M, P = 8, 1000
+    tp, tl, v = tensors.numpy_inputs(M, P, dtype="bf16", mom_std=1e-3, seed=29)
+    rp, ci, w = graphs.ring_weights(M)
+    m2 = oracle.Mix("csr", rp, ci, w, rounds=1)
+    segs = [(0, 129), (400, 401), (700, 1000)]
+    ts, vs, _ = oracle.outer_step(tp, tl, v, oracle.Mix("global"), m2, subset=segs)
+    tf, vf, _ = oracle.outer_step(tp, tl, v, oracle.Mix("global"), m2)
+    tn, vn, _ = oracle.outer_step(tp, tl, v, oracle.Mix("global"), oracle.Mix("identity"))
+    inset = np.zeros(P, bool)
+    for b, e in segs:
+        inset[b:e] = True
+    assert np.array_equal(ts[:, inset], tf[:, inset]) and np.array_equal(vs[:, inset], vf[:, inset])
+    assert np.array_equal(ts[:, ~inset], tn[:, ~inset]) and np.array_equal(vs[:, ~inset], vn[:, ~inset])
+
+
+@pytest.mark.parametrize("segs", [[(5, 5)], [(10, 20), (15, 30)], [(30, 40), (10, 20)], [(0, 601)], [(-1, 3)]])
+def test_subset_rejects_bad_segments(segs):
+    M, P = 2, 600
+    tp, tl, v = tensors.numpy_inputs(M, P, seed=1)
+    with pytest.raises(ValueError):
+        oracle.outer_step(tp, tl, v, oracle.Mix("global"), oracle.Mix("global"), subset=segs)
