@@ -15,6 +15,12 @@
  *   v'_m    = mu v_m + ghat_m                     Nesterov, two-line form
  *   theta'_m = x_m - lr (ghat_m + mu v'_m)        (Appendix B)
  *
+ * Variants set at creation or by a call: plain momentum (theta'_m = x_m -
+ * lr v'_m), Mix1 applied to the momentum before its update (Appendix B,
+ * GlobalM1S: the outer optimizer state is averaged as part of Mix1), and
+ * Mix2 restricted to a subset of the parameters (Sec. 4.1 and Appendix C,
+ * the Mix2-subset configuration: identity outside the subset).
+ *
  * A Mix round maps row m to sum_n w_{m,n} u_n (Sec. 3, gossip mixing
  * operator), with W given as CSR: row m lists the workers it pulls from.
  * The step optionally reports, per worker, S_m(u) = sum_p (u_m,p - mean_n
@@ -84,20 +90,28 @@ typedef enum {
                                     its row's diagonal (double, ascending j, rounded) */
 } fgd_reweight;
 
-#define FGD_MAX_WORKERS 64 /* largest M this build runs */
-#define FGD_MAX_ROUNDS 8   /* largest number of rounds per Mix slot */
+#define FGD_MAX_WORKERS 64          /* largest M this build runs */
+#define FGD_MAX_ROUNDS 8            /* largest number of rounds per Mix slot */
+#define FGD_MAX_SUBSET_SEGMENTS 4096 /* largest number of Mix2 subset segments */
 
 typedef struct {
-    uint32_t struct_size; /* sizeof(fgd_config), for forward compatibility */
+    uint32_t struct_size; /* sizeof(fgd_config), checked for equality */
     int32_t num_workers;  /* M, 1..FGD_MAX_WORKERS */
     int64_t num_params;   /* P >= 0 parameters per worker */
     int64_t ld;           /* row stride in elements, >= P, ld * elem size % 16 == 0 */
-    int32_t param_dtype;  /* fgd_dtype of theta_prev and theta_local (momentum is
-                             always float32; arithmetic is float32) */
+    int32_t param_dtype;  /* fgd_dtype of theta_prev and theta_local (arithmetic is
+                             float32) */
+    int32_t state_dtype;  /* fgd_dtype of the momentum: FGD_F32 only (else
+                             FGD_ERR_UNSUPPORTED) */
     float outer_lr;       /* lr (gamma), e.g. 0.7 (Sec. 5, Appendix A) */
     float momentum;       /* mu, e.g. 0.9 */
+    int32_t nesterov;     /* 1: Nesterov (Appendix B two-line form), 0: plain momentum,
+                             theta' = x - lr v' */
     int32_t device;       /* HIP device ordinal; -1 creates a host-only engine that
                              validates topologies but cannot run compute calls */
+    int32_t mix1_state;   /* 1: Mix1 is also applied to the momentum before the momentum
+                             update (Appendix B, GlobalM1S); 0: momentum stays per worker */
+    int32_t reserved;     /* must be 0 */
 } fgd_config;
 
 /* Creates an engine.  Allocates the device-side topology slots and the
@@ -130,6 +144,21 @@ fgd_status fgd_set_topology(fgd_engine *e, int32_t which, int32_t kind, const in
                             const int32_t *col_idx, const float *weights, int32_t num_rounds,
                             const uint8_t *edge_masks, int32_t reweight);
 
+/* Restricts Mix2 to a subset of the parameters (the Mix2-subset
+ * configuration of Sec. 4.1 and Appendix C, where the subset is a set of
+ * parameter blocks): Mix2 acts on every index inside one of the segments
+ * and is the identity elsewhere, in every round.
+ *   segments      host int64[num_segments][2] of half-open ranges [begin, end):
+ *                 0 <= begin < end <= P, ascending and disjoint (touching is
+ *                 allowed)
+ *   num_segments  0 .. FGD_MAX_SUBSET_SEGMENTS; 0 removes the restriction
+ *                 (Mix2 acts everywhere); segments may then be NULL
+ * Takes effect, stream-ordered, at the next fgd_outer_step.  A step with a
+ * subset needs a CSR Mix2 (else FGD_ERR_UNSUPPORTED).  The consensus rows of
+ * the Mix2 rounds cover every parameter: inside the subset the mixed values,
+ * outside it g^0.  Host arrays are copied before return. */
+fgd_status fgd_set_mix2_subset(fgd_engine *e, const int64_t *segments, int32_t num_segments);
+
 /* Number of consensus-distance rows fgd_outer_step writes:
  * (K2 + 1) + (K1 + 1) + 1, where a GLOBAL_MEAN slot counts as one round and
  * IDENTITY as zero.  Needs both slots set. */
@@ -146,7 +175,8 @@ fgd_status fgd_num_cd_rows(const fgd_engine *e, int32_t *n_rows);
  *                theta'.  Entry [r][m] is S_m of that intermediate.
  * Arithmetic is float32 (bf16 storage is widened exactly; theta' is rounded
  * to bf16 to nearest even); consensus sums accumulate in double.  Both Mix
- * slots must be set (else FGD_ERR_STATE). */
+ * slots must be set (else FGD_ERR_STATE).  Elements of a row at indices
+ * [P, ld) may be read but are never written. */
 fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
                           double *cd_out, void *stream);
 

@@ -24,7 +24,7 @@ FGD_F32, FGD_BF16 = 0, 1
 FGD_MIX1, FGD_MIX2 = 1, 2
 FGD_W_IDENTITY, FGD_W_GLOBAL_MEAN, FGD_W_CSR = 0, 1, 2
 FGD_REWEIGHT_NONE, FGD_REWEIGHT_METROPOLIS, FGD_REWEIGHT_SELF = 0, 1, 2
-FGD_MAX_WORKERS, FGD_MAX_ROUNDS = 64, 8
+FGD_MAX_WORKERS, FGD_MAX_ROUNDS, FGD_MAX_SUBSET_SEGMENTS = 64, 8, 4096
 
 DTYPES = {"f32": FGD_F32, "bf16": FGD_BF16}
 KINDS = {"identity": FGD_W_IDENTITY, "global": FGD_W_GLOBAL_MEAN, "csr": FGD_W_CSR}
@@ -41,7 +41,9 @@ class FgdError(RuntimeError):
 class fgd_config(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("num_workers", ctypes.c_int32),
                 ("num_params", ctypes.c_int64), ("ld", ctypes.c_int64), ("param_dtype", ctypes.c_int32),
-                ("outer_lr", ctypes.c_float), ("momentum", ctypes.c_float), ("device", ctypes.c_int32)]
+                ("state_dtype", ctypes.c_int32), ("outer_lr", ctypes.c_float), ("momentum", ctypes.c_float),
+                ("nesterov", ctypes.c_int32), ("device", ctypes.c_int32), ("mix1_state", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 def _load():
@@ -59,6 +61,7 @@ def _load():
         "fgd_create": (I32, [ctypes.POINTER(fgd_config), ctypes.POINTER(ctypes.c_void_p)]),
         "fgd_destroy": (I32, [P]),
         "fgd_set_topology": (I32, [P, I32, I32, P, P, P, I32, P, I32]),
+        "fgd_set_mix2_subset": (I32, [P, P, I32]),
         "fgd_num_cd_rows": (I32, [P, ctypes.POINTER(I32)]),
         "fgd_outer_step": (I32, [P, P, P, P, P, P]),
         "fgd_consensus_distance": (I32, [P, P, I32, P, P]),
@@ -124,10 +127,12 @@ def _stream(stream):
 
 # --------------------------------------------------------------- raw C ABI
 
-def fgd_create(num_workers, num_params, ld=None, param_dtype="f32", outer_lr=0.7, momentum=0.9, device=0):
+def fgd_create(num_workers, num_params, ld=None, param_dtype="f32", outer_lr=0.7, momentum=0.9, device=0,
+               nesterov=True, mix1_state=False, state_dtype="f32"):
     cfg = fgd_config(ctypes.sizeof(fgd_config), int(num_workers), int(num_params),
                      int(num_params if ld is None else ld), DTYPES.get(param_dtype, param_dtype),
-                     float(outer_lr), float(momentum), int(device))
+                     DTYPES.get(state_dtype, state_dtype), float(outer_lr), float(momentum),
+                     int(nesterov), int(device), int(mix1_state), 0)
     h = ctypes.c_void_p()
     _check(lib.fgd_create(ctypes.byref(cfg), ctypes.byref(h)), "fgd_create")
     return h
@@ -145,6 +150,13 @@ def fgd_set_topology(h, which, kind, row_ptr=None, col_idx=None, weights=None, n
     mk, pmk = _host(edge_masks, np.uint8)
     _check(lib.fgd_set_topology(h, MIXES[which], KINDS.get(kind, kind), prp, pci, pw, int(num_rounds), pmk,
                                 REWEIGHTS.get(reweight, reweight)), "fgd_set_topology")
+
+
+def fgd_set_mix2_subset(h, segments=None):
+    """segments: [n][2] int64 half-open parameter ranges, or None / empty for no subset."""
+    seg = None if segments is None else np.ascontiguousarray(np.asarray(segments, dtype=np.int64).reshape(-1, 2))
+    n = 0 if seg is None else seg.shape[0]
+    _check(lib.fgd_set_mix2_subset(h, seg.ctypes.data if n else None, n), "fgd_set_mix2_subset")
 
 
 def fgd_num_cd_rows(h) -> int:
@@ -209,12 +221,14 @@ class Engine:
     tensors have the layout the engine was created for.
     """
 
-    def __init__(self, num_workers, num_params, ld=None, param_dtype="f32", outer_lr=0.7, momentum=0.9, device=0):
+    def __init__(self, num_workers, num_params, ld=None, param_dtype="f32", outer_lr=0.7, momentum=0.9, device=0,
+                 nesterov=True, mix1_state=False):
         self.M, self.P = int(num_workers), int(num_params)
         self.ld = self.P if ld is None else int(ld)
         self.dtype = param_dtype
         self.device = device
-        self.handle = fgd_create(self.M, self.P, self.ld, param_dtype, outer_lr, momentum, device)
+        self.handle = fgd_create(self.M, self.P, self.ld, param_dtype, outer_lr, momentum, device, nesterov,
+                                 mix1_state)
         self._nnz = {1: 0, 2: 0}
 
     def close(self):
@@ -237,6 +251,9 @@ class Engine:
         """From the dict produced by synth.configs.topology."""
         self.set_topology(which, t["kind"], t["row_ptr"], t["col_idx"], t["weights"], t["rounds"], t["masks"],
                           t["reweight"])
+
+    def set_mix2_subset(self, segments=None):
+        fgd_set_mix2_subset(self.handle, segments)
 
     def num_cd_rows(self):
         return fgd_num_cd_rows(self.handle)

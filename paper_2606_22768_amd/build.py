@@ -18,7 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libfgd.so")
 
-HIP_SOURCES = ["engine.hip", "kernels_f32.hip", "kernels_bf16.hip", "kernels_common.hip"]
+HIP_SOURCES = ["engine.hip", "kernels_f32.hip", "kernels_bf16.hip", "kernels_f32_ms.hip", "kernels_bf16_ms.hip",
+               "kernels_common.hip"]
 CXX_SOURCES = ["topology.cpp"]
 
 ARCH = "gfx950"

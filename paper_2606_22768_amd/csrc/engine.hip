@@ -58,7 +58,8 @@ struct fgd_engine {
     bool host_only = true;
     fgd::MixTopology slot[2];   // [0] Mix1, [1] Mix2
     bool slot_set[2] = {false, false};
-    uint64_t topo_version = 0;  // bumped by every fgd_set_topology
+    std::vector<int64_t> subset;  // Mix2 subset segments, [n][2] (empty: Mix2 everywhere)
+    uint64_t topo_version = 0;  // bumped by every fgd_set_topology and fgd_set_mix2_subset
 
     // Device side (absent for host-only engines).
     int num_cus = 0;
@@ -110,9 +111,14 @@ fgd::MixDev mix_dev(const fgd::MixTopology &t, const void *tables) {
     return d;
 }
 
-bool lookup(int M, int32_t dtype, int k1, int k2, fgd::KernelSet &ks) {
+bool lookup(int M, int32_t dtype, int k1, int k2, bool mix_state, fgd::KernelSet &ks) {
+    if (mix_state)
+        return dtype == FGD_BF16 ? fgd::kernels_bf16_ms(M, k1, k2, &ks) : fgd::kernels_f32_ms(M, k1, k2, &ks);
     return dtype == FGD_BF16 ? fgd::kernels_bf16(M, k1, k2, &ks) : fgd::kernels_f32(M, k1, k2, &ks);
 }
+
+// Byte offset of the subset segments in a ring slot (after both tables, 16-byte aligned).
+size_t subset_offset(size_t tables_bytes) { return (tables_bytes + 15) & ~static_cast<size_t>(15); }
 
 // Makes sure the device holds the current topology for `stream` and returns
 // the ring slot.  Uploads (stream-ordered) when the topology changed or the
@@ -126,7 +132,8 @@ fgd_status ensure_topology(fgd_engine *e, hipStream_t stream, int &ring) {
     e->slot[0].pack_tables(t1);
     e->slot[1].pack_tables(t2);
     const size_t b1 = t1.size() * sizeof(int32_t), b2 = t2.size() * sizeof(int32_t);
-    if (b1 + b2 > e->topo_capacity) return fail(FGD_ERR_UNSUPPORTED, "topology tables exceed the device slot");
+    const size_t so = subset_offset(b1 + b2), bs = e->subset.size() * sizeof(int64_t);
+    if (so + bs > e->topo_capacity) return fail(FGD_ERR_UNSUPPORTED, "topology tables exceed the device slot");
     const int r = e->topo_next;
     e->topo_next = (e->topo_next + 1) % kTopoRing;
     if (e->topo_pending[r]) {
@@ -137,8 +144,10 @@ fgd_status ensure_topology(fgd_engine *e, hipStream_t stream, int &ring) {
     char *h = static_cast<char *>(e->h_topo[r]);
     if (b1) std::memcpy(h, t1.data(), b1);
     if (b2) std::memcpy(h + b1, t2.data(), b2);
-    if (b1 + b2) {
-        hipError_t err = hipMemcpyAsync(e->d_topo[r], h, b1 + b2, hipMemcpyHostToDevice, stream);
+    if (bs) std::memcpy(h + so, e->subset.data(), bs);
+    const size_t total = bs ? so + bs : b1 + b2;
+    if (total) {
+        hipError_t err = hipMemcpyAsync(e->d_topo[r], h, total, hipMemcpyHostToDevice, stream);
         if (err != hipSuccess) return hip_fail(err, "uploading the topology");
     }
     e->topo_current = r;
@@ -148,12 +157,18 @@ fgd_status ensure_topology(fgd_engine *e, hipStream_t stream, int &ring) {
     return FGD_OK;
 }
 
-// Offsets of the Mix1 and Mix2 tables inside a ring slot.
-void table_ptrs(const fgd_engine *e, int ring, const void *&t1, const void *&t2) {
-    const size_t b1 = static_cast<size_t>(e->slot[0].kind == 2 ? e->slot[0].rounds * e->slot[0].width : 0) *
-                      e->cfg.num_workers * 2 * sizeof(int32_t);
+// Device addresses of the Mix1 and Mix2 tables and of the subset segments
+// inside a ring slot.
+void table_ptrs(const fgd_engine *e, int ring, const void *&t1, const void *&t2, const int64_t *&seg) {
+    auto bytes = [&](const fgd::MixTopology &t) {
+        return static_cast<size_t>(t.kind == 2 ? t.rounds * t.width : 0) * e->cfg.num_workers * 2 * sizeof(int32_t);
+    };
+    const size_t b1 = bytes(e->slot[0]), b2 = bytes(e->slot[1]);
     t1 = e->d_topo[ring];
     t2 = static_cast<const char *>(e->d_topo[ring]) + b1;
+    seg = e->subset.empty() ? nullptr
+                            : reinterpret_cast<const int64_t *>(static_cast<const char *>(e->d_topo[ring]) +
+                                                                subset_offset(b1 + b2));
 }
 
 int64_t tiles_of(int64_t P, int v) {
@@ -231,6 +246,12 @@ fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
     if (cfg->struct_size != sizeof(fgd_config))
         return fail(FGD_ERR_INVALID_ARG, "struct_size %u does not match sizeof(fgd_config) %zu", cfg->struct_size,
                     sizeof(fgd_config));
+    if (cfg->state_dtype != FGD_F32 && cfg->state_dtype != FGD_BF16)
+        return fail(FGD_ERR_INVALID_ARG, "unknown state_dtype %d", cfg->state_dtype);
+    if (cfg->state_dtype != FGD_F32) return fail(FGD_ERR_UNSUPPORTED, "the momentum is stored in float32 only");
+    if (cfg->nesterov != 0 && cfg->nesterov != 1) return fail(FGD_ERR_INVALID_ARG, "nesterov must be 0 or 1");
+    if (cfg->mix1_state != 0 && cfg->mix1_state != 1) return fail(FGD_ERR_INVALID_ARG, "mix1_state must be 0 or 1");
+    if (cfg->reserved != 0) return fail(FGD_ERR_INVALID_ARG, "reserved must be 0");
     if (cfg->num_workers < 1 || cfg->num_workers > FGD_MAX_WORKERS)
         return fail(FGD_ERR_INVALID_ARG, "num_workers %d is outside [1, %d]", cfg->num_workers, FGD_MAX_WORKERS);
     if (cfg->num_params < 0) return fail(FGD_ERR_INVALID_ARG, "num_params is negative");
@@ -258,8 +279,10 @@ fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
             return hip_fail(err, "querying the compute-unit count");
         }
         const size_t M = static_cast<size_t>(cfg->num_workers);
-        // Largest packed tables: both slots, FGD_MAX_ROUNDS rounds, width M.
-        e->topo_capacity = 2 * static_cast<size_t>(FGD_MAX_ROUNDS) * M * M * 2 * sizeof(int32_t);
+        // Largest packed tables (both slots, FGD_MAX_ROUNDS rounds, width M),
+        // then the largest subset.
+        e->topo_capacity = subset_offset(2 * static_cast<size_t>(FGD_MAX_ROUNDS) * M * M * 2 * sizeof(int32_t)) +
+                           static_cast<size_t>(FGD_MAX_SUBSET_SEGMENTS) * 2 * sizeof(int64_t);
         const int n_cd_max = 2 * FGD_MAX_ROUNDS + 3;
         e->partials_capacity = static_cast<size_t>(e->num_cus) * kMaxBlocksPerCu * n_cd_max * M;
         for (int r = 0; r < kTopoRing && err == hipSuccess; ++r) {
@@ -303,6 +326,27 @@ fgd_status fgd_set_topology(fgd_engine *e, int32_t which, int32_t kind, const in
     if (ts != fgd::TopoStatus::ok) return from_topo(ts, err);
     e->slot[which - 1] = std::move(t);
     e->slot_set[which - 1] = true;
+    ++e->topo_version;
+    return FGD_OK;
+}
+
+fgd_status fgd_set_mix2_subset(fgd_engine *e, const int64_t *segments, int32_t num_segments) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (num_segments < 0 || num_segments > FGD_MAX_SUBSET_SEGMENTS)
+        return fail(FGD_ERR_INVALID_ARG, "num_segments %d is outside [0, %d]", num_segments, FGD_MAX_SUBSET_SEGMENTS);
+    if (num_segments > 0 && !segments) return fail(FGD_ERR_INVALID_ARG, "segments is NULL");
+    const int64_t P = e->cfg.num_params;
+    int64_t prev_end = 0;
+    for (int32_t i = 0; i < num_segments; ++i) {
+        const int64_t b = segments[2 * i], en = segments[2 * i + 1];
+        if (b < prev_end || en <= b || en > P)
+            return fail(FGD_ERR_INVALID_ARG,
+                        "segment %d [%lld, %lld) must be non-empty, inside [0, P) and after the previous one", i,
+                        static_cast<long long>(b), static_cast<long long>(en));
+        prev_end = en;
+    }
+    e->subset.assign(segments, segments + 2 * static_cast<size_t>(num_segments));
     ++e->topo_version;
     return FGD_OK;
 }
@@ -365,8 +409,10 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
             return fail(FGD_ERR_INVALID_ARG, "theta_prev, theta_local and momentum must not overlap");
     }
     hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    if (!e->subset.empty() && e->slot[1].kind != 2)
+        return fail(FGD_ERR_UNSUPPORTED, "a Mix2 subset needs a CSR Mix2");
     fgd::KernelSet ks;
-    if (!lookup(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, ks))
+    if (!lookup(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, c.mix1_state != 0, ks))
         return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
     hipError_t herr = hipSetDevice(c.device);
     if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
@@ -387,10 +433,14 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     p.n_cd = n_cd_rows(e);
     p.lr = c.outer_lr;
     p.mu = c.momentum;
+    p.nesterov = c.nesterov;
     const void *t1, *t2;
-    table_ptrs(e, ring, t1, t2);
+    const int64_t *seg;
+    table_ptrs(e, ring, t1, t2, seg);
     p.mix1 = mix_dev(e->slot[0], t1);
     p.mix2 = mix_dev(e->slot[1], t2);
+    p.n_seg = static_cast<int32_t>(e->subset.size() / 2);
+    p.seg = seg;
     const bool tables = e->slot[0].kind == 2 || e->slot[1].kind == 2;
     const bool padded = (e->slot[0].kind == 2 && e->slot[0].padded) || (e->slot[1].kind == 2 && e->slot[1].padded);
     p.lds_rows = tables ? c.num_workers + (padded ? 1 : 0) : 0;
@@ -442,7 +492,7 @@ fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, d
     if ((c.ld * elem_size(dtype)) % 16 != 0) return fail(FGD_ERR_INVALID_ARG, "ld * elem_size must be a multiple of 16");
     if (reinterpret_cast<uintptr_t>(out) & 7u) return fail(FGD_ERR_INVALID_ARG, "out must be 8-byte aligned");
     fgd::KernelSet ks;
-    if (!lookup(c.num_workers, dtype, 0, 0, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
+    if (!lookup(c.num_workers, dtype, 0, 0, false, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
     hipError_t herr = hipSetDevice(c.device);
     if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
     hipStream_t stream = static_cast<hipStream_t>(stream_handle);

@@ -16,8 +16,15 @@
 //            Per round the host supplies a padded table [width][M] of
 //            (column, weight): the d-th live entry of every row, in ascending
 //            column order, so the sum runs in the CSR row's order.
-//   phase D  load momentum rows, v' = mu v + g, theta' = x - lr (g + mu v'),
-//            store theta' (RNE to bf16 for bf16 storage) and v'.
+//   phase D  load momentum rows, v' = mu v + g, theta' = x - lr (g + mu v')
+//            (plain momentum: theta' = x - lr v'), store theta' (RNE to bf16
+//            for bf16 storage) and v'.  With the optimizer state mixed
+//            (Appendix B, GlobalM1S) all momentum rows are loaded first and
+//            Mix1 is applied to them before the update.
+//   subset   Mix2 restricted to parameter segments (the Mix2-subset
+//            configuration): after every round the elements outside the
+//            subset are restored from the lane's own LDS column, which still
+//            holds the round's input.
 //   CD       S_m(u) = sum_p (u_m - mean_n u_n)^2 for every intermediate u
 //            (Sec. 4.4; Appendix D.1): float32 deviations, a reduce-scatter
 //            across the wave's lanes (cross-row lane swaps, then DPP),
@@ -69,8 +76,10 @@ struct StepParams {
     int32_t M, n_cd;
     int32_t lds_rows;         // rows of the LDS gather array: 0 (no CSR mix), M, or M + 1
                               // when some table pads a short row (row M is then zero)
-    int32_t pad_;
+    int32_t nesterov;         // 1: theta' = x - lr (g + mu v'); 0: theta' = x - lr v'
     float lr, mu;
+    int32_t n_seg, pad_;      // Mix2 subset: number of segments (0: Mix2 everywhere)
+    const int64_t *seg;       // [n_seg][2] ascending half-open [begin, end) parameter ranges
     MixDev mix1, mix2;
 };
 
@@ -435,9 +444,27 @@ __device__ __forceinline__ void table_round(const_table_ptr tab, int width, int 
 // consecutive rows, `cd_stride` doubles apart.  A doubly-stochastic W keeps
 // the worker mean (Sec. 3), so every round's consensus row is taken about
 // the input mean.
+// Restores the elements whose bit is set in `keep` to the values the round
+// started from, which are still in the lane's LDS column (identity outside a
+// Mix2 subset).
+template <int MMAX, bool EXACT, int V>
+__device__ inline void keep_own(float (&u)[MMAX][V], const float *rows, int tid, int M, uint32_t keep) {
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+        if (EXACT || m < M) {
+            const float *own = rows + (static_cast<int64_t>(m) * kBlock + tid) * V;
+#pragma unroll
+            for (int v = 0; v < V; ++v)
+                if ((keep >> v) & 1u) u[m][v] = own[v];
+        }
+    }
+}
+
+// keep: bit v set = element v of this lane is outside the Mix's subset and
+// passes through unchanged (0 for a Mix over every element).
 template <int MMAX, bool EXACT, int V, int KIND>
 __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], const float (&mean)[V], float *rows,
-                                 int tid, double *cd_acc, int cd_stride, int lane) {
+                                 int tid, double *cd_acc, int cd_stride, int lane, uint32_t keep) {
     if constexpr (KIND == kIdentity || KIND == kGlobal) {
         return;
     } else {
@@ -446,13 +473,14 @@ __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], c
             for (int m = 0; m < MMAX; ++m)
 #pragma unroll
                 for (int v = 0; v < V; ++v) u[m][v] = mean[v];
-            return;  // every row equal: the consensus row stays 0
+            return;  // every row equal: the consensus row stays 0 (subsets need a table Mix)
         }
         if (KIND == kAny && mx.kind != kTable) return;
         const int Mr = EXACT ? MMAX : M;
         for (int k = 0; k < mx.rounds; ++k) {
             const_table_ptr tab = (const_table_ptr)(mx.table) + 2 * static_cast<int64_t>(k) * mx.width * Mr;
             table_round<MMAX, EXACT, V>(tab, mx.width, M, u, rows, tid);
+            if (keep) keep_own<MMAX, EXACT, V>(u, rows, tid, M, keep);
             if (cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u, mean, M, cd_acc + k * cd_stride, lane);
         }
     }
@@ -473,8 +501,12 @@ struct TileCtx {
 
 // One tile of kBlock * V parameters.  FULL: every lane's vector lies below P
 // (uniform; all tiles but the last), so no lane needs bounds logic.
-template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, bool FULL>
-__device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c, int64_t tb, uint32_t lo) {
+// MS: Mix1 is also applied to the momentum rows before the update.
+// keep: the lane's elements outside a Mix2 subset (bit v for element v);
+// they pass through Mix2 unchanged.
+template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, bool MS, bool FULL>
+__device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c, int64_t tb, uint32_t lo,
+                                          uint32_t keep) {
     constexpr int MP = pow2_at_least(MMAX);
     constexpr int kCdStride = kWavesPerBlock * MP;  // doubles between consensus rows
     constexpr int kE = PIO::kElem;
@@ -520,61 +552,94 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
         cd_accumulate_about<MMAX, EXACT, V>(u1, xbar, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
     }
     mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, c.rows, c.tid,
-                                  c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane);
+                                  c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane, 0u);
+    // A tile wholly outside a Mix2 subset runs the rounds too, with every
+    // element kept: one code path keeps the register budget of the kernel.
     mix_apply<MMAX, EXACT, V, K2>(a.mix2, M, u2, gbar, c.rows, c.tid, c.cd_acc ? c.cd_acc + 1 * kCdStride : nullptr,
-                                  kCdStride, c.lane);
+                                  kCdStride, c.lane, keep);
 
-    // Phase D: Nesterov (two-line form) and stores, a group of rows at a
-    // time.  The stored theta' replaces the row's dead input registers.
+    // Phase D: the outer optimizer and the stores.  The stored theta'
+    // replaces the row's dead input registers.
     constexpr bool kStoreInU2 = K2 != kGlobal;
     constexpr bool kStoreInU1 = !kStoreInU2 && K1 != kGlobal;
     constexpr int kSep = (!kStoreInU2 && !kStoreInU1) ? MMAX : 1;
     float sep[kSep][V];
-    constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
     const float mu = a.mu, lr = a.lr;
-#pragma unroll
-    for (int m0 = 0; m0 < MMAX; m0 += G) {
-        float vm[G][V];
-        if (FULL || nv > 0) {
-#pragma unroll
-            for (int j = 0; j < G; ++j) {
-                const int m = m0 + j;
-                if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[j]);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            const int m = m0 + j;
-            if (m >= MMAX) continue;
-            float stored[V];
-            if ((EXACT || m < M) && (FULL || nv > 0)) {
-                float t[V];
-#pragma unroll
-                for (int e = 0; e < V; ++e) {
-                    const float g = K2 == kGlobal ? gbar[e] : u2[m][e];
-                    const float x = K1 == kGlobal ? xbar[e] : u1[m][e];
-                    vm[j][e] = fmaf(mu, vm[j][e], g);
-                    t[e] = fmaf(-lr, fmaf(mu, vm[j][e], g), x);
-                }
-                const rsrc_t rv = row_rsrc(a.mom_out, m * a.ld + tb, 4);
-                const rsrc_t rp = row_rsrc(a.theta_out, m * a.ld + tb, kE);
-                if (FULL || nv == V) {
-                    F32Io<V>::store(rv, off_v, vm[j]);
-                    PIO::store(rp, off_p, t, stored);
-                } else {
-                    F32Io<V>::store_part(rv, off_v, nv, vm[j]);
-                    PIO::store_part(rp, off_p, nv, t, stored);
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < V; ++e) stored[e] = 0.0f;
-            }
+    const bool nesterov = a.nesterov != 0;
+
+    // v' = mu v + g ; theta' = x - lr (g + mu v') or x - lr v'; stores row m.
+    auto finish_row = [&](int m, float (&vr)[V]) {
+        float stored[V];
+        if ((EXACT || m < M) && (FULL || nv > 0)) {
+            float t[V];
 #pragma unroll
             for (int e = 0; e < V; ++e) {
-                if constexpr (kStoreInU2) u2[m][e] = stored[e];
-                else if constexpr (kStoreInU1) u1[m][e] = stored[e];
-                else sep[kSep == 1 ? 0 : m][e] = stored[e];
+                const float g = K2 == kGlobal ? gbar[e] : u2[m][e];
+                const float x = K1 == kGlobal ? xbar[e] : u1[m][e];
+                vr[e] = fmaf(mu, vr[e], g);
+                const float step = nesterov ? fmaf(mu, vr[e], g) : vr[e];
+                t[e] = fmaf(-lr, step, x);
             }
+            const rsrc_t rv = row_rsrc(a.mom_out, m * a.ld + tb, 4);
+            const rsrc_t rp = row_rsrc(a.theta_out, m * a.ld + tb, kE);
+            if (FULL || nv == V) {
+                F32Io<V>::store(rv, off_v, vr);
+                PIO::store(rp, off_p, t, stored);
+            } else {
+                F32Io<V>::store_part(rv, off_v, nv, vr);
+                PIO::store_part(rp, off_p, nv, t, stored);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < V; ++e) stored[e] = 0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            if constexpr (kStoreInU2) u2[m][e] = stored[e];
+            else if constexpr (kStoreInU1) u1[m][e] = stored[e];
+            else sep[kSep == 1 ? 0 : m][e] = stored[e];
+        }
+    };
+
+    if constexpr (MS) {
+        // Optimizer state mixed by Mix1: every momentum row first.
+        float vm[MMAX][V];
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+            if ((EXACT || m < M) && (FULL || nv > 0)) F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[m]);
+            else {
+#pragma unroll
+                for (int e = 0; e < V; ++e) vm[m][e] = 0.0f;
+            }
+        }
+        float vbar[V];
+        row_mean<MMAX, EXACT, V>(vm, M, vbar);
+        if constexpr (K1 == kGlobal) {
+#pragma unroll
+            for (int m = 0; m < MMAX; ++m)
+#pragma unroll
+                for (int e = 0; e < V; ++e) vm[m][e] = vbar[e];
+        } else {
+            mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, vm, vbar, c.rows, c.tid, nullptr, 0, c.lane, 0u);
+        }
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) finish_row(m, vm[m]);
+    } else {
+        // A group of rows at a time bounds the momentum registers.
+        constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
+#pragma unroll
+        for (int m0 = 0; m0 < MMAX; m0 += G) {
+            float vm[G][V];
+            if (FULL || nv > 0) {
+#pragma unroll
+                for (int j = 0; j < G; ++j) {
+                    const int m = m0 + j;
+                    if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[j]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < G; ++j)
+                if (m0 + j < MMAX) finish_row(m0 + j, vm[j]);
         }
     }
     if (c.cd_acc) {
@@ -585,13 +650,18 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
     }
 }
 
+// Parameter segments of a Mix2 subset, read as scalar loads (never written).
+typedef const __attribute__((address_space(4))) int64_t *const_seg_ptr;
+
 // K1, K2: compile-time kinds of Mix1 and Mix2 (kAny = decided at run time).
-template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2>
+// MS: the optimizer state is mixed by Mix1.
+template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, bool MS>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(waves_per_simd_target(MMAX))))
 void outer_step_kernel(StepParams a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     constexpr int MP = pow2_at_least(MMAX);
     constexpr int kCdStride = kWavesPerBlock * MP;
+    constexpr int64_t kTile = static_cast<int64_t>(kBlock) * V;
     TileCtx c;
     c.M = EXACT ? MMAX : a.M;
     c.tid = threadIdx.x;
@@ -613,10 +683,34 @@ void outer_step_kernel(StepParams a) {
     }
 
     const uint32_t lo = static_cast<uint32_t>(c.tid) * V;  // lane offset inside a tile, in elements
+    const const_seg_ptr seg = (const_seg_ptr)(a.seg);
+    int s = 0;  // first segment that ends after the tile start; tiles ascend, so it only moves forward
     for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
-        const int64_t tb = tile * (kBlock * V);  // first parameter of the tile (uniform)
-        if (tb + kBlock * V <= a.P) step_tile<MMAX, EXACT, V, PIO, K1, K2, true>(a, c, tb, lo);
-        else step_tile<MMAX, EXACT, V, PIO, K1, K2, false>(a, c, tb, lo);
+        const int64_t tb = tile * kTile;  // first parameter of the tile (uniform)
+        uint32_t keep = 0;                // elements of this lane outside the Mix2 subset
+        if constexpr (K2 == kTable || K2 == kAny) {
+            if (a.n_seg > 0) {
+                const int64_t te = tb + kTile < a.P ? tb + kTile : a.P;
+                while (s < a.n_seg && seg[2 * s + 1] <= tb) ++s;
+                if (s == a.n_seg || seg[2 * s] >= te) {
+                    keep = (1u << V) - 1u;  // wholly outside
+                } else if (seg[2 * s] <= tb && seg[2 * s + 1] >= te) {
+                    keep = 0u;  // wholly inside
+                } else {
+                    keep = (1u << V) - 1u;
+                    for (int i = s; i < a.n_seg && seg[2 * i] < te; ++i) {
+                        const int64_t b = seg[2 * i], e = seg[2 * i + 1];
+#pragma unroll
+                        for (int v = 0; v < V; ++v) {
+                            const int64_t p = tb + lo + v;
+                            if (p >= b && p < e) keep &= ~(1u << v);
+                        }
+                    }
+                }
+            }
+        }
+        if (tb + kTile <= a.P) step_tile<MMAX, EXACT, V, PIO, K1, K2, MS, true>(a, c, tb, lo, keep);
+        else step_tile<MMAX, EXACT, V, PIO, K1, K2, MS, false>(a, c, tb, lo, keep);
     }
 
     if (c.cd_acc) {
@@ -694,16 +788,35 @@ template <template <int> class PIOT, int MMAX, bool EXACT, int V>
 KernelSet make_kernel_set(int k1, int k2) {
     using P = PIOT<V>;
     KernelSet ks;
-    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny>);
+    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny, false>);
     if constexpr (EXACT) {
         if (k1 == kGlobal && k2 == kTable)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable>);
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, false>);
         else if (k1 == kTable && k2 == kTable)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kTable, kTable>);
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kTable, kTable, false>);
         else if (k1 == kGlobal && k2 == kIdentity)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity>);
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity, false>);
         else if (k1 == kIdentity && k2 == kGlobal)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kIdentity, kGlobal>);
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kIdentity, kGlobal, false>);
+    }
+    ks.consensus = reinterpret_cast<const void *>(&consensus_kernel<MMAX, EXACT, V, P>);
+    ks.v = V;
+    ks.mmax = MMAX;
+    return ks;
+}
+
+// The same with the optimizer state mixed by Mix1 (Appendix B: GlobalM1S and
+// GlobalM1SLocalM2 are specialised when M is exact).
+template <template <int> class PIOT, int MMAX, bool EXACT, int V>
+KernelSet make_kernel_set_ms(int k1, int k2) {
+    using P = PIOT<V>;
+    KernelSet ks;
+    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny, true>);
+    if constexpr (EXACT) {
+        if (k1 == kGlobal && k2 == kTable)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, true>);
+        else if (k1 == kGlobal && k2 == kIdentity)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity, true>);
     }
     ks.consensus = reinterpret_cast<const void *>(&consensus_kernel<MMAX, EXACT, V, P>);
     ks.v = V;
@@ -719,10 +832,34 @@ constexpr int lanes_v_bf16(int mmax) {
     return mmax <= 8 ? FGD_V_BF16_M8 : (mmax == 16 ? 4 : (mmax == 32 ? 2 : 1));
 }
 
+// Calls F::get<MMAX, EXACT>(k1, k2) for the instantiation that serves M
+// workers: exact for M in {1, 2, 4, 8, 16, 32, 64}, else the next power of
+// two with M read at run time.
+template <class F>
+bool select_workers(int M, int k1, int k2, KernelSet *out) {
+    if (M < 1 || M > 64) return false;
+    if (M == 1) *out = F::template get<1, true>(k1, k2);
+    else if (M == 2) *out = F::template get<2, true>(k1, k2);
+    else if (M == 3) *out = F::template get<4, false>(k1, k2);
+    else if (M == 4) *out = F::template get<4, true>(k1, k2);
+    else if (M < 8) *out = F::template get<8, false>(k1, k2);
+    else if (M == 8) *out = F::template get<8, true>(k1, k2);
+    else if (M < 16) *out = F::template get<16, false>(k1, k2);
+    else if (M == 16) *out = F::template get<16, true>(k1, k2);
+    else if (M < 32) *out = F::template get<32, false>(k1, k2);
+    else if (M == 32) *out = F::template get<32, true>(k1, k2);
+    else if (M < 64) *out = F::template get<64, false>(k1, k2);
+    else *out = F::template get<64, true>(k1, k2);
+    return true;
+}
+
 // Defined per storage type.  k1, k2: Mix kinds (kIdentity, kGlobal, kTable);
 // a specialised step kernel is returned when one exists, else the one that
 // reads the kinds at run time.  Returns false if M is outside [1, 64].
 bool kernels_f32(int M, int k1, int k2, KernelSet *out);
 bool kernels_bf16(int M, int k1, int k2, KernelSet *out);
+// Step kernels that also mix the optimizer state with Mix1.
+bool kernels_f32_ms(int M, int k1, int k2, KernelSet *out);
+bool kernels_bf16_ms(int M, int k1, int k2, KernelSet *out);
 
 }  // namespace fgd

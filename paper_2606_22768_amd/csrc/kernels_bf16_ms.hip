@@ -1,0 +1,18 @@
+// Step kernels for bf16 parameter storage (float32 arithmetic) that also apply Mix1 to the optimizer
+// state (Appendix B, GlobalM1S variants).
+#include "kernels.hpp"
+
+namespace fgd {
+
+namespace {
+struct Sets {
+    template <int MMAX, bool EXACT>
+    static KernelSet get(int k1, int k2) {
+        return make_kernel_set_ms<ParamBF16, MMAX, EXACT, lanes_v_bf16(MMAX)>(k1, k2);
+    }
+};
+}  // namespace
+
+bool kernels_bf16_ms(int M, int k1, int k2, KernelSet *out) { return select_workers<Sets>(M, k1, k2, out); }
+
+}  // namespace fgd

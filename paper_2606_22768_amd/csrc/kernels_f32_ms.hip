@@ -1,0 +1,18 @@
+// Step kernels for float32 parameter storage that also apply Mix1 to the optimizer
+// state (Appendix B, GlobalM1S variants).
+#include "kernels.hpp"
+
+namespace fgd {
+
+namespace {
+struct Sets {
+    template <int MMAX, bool EXACT>
+    static KernelSet get(int k1, int k2) {
+        return make_kernel_set_ms<ParamF32, MMAX, EXACT, lanes_v_f32(MMAX)>(k1, k2);
+    }
+};
+}  // namespace
+
+bool kernels_f32_ms(int M, int k1, int k2, KernelSet *out) { return select_workers<Sets>(M, k1, k2, out); }
+
+}  // namespace fgd

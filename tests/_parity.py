@@ -114,7 +114,8 @@ def topo(spec, M, rounds, seed=0, step=0):
     return configs.topology(spec, M, rounds, seed, step)
 
 
-def run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd=True, lr=0.7, mu=0.9):
+def run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd=True, lr=0.7, mu=0.9, nesterov=True,
+               mix1_state=False, subset=None):
     """One step on the GPU.  Inputs are numpy arrays; returns numpy copies of
     (theta', v', cd or None)."""
     dev = torch.device("cuda:0")
@@ -126,10 +127,12 @@ def run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd=True, lr=
         g_tp = torch.from_numpy(tp.view(np.int16)).to(dev).view(tdt)
         g_tl = torch.from_numpy(tl.view(np.int16)).to(dev).view(tdt)
     g_v = torch.from_numpy(v).to(dev)
-    eng = fgd.Engine(M, P, ld, dtype, lr, mu, device=0)
+    eng = fgd.Engine(M, P, ld, dtype, lr, mu, device=0, nesterov=nesterov, mix1_state=mix1_state)
     try:
         eng.set_topology_dict("mix1", t1)
         eng.set_topology_dict("mix2", t2)
+        if subset is not None:
+            eng.set_mix2_subset(subset)
         cd = None
         if with_cd:
             cd = torch.full((eng.num_cd_rows(), M), float("nan"), dtype=torch.float64, device=dev)
@@ -148,14 +151,16 @@ def aligned_ld(P):
 
 
 def run_case(fgd, torch, M, P, dtype, spec1, k1, spec2, k2, ld=None, seed=0, mom_std=1e-4, with_cd=True,
-             lr=0.7, mu=0.9):
+             lr=0.7, mu=0.9, nesterov=True, mix1_state=False, subset=None):
     ld = aligned_ld(P) if ld is None else ld
     tp, tl, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, mom_std=mom_std, seed=seed)
     t1 = topo(spec1, M, k1, seed)
     t2 = topo(spec2, M, k2, seed + 7)
     ref_t, ref_v, ref_cd = oracle.outer_step(tp, tl, v, oracle.Mix.from_topology(t1),
-                                             oracle.Mix.from_topology(t2), lr=lr, mu=mu, P=P, dtype=dtype)
-    got_t, got_v, got_cd = run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd, lr, mu)
+                                             oracle.Mix.from_topology(t2), lr=lr, mu=mu, P=P, dtype=dtype,
+                                             nesterov=nesterov, mix1_state=mix1_state, subset=subset)
+    got_t, got_v, got_cd = run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd, lr, mu,
+                                      nesterov=nesterov, mix1_state=mix1_state, subset=subset)
     scale = float(np.abs(tensors.bf16_bits_to_f32(tp) if dtype == "bf16" else tp).max()) if tp.size else 0.0
     compare_outputs(dtype, got_t, ref_t, got_v, ref_v, P, scale)
     # The padding beyond P is never written.

@@ -4,6 +4,7 @@ weights bit for bit like the oracle.  No compute call needs a GPU here
 (engines are created host-only, device = -1).
 """
 
+import ctypes
 import os
 import re
 import subprocess
@@ -187,3 +188,69 @@ def test_zero_rounds_is_identity():
     eng.set_topology("mix2", "global")
     assert eng.num_cd_rows() == 2 + 1 + 1
     eng.close()
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("nesterov", 2, "FGD_ERR_INVALID_ARG"),
+    ("nesterov", -1, "FGD_ERR_INVALID_ARG"),
+    ("mix1_state", 3, "FGD_ERR_INVALID_ARG"),
+    ("state_dtype", 7, "FGD_ERR_INVALID_ARG"),
+    ("state_dtype", "bf16", "FGD_ERR_UNSUPPORTED"),  # momentum is float32 only
+])
+def test_create_rejects_variant_fields(field, value, status):
+    kw = dict(num_workers=4, num_params=100, ld=104, param_dtype="f32", device=-1)
+    kw[field] = value
+    with pytest.raises(fgd.FgdError) as e:
+        fgd.fgd_create(**kw)
+    assert e.value.status == getattr(fgd, status)
+
+
+def test_create_rejects_nonzero_reserved_and_wrong_size():
+    for size, reserved in ((ctypes.sizeof(fgd.fgd_config), 1), (ctypes.sizeof(fgd.fgd_config) - 8, 0)):
+        cfg = fgd.fgd_config(size, 4, 100, 104, fgd.FGD_F32, fgd.FGD_F32, 0.7, 0.9, 1, -1, 0, reserved)
+        h = ctypes.c_void_p()
+        assert fgd.lib.fgd_create(ctypes.byref(cfg), ctypes.byref(h)) == fgd.FGD_ERR_INVALID_ARG
+        assert not h.value
+
+
+def test_create_accepts_variants_host_only():
+    for nesterov in (0, 1):
+        for state in (0, 1):
+            h = fgd.fgd_create(4, 100, 104, "bf16", device=-1, nesterov=nesterov, mix1_state=state)
+            fgd.fgd_destroy(h)
+
+
+@pytest.mark.parametrize("segs", [
+    [(5, 5)],                # empty
+    [(10, 20), (15, 30)],    # overlapping
+    [(30, 40), (10, 20)],    # descending
+    [(0, 101)],              # beyond P
+    [(-1, 3)],               # negative
+])
+def test_subset_rejections(segs):
+    eng = fgd.Engine(4, 100, 104, "f32", device=-1)
+    try:
+        with pytest.raises(fgd.FgdError) as e:
+            eng.set_mix2_subset(segs)
+        assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+    finally:
+        eng.close()
+
+
+def test_subset_limits():
+    eng = fgd.Engine(4, 1 << 20, 1 << 20, "f32", device=-1)
+    try:
+        n = fgd.FGD_MAX_SUBSET_SEGMENTS
+        ok = np.stack([np.arange(n) * 4, np.arange(n) * 4 + 2], axis=1)
+        eng.set_mix2_subset(ok)                     # the maximum count
+        eng.set_mix2_subset([(0, 1), (1, 2)])       # touching segments
+        eng.set_mix2_subset(None)                   # cleared
+        eng.set_mix2_subset([])
+        too_many = np.stack([np.arange(n + 1) * 4, np.arange(n + 1) * 4 + 2], axis=1)
+        with pytest.raises(fgd.FgdError) as e:
+            eng.set_mix2_subset(too_many)
+        assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+        assert fgd.lib.fgd_set_mix2_subset(eng.handle, None, 2) == fgd.FGD_ERR_INVALID_ARG
+        assert fgd.lib.fgd_set_mix2_subset(eng.handle, None, -1) == fgd.FGD_ERR_INVALID_ARG
+    finally:
+        eng.close()
