@@ -95,8 +95,14 @@ def cpu_baseline(sl, w, topo1, topo2):
     h_tp, h_tl, h_v = sl
     p_slice = h_tp.shape[1]
     m1, m2 = oracle.Mix.from_topology(topo1), oracle.Mix.from_topology(topo2)
+    segs = configs.subset_segments(w)
+    if segs is not None:  # the subset restricted to the slice
+        segs = [(b, min(e, p_slice)) for b, e in segs.tolist() if b < p_slice]
+        if not segs:  # no subset parameter in the slice: Mix2 is the identity there
+            m2, segs = oracle.Mix("identity"), None
     t0 = time.perf_counter()
-    oracle.outer_step(h_tp, h_tl, h_v, m1, m2, lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=w["dtype"])
+    oracle.outer_step(h_tp, h_tl, h_v, m1, m2, lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=w["dtype"],
+                      mix1_state=bool(w.get("mix1_state")), subset=segs)
     dt = time.perf_counter() - t0
     gbs = configs.min_bytes_per_step(M, p_slice, w["dtype"]) / dt / 1e9
     model, ncpu = host_cpu()
@@ -139,7 +145,11 @@ def main():
     tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
                                      mom_std=w["mom_std"], seed=w["seed"], device=dev)
     sl = None if args.no_cpu_baseline else host_slice(tp, tl, v, dtype, min(args.cpu_slice, P))
-    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0)
+    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0,
+                     mix1_state=bool(w.get("mix1_state")))
+    segs = configs.subset_segments(w)
+    if segs is not None:
+        eng.set_mix2_subset(segs)
     topo1 = configs.topology(w["mix1"], M, w["k1"], w["seed"])
     eng.set_topology_dict("mix1", topo1)
     per_step_masks = w["mix2"][1] == "metropolis" and w["mix2"][0] == "ring"
@@ -166,12 +176,17 @@ def main():
     torch.cuda.synchronize()
     eng.enable_timing(True)
     print("[bench] timed steps", file=sys.stderr, flush=True)
+    # Events on the launch stream bracket every step (median and min per step).
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev[0].record(stream)
     for i in range(args.steps):
         step(args.warmup + i)
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
     kernel_ms, n_kernels = eng.read_timing()
     eng.enable_timing(False)
 
@@ -206,6 +221,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
+        "step_ms_min": round(step_ms[0], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -216,6 +233,9 @@ def main():
         "config": {"workload": args.workload, "workers": M, "params_per_worker": P, "row_stride": ld,
                    "storage": "bf16 parameters, f32 momentum" if dtype == "bf16" else "f32 parameters and momentum",
                    "mix1": f"{w['mix1']} x{w['k1']}", "mix2": f"{w['mix2']} x{w['k2']}",
+                   "mix1_also_on_momentum": bool(w.get("mix1_state")),
+                   "mix2_subset_fraction": (None if segs is None else
+                                            round(float(sum(e - b for b, e in segs.tolist())) / P, 4)),
                    "outer_lr": configs.OUTER_LR, "momentum": configs.MOMENTUM,
                    "consensus": "fused, every intermediate", "algorithmic_bytes_per_step": bytes_step,
                    "parallelism": "single GPU, workers simulated as rows"},

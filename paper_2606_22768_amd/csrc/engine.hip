@@ -111,10 +111,11 @@ fgd::MixDev mix_dev(const fgd::MixTopology &t, const void *tables) {
     return d;
 }
 
-bool lookup(int M, int32_t dtype, int k1, int k2, bool mix_state, fgd::KernelSet &ks) {
+bool lookup(int M, int32_t dtype, int k1, int k2, bool mix_state, bool subset, fgd::KernelSet &ks) {
     if (mix_state)
-        return dtype == FGD_BF16 ? fgd::kernels_bf16_ms(M, k1, k2, &ks) : fgd::kernels_f32_ms(M, k1, k2, &ks);
-    return dtype == FGD_BF16 ? fgd::kernels_bf16(M, k1, k2, &ks) : fgd::kernels_f32(M, k1, k2, &ks);
+        return dtype == FGD_BF16 ? fgd::kernels_bf16_ms(M, k1, k2, subset, &ks)
+                                 : fgd::kernels_f32_ms(M, k1, k2, subset, &ks);
+    return dtype == FGD_BF16 ? fgd::kernels_bf16(M, k1, k2, subset, &ks) : fgd::kernels_f32(M, k1, k2, subset, &ks);
 }
 
 // Byte offset of the subset segments in a ring slot (after both tables, 16-byte aligned).
@@ -176,7 +177,7 @@ int64_t tiles_of(int64_t P, int v) {
     return (P + per - 1) / per;
 }
 
-fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntiles, int &grid) {
+fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntiles, int &grid, int cap = kMaxBlocksPerCu) {
     int per_cu = 0;
     if (lds > 65536) {
         hipError_t err = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
@@ -185,7 +186,7 @@ fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntile
     hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, fgd::kBlock, lds);
     if (err != hipSuccess) return hip_fail(err, "occupancy query");
     if (per_cu < 1) return fail(FGD_ERR_UNSUPPORTED, "kernel does not fit on a compute unit (LDS %zu bytes)", lds);
-    per_cu = std::min(per_cu, kMaxBlocksPerCu);
+    per_cu = std::min(per_cu, std::min(cap, kMaxBlocksPerCu));
     const int64_t g = std::min<int64_t>(static_cast<int64_t>(per_cu) * e->num_cus, std::max<int64_t>(ntiles, 1));
     grid = static_cast<int>(g);
     return FGD_OK;
@@ -412,7 +413,8 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     if (!e->subset.empty() && e->slot[1].kind != 2)
         return fail(FGD_ERR_UNSUPPORTED, "a Mix2 subset needs a CSR Mix2");
     fgd::KernelSet ks;
-    if (!lookup(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, c.mix1_state != 0, ks))
+    if (!lookup(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, c.mix1_state != 0,
+                !e->subset.empty(), ks))
         return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
     hipError_t herr = hipSetDevice(c.device);
     if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
@@ -448,7 +450,7 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
 
     int grid = 0;
-    if (fgd_status st = grid_for(e, ks.step, lds, p.ntiles, grid)) return st;
+    if (fgd_status st = grid_for(e, ks.step, lds, p.ntiles, grid, ks.step_blocks_per_cu)) return st;
     if (cd_out) {
         if (static_cast<size_t>(grid) * p.n_cd * c.num_workers > e->partials_capacity)
             return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
@@ -492,7 +494,7 @@ fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, d
     if ((c.ld * elem_size(dtype)) % 16 != 0) return fail(FGD_ERR_INVALID_ARG, "ld * elem_size must be a multiple of 16");
     if (reinterpret_cast<uintptr_t>(out) & 7u) return fail(FGD_ERR_INVALID_ARG, "out must be 8-byte aligned");
     fgd::KernelSet ks;
-    if (!lookup(c.num_workers, dtype, 0, 0, false, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
+    if (!lookup(c.num_workers, dtype, 0, 0, false, false, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
     hipError_t herr = hipSetDevice(c.device);
     if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
     hipStream_t stream = static_cast<hipStream_t>(stream_handle);

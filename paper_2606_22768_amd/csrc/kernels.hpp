@@ -111,7 +111,15 @@ constexpr int ilog2(int m) { return m <= 1 ? 0 : 1 + ilog2(m / 2); }
 
 // ------------------------------------------------------------ storage access
 
-constexpr int kCachePolicy = FGD_NT ? 2 : 0;  // buffer-instruction cache bits: nontemporal
+#ifndef FGD_NT_LOAD
+#define FGD_NT_LOAD FGD_NT
+#endif
+#ifndef FGD_NT_STORE
+#define FGD_NT_STORE FGD_NT
+#endif
+// Buffer-instruction cache bits of the streaming loads and stores (2: nontemporal).
+constexpr int kLoadPolicy = FGD_NT_LOAD ? 2 : 0;
+constexpr int kStorePolicy = FGD_NT_STORE ? 2 : 0;
 constexpr int kRawBufferFlags = 0x00020000;   // raw (untyped) buffer descriptor, dword 3
 
 // Descriptor of the row that starts `elem` elements (of `es` bytes) past
@@ -126,33 +134,33 @@ template <int V>
 struct F32Io {
     __device__ static void load(rsrc_t r, uint32_t off, float (&o)[V]) {
         if constexpr (V == 4) {
-            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCachePolicy);
+            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadPolicy);
 #pragma unroll
             for (int v = 0; v < 4; ++v) o[v] = __uint_as_float(t[v]);
         } else if constexpr (V == 2) {
-            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCachePolicy);
+            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kLoadPolicy);
             o[0] = __uint_as_float(t[0]);
             o[1] = __uint_as_float(t[1]);
         } else {
-            o[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCachePolicy));
+            o[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadPolicy));
         }
     }
     __device__ static void store(rsrc_t r, uint32_t off, const float (&i)[V]) {
         if constexpr (V == 4) {
             const u32x4 t = {__float_as_uint(i[0]), __float_as_uint(i[1]), __float_as_uint(i[2]), __float_as_uint(i[3])};
-            __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kCachePolicy);
+            __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kStorePolicy);
         } else if constexpr (V == 2) {
             const u32x2 t = {__float_as_uint(i[0]), __float_as_uint(i[1])};
-            __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kCachePolicy);
+            __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kStorePolicy);
         } else {
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(i[0]), r, off, 0, kCachePolicy);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(i[0]), r, off, 0, kStorePolicy);
         }
     }
     // Writes only the first n < V values (ragged end of a row).
     __device__ static void store_part(rsrc_t r, uint32_t off, int n, const float (&i)[V]) {
 #pragma unroll
         for (int v = 0; v < V; ++v)
-            if (v < n) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(i[v]), r, off + 4 * v, 0, kCachePolicy);
+            if (v < n) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(i[v]), r, off + 4 * v, 0, kStorePolicy);
     }
 };
 
@@ -188,24 +196,24 @@ struct ParamBF16 {
     static constexpr int kElem = 2;
     __device__ static void load(rsrc_t r, uint32_t off, float (&o)[V]) {
         if constexpr (V == 8) {
-            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCachePolicy);
+            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadPolicy);
 #pragma unroll
             for (int k = 0; k < 4; ++k) { o[2 * k] = bf16_lo(t[k]); o[2 * k + 1] = bf16_hi(t[k]); }
         } else if constexpr (V == 4) {
-            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCachePolicy);
+            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kLoadPolicy);
             o[0] = bf16_lo(t[0]); o[1] = bf16_hi(t[0]); o[2] = bf16_lo(t[1]); o[3] = bf16_hi(t[1]);
         } else if constexpr (V == 2) {
-            const uint32_t t = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCachePolicy);
+            const uint32_t t = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadPolicy);
             o[0] = bf16_lo(t); o[1] = bf16_hi(t);
         } else {
-            const uint16_t t = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kCachePolicy);
+            const uint16_t t = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kLoadPolicy);
             o[0] = __uint_as_float(static_cast<uint32_t>(t) << 16);
         }
     }
     __device__ static void store(rsrc_t r, uint32_t off, const float (&i)[V], float (&s)[V]) {
         if constexpr (V == 1) {
             const uint32_t w = pack_bf16(i[0], 0.0f);
-            __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(w & 0xFFFFu), r, off, 0, kCachePolicy);
+            __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(w & 0xFFFFu), r, off, 0, kStorePolicy);
             s[0] = bf16_lo(w);
         } else {
             uint32_t w[V / 2];
@@ -217,12 +225,12 @@ struct ParamBF16 {
             }
             if constexpr (V == 8) {
                 const u32x4 t = {w[0], w[1], w[2], w[3]};
-                __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kCachePolicy);
+                __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kStorePolicy);
             } else if constexpr (V == 4) {
                 const u32x2 t = {w[0], w[1]};
-                __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kCachePolicy);
+                __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kStorePolicy);
             } else {
-                __builtin_amdgcn_raw_buffer_store_b32(w[0], r, off, 0, kCachePolicy);
+                __builtin_amdgcn_raw_buffer_store_b32(w[0], r, off, 0, kStorePolicy);
             }
         }
     }
@@ -231,7 +239,7 @@ struct ParamBF16 {
         for (int v = 0; v < V; ++v) {
             const uint32_t w = pack_bf16(i[v], 0.0f);
             if (v < n) __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(w & 0xFFFFu), r, off + 2 * v, 0,
-                                                             kCachePolicy);
+                                                             kStorePolicy);
             s[v] = v < n ? bf16_lo(w) : 0.0f;
         }
     }
@@ -653,11 +661,17 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
 // Parameter segments of a Mix2 subset, read as scalar loads (never written).
 typedef const __attribute__((address_space(4))) int64_t *const_seg_ptr;
 
+// Step-kernel variant flags.
+constexpr int kMixState = 1;  // Mix1 also mixes the optimizer state
+constexpr int kSubset = 2;    // Mix2 may be restricted to a parameter subset
+
 // K1, K2: compile-time kinds of Mix1 and Mix2 (kAny = decided at run time).
-// MS: the optimizer state is mixed by Mix1.
-template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, bool MS>
+// FLAGS: kMixState | kSubset.
+template <int MMAX, bool EXACT, int V, class PIO, int K1, int K2, int FLAGS>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(waves_per_simd_target(MMAX))))
 void outer_step_kernel(StepParams a) {
+    constexpr bool MS = (FLAGS & kMixState) != 0;
+    constexpr bool SUB = (FLAGS & kSubset) != 0 && (K2 == kTable || K2 == kAny);
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     constexpr int MP = pow2_at_least(MMAX);
     constexpr int kCdStride = kWavesPerBlock * MP;
@@ -688,7 +702,7 @@ void outer_step_kernel(StepParams a) {
     for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
         const int64_t tb = tile * kTile;  // first parameter of the tile (uniform)
         uint32_t keep = 0;                // elements of this lane outside the Mix2 subset
-        if constexpr (K2 == kTable || K2 == kAny) {
+        if constexpr (SUB) {
             if (a.n_seg > 0) {
                 const int64_t te = tb + kTile < a.P ? tb + kTile : a.P;
                 while (s < a.n_seg && seg[2 * s + 1] <= tb) ++s;
@@ -779,48 +793,73 @@ struct KernelSet {
     const void *consensus;  // consensus_kernel instantiation
     int v;                  // elements per lane per row
     int mmax;               // compile-time worker bound
+    int step_blocks_per_cu; // cap on resident step blocks per compute unit
 };
+
+#ifndef FGD_STEP_BLOCKS_PER_CU_SMALL
+#define FGD_STEP_BLOCKS_PER_CU_SMALL 1
+#endif
+// Step blocks per compute unit.  Up to 16 workers a block streams 3M rows of
+// 16-byte (8-byte bf16) accesses per tile, all issued before first use, which
+// keeps enough bytes in flight with one block per CU; more resident blocks
+// only add DRAM contention (measured 5-7% slower with 4 at 8 workers).  With
+// 32 or 64 workers a lane holds one or two parameters and the rows are
+// gathered through LDS, so a second block is needed to cover that latency.
+constexpr int step_blocks_per_cu(int mmax) { return mmax <= 16 ? FGD_STEP_BLOCKS_PER_CU_SMALL : 8; }
 
 // Kernel set of one instantiation; the step kernel is specialised on the
 // (Mix1, Mix2) kinds of the paper's configurations (Appendix A table:
-// GlobalM1LocalM2, LocalM1M2, GlobalM1, DiLoCo) when M is exact.
+// GlobalM1LocalM2, LocalM1M2, GlobalM1, DiLoCo) when M is exact.  `subset`:
+// a Mix2 subset is set; only GlobalM1LocalM2 has a specialisation for it
+// (the paper's subset configuration), the rest run on the run-time-kind
+// kernel, which always handles subsets.
 template <template <int> class PIOT, int MMAX, bool EXACT, int V>
-KernelSet make_kernel_set(int k1, int k2) {
+KernelSet make_kernel_set(int k1, int k2, bool subset) {
     using P = PIOT<V>;
     KernelSet ks;
-    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny, false>);
+    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny, kSubset>);
     if constexpr (EXACT) {
-        if (k1 == kGlobal && k2 == kTable)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, false>);
-        else if (k1 == kTable && k2 == kTable)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kTable, kTable, false>);
-        else if (k1 == kGlobal && k2 == kIdentity)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity, false>);
-        else if (k1 == kIdentity && k2 == kGlobal)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kIdentity, kGlobal, false>);
+        if (subset) {
+            if (k1 == kGlobal && k2 == kTable)
+                ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, kSubset>);
+        } else if (k1 == kGlobal && k2 == kTable) {
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, 0>);
+        } else if (k1 == kTable && k2 == kTable) {
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kTable, kTable, 0>);
+        } else if (k1 == kGlobal && k2 == kIdentity) {
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity, 0>);
+        } else if (k1 == kIdentity && k2 == kGlobal) {
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kIdentity, kGlobal, 0>);
+        }
     }
     ks.consensus = reinterpret_cast<const void *>(&consensus_kernel<MMAX, EXACT, V, P>);
     ks.v = V;
     ks.mmax = MMAX;
+    ks.step_blocks_per_cu = step_blocks_per_cu(MMAX);
     return ks;
 }
 
-// The same with the optimizer state mixed by Mix1 (Appendix B: GlobalM1S and
-// GlobalM1SLocalM2 are specialised when M is exact).
+// The same with the optimizer state mixed by Mix1 (Appendix B: GlobalM1S,
+// GlobalM1SLocalM2 and GlobalM1SLocalM2-subset are specialised when M is
+// exact).
 template <template <int> class PIOT, int MMAX, bool EXACT, int V>
-KernelSet make_kernel_set_ms(int k1, int k2) {
+KernelSet make_kernel_set_ms(int k1, int k2, bool subset) {
     using P = PIOT<V>;
+    constexpr int MSF = kMixState;
     KernelSet ks;
-    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny, true>);
+    ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kAny, kAny, MSF | kSubset>);
     if constexpr (EXACT) {
         if (k1 == kGlobal && k2 == kTable)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, true>);
-        else if (k1 == kGlobal && k2 == kIdentity)
-            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity, true>);
+            ks.step = subset ? reinterpret_cast<const void *>(
+                                   &outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, MSF | kSubset>)
+                             : reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kTable, MSF>);
+        else if (k1 == kGlobal && k2 == kIdentity && !subset)
+            ks.step = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kGlobal, kIdentity, MSF>);
     }
     ks.consensus = reinterpret_cast<const void *>(&consensus_kernel<MMAX, EXACT, V, P>);
     ks.v = V;
     ks.mmax = MMAX;
+    ks.step_blocks_per_cu = step_blocks_per_cu(MMAX);
     return ks;
 }
 
@@ -836,30 +875,31 @@ constexpr int lanes_v_bf16(int mmax) {
 // workers: exact for M in {1, 2, 4, 8, 16, 32, 64}, else the next power of
 // two with M read at run time.
 template <class F>
-bool select_workers(int M, int k1, int k2, KernelSet *out) {
+bool select_workers(int M, int k1, int k2, bool subset, KernelSet *out) {
     if (M < 1 || M > 64) return false;
-    if (M == 1) *out = F::template get<1, true>(k1, k2);
-    else if (M == 2) *out = F::template get<2, true>(k1, k2);
-    else if (M == 3) *out = F::template get<4, false>(k1, k2);
-    else if (M == 4) *out = F::template get<4, true>(k1, k2);
-    else if (M < 8) *out = F::template get<8, false>(k1, k2);
-    else if (M == 8) *out = F::template get<8, true>(k1, k2);
-    else if (M < 16) *out = F::template get<16, false>(k1, k2);
-    else if (M == 16) *out = F::template get<16, true>(k1, k2);
-    else if (M < 32) *out = F::template get<32, false>(k1, k2);
-    else if (M == 32) *out = F::template get<32, true>(k1, k2);
-    else if (M < 64) *out = F::template get<64, false>(k1, k2);
-    else *out = F::template get<64, true>(k1, k2);
+    if (M == 1) *out = F::template get<1, true>(k1, k2, subset);
+    else if (M == 2) *out = F::template get<2, true>(k1, k2, subset);
+    else if (M == 3) *out = F::template get<4, false>(k1, k2, subset);
+    else if (M == 4) *out = F::template get<4, true>(k1, k2, subset);
+    else if (M < 8) *out = F::template get<8, false>(k1, k2, subset);
+    else if (M == 8) *out = F::template get<8, true>(k1, k2, subset);
+    else if (M < 16) *out = F::template get<16, false>(k1, k2, subset);
+    else if (M == 16) *out = F::template get<16, true>(k1, k2, subset);
+    else if (M < 32) *out = F::template get<32, false>(k1, k2, subset);
+    else if (M == 32) *out = F::template get<32, true>(k1, k2, subset);
+    else if (M < 64) *out = F::template get<64, false>(k1, k2, subset);
+    else *out = F::template get<64, true>(k1, k2, subset);
     return true;
 }
 
 // Defined per storage type.  k1, k2: Mix kinds (kIdentity, kGlobal, kTable);
-// a specialised step kernel is returned when one exists, else the one that
-// reads the kinds at run time.  Returns false if M is outside [1, 64].
-bool kernels_f32(int M, int k1, int k2, KernelSet *out);
-bool kernels_bf16(int M, int k1, int k2, KernelSet *out);
+// subset: a Mix2 subset is set.  A specialised step kernel is returned when
+// one exists, else the one that reads the kinds at run time.  Returns false
+// if M is outside [1, 64].
+bool kernels_f32(int M, int k1, int k2, bool subset, KernelSet *out);
+bool kernels_bf16(int M, int k1, int k2, bool subset, KernelSet *out);
 // Step kernels that also mix the optimizer state with Mix1.
-bool kernels_f32_ms(int M, int k1, int k2, KernelSet *out);
-bool kernels_bf16_ms(int M, int k1, int k2, KernelSet *out);
+bool kernels_f32_ms(int M, int k1, int k2, bool subset, KernelSet *out);
+bool kernels_bf16_ms(int M, int k1, int k2, bool subset, KernelSet *out);
 
 }  // namespace fgd

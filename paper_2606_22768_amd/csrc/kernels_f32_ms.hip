@@ -7,12 +7,14 @@ namespace fgd {
 namespace {
 struct Sets {
     template <int MMAX, bool EXACT>
-    static KernelSet get(int k1, int k2) {
-        return make_kernel_set_ms<ParamF32, MMAX, EXACT, lanes_v_f32(MMAX)>(k1, k2);
+    static KernelSet get(int k1, int k2, bool subset) {
+        return make_kernel_set_ms<ParamF32, MMAX, EXACT, lanes_v_f32(MMAX)>(k1, k2, subset);
     }
 };
 }  // namespace
 
-bool kernels_f32_ms(int M, int k1, int k2, KernelSet *out) { return select_workers<Sets>(M, k1, k2, out); }
+bool kernels_f32_ms(int M, int k1, int k2, bool subset, KernelSet *out) {
+    return select_workers<Sets>(M, k1, k2, subset, out);
+}
 
 }  // namespace fgd

@@ -1,4 +1,4 @@
-"""The five outer-step workloads, as data.
+"""The five outer-step workloads and the step variants measured on the largest, as data.
 
 Each entry states the worker count M, the parameter count P per worker, the
 storage dtype, the input distributions, the (Mix1, Mix2) topologies and rounds,
@@ -49,6 +49,28 @@ WORKLOADS = {
         M=64, P=124_000_000, dtype="f32", prev_std=0.02, drift_std=2e-3, mom_std=1e-4, seed=0,
         mix1=("regular", "metropolis", 4), k1=1, mix2=("regular", "metropolis", 4), k2=3),
 }
+
+# Step variants on the 8 x 1.1e9 bf16 workload (same inputs and topologies):
+#   subset43   GlobalM1LocalM2-subset: Mix2 on 43% of the parameters, as two
+#              blocks at the two ends of the flattened vector (the paper's
+#              subset is the token embeddings and first two layers at the
+#              front plus the LM head at the back, 43% of a 1.5B model)
+#   m1s        GlobalM1SLocalM2: the momentum is averaged by Mix1 too
+#   m1s_subset43  both
+SUBSET43 = ((0.0, 0.33), (0.90, 1.0))
+for _name, _extra in (("subset43", dict(subset=SUBSET43)), ("m1s", dict(mix1_state=True)),
+                      ("m1s_subset43", dict(subset=SUBSET43, mix1_state=True))):
+    WORKLOADS["m8_p1100m_bf16_" + _name] = dict(WORKLOADS["m8_p1100m_bf16"], **_extra)
+
+
+def subset_segments(w):
+    """[n][2] int64 Mix2 subset segments of a workload (None: Mix2 everywhere).
+    Fractions of P are rounded down to multiples of 8 parameters."""
+    if not w.get("subset"):
+        return None
+    P = w["P"]
+    cut = lambda f: min(P, int(f * P) // 8 * 8)
+    return np.array([(cut(a), cut(b) if b < 1.0 else P) for a, b in w["subset"]], dtype=np.int64)
 
 
 def regular4_m64():

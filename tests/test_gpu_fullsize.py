@@ -13,7 +13,10 @@ hold at any size:
   - theta' row = standalone consensus kernel on the stored output;
   - a global-mean round leaves an exactly zero row;
   - each CSR round contracts: S(W u) <= sigma_2(W)^2 S(u), sigma_2 from the
-    round's effective weights (Sec. 3 contraction factor).
+    round's effective weights (Sec. 3 contraction factor); with a Mix2 subset
+    only S(round) <= S(input) holds, since the rest passes through.
+The step variants (Mix1 over the momentum, Mix2 on a 43% subset) run on the
+8 x 1.1e9 bf16 inputs.
 """
 
 import gc
@@ -28,7 +31,7 @@ from tests import _parity as pa
 
 pytestmark = pytest.mark.gpu
 
-WORKLOADS = ["m8_p150m_f32", "m16_p500m_f32", "m8_p1100m_bf16", "m64_p124m_f32"]
+WORKLOADS = ["m8_p150m_f32", "m16_p500m_f32", "m8_p1100m_bf16", "m64_p124m_f32", "m8_p1100m_bf16_m1s_subset43"]
 
 
 @pytest.fixture(scope="module")
@@ -47,6 +50,26 @@ def _sample_columns(P, seed, n_edge=2048, n_random=8192):
     cols |= set(range(max(0, P - n_edge), P))
     cols |= set(rng.integers(0, P, n_random).tolist())
     return np.array(sorted(cols), dtype=np.int64)
+
+
+def _segments_in_sample(cols, segs):
+    """The subset as segments of the gathered column index space."""
+    if segs is None:
+        return None
+    inside = np.zeros(len(cols), dtype=bool)
+    for b, e in segs.tolist():
+        inside |= (cols >= b) & (cols < e)
+    out, j = [], 0
+    while j < len(cols):
+        if inside[j]:
+            k = j
+            while k < len(cols) and inside[k]:
+                k += 1
+            out.append((j, k))
+            j = k
+        else:
+            j += 1
+    return out
 
 
 def _host(t, dtype):
@@ -78,9 +101,13 @@ def test_fullsize_step(env, workload):
 
     t1 = configs.topology(w["mix1"], M, w["k1"], w["seed"])
     t2 = configs.topology(w["mix2"], M, w["k2"], w["seed"], step=0)
-    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0)
+    state = bool(w.get("mix1_state"))
+    segs = configs.subset_segments(w)
+    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0, mix1_state=state)
     eng.set_topology_dict("mix1", t1)
     eng.set_topology_dict("mix2", t2)
+    if segs is not None:
+        eng.set_mix2_subset(segs)
     n_rows = eng.num_cd_rows()
 
     # Standalone consensus of the inputs, by a different kernel.
@@ -108,8 +135,11 @@ def test_fullsize_step(env, workload):
     cd = cd.cpu().numpy()
 
     # Element-by-element parity on the sampled columns.
-    ref_t, ref_v, _ = oracle.outer_step(s_tp, s_tl, s_v, oracle.Mix.from_topology(t1), oracle.Mix.from_topology(t2),
-                                        lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=dtype)
+    s_segs = _segments_in_sample(cols, segs)
+    m2 = oracle.Mix.from_topology(t2) if (s_segs is None or s_segs) else oracle.Mix("identity")
+    ref_t, ref_v, _ = oracle.outer_step(s_tp, s_tl, s_v, oracle.Mix.from_topology(t1), m2,
+                                        lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=dtype, mix1_state=state,
+                                        subset=s_segs if s_segs else None)
     scale = float(np.abs(tensors.bf16_bits_to_f32(s_tp) if dtype == "bf16" else s_tp).max())
     pa.compare_outputs(dtype, got_t, ref_t, got_v, ref_v, len(cols), scale)
 
@@ -129,6 +159,8 @@ def test_fullsize_step(env, workload):
                 continue
             which = "mix2" if t is t2 else "mix1"
             s2 = _sigma2(t["row_ptr"], t["col_idx"], eng.effective_weights(which, k))
+            if which == "mix2" and segs is not None:
+                s2 = 1.0
             assert after <= s2 ** 2 * before * (1 + 1e-5), (workload, which, k, after / before, s2 ** 2)
     print(f"[fullsize] {workload}: ok, consensus rows {np.round(cd.mean(axis=1), 6).tolist()}", flush=True)
     eng.close()
