@@ -73,6 +73,15 @@ def lib():
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.POINTER(_Mix), ctypes.POINTER(_Mix), ctypes.POINTER(_Opts),
                                       ctypes.c_void_p]
+        L.fgdo_mix1_split.restype = ctypes.c_int
+        L.fgdo_mix1_split.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(_Mix),
+                                      ctypes.c_int32, ctypes.c_void_p]
+        L.fgdo_outer_blocking.restype = ctypes.c_int
+        L.fgdo_outer_blocking.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.POINTER(_Mix), ctypes.POINTER(_Opts), ctypes.c_int32,
+                                          ctypes.c_void_p]
         L.fgdo_consensus.restype = ctypes.c_int
         L.fgdo_consensus.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                      ctypes.c_void_p, ctypes.c_void_p]
@@ -182,6 +191,48 @@ def outer_step(theta_prev, theta_local, mom, mix1: Mix, mix2: Mix, lr=0.7, mu=0.
     if rc:
         raise ValueError(f"oracle outer step failed (rc={rc})")
     return tp, v, cd
+
+
+def mix1_split(theta_prev, mix1: Mix, mom=None, mix1_state=False, P=None, dtype=None):
+    """First half of split execution: returns (x stored in the parameter type,
+    momentum after the optional state mix (a copy), cd[K1 + 1, M])."""
+    tp = np.ascontiguousarray(theta_prev)
+    if dtype is None:
+        dtype = "bf16" if tp.dtype == np.uint16 else "f32"
+    M, ld = tp.shape
+    P = ld if P is None else P
+    x = np.array(tp, copy=True)  # same type and shape; every [0, P) entry is overwritten
+    v = None if mom is None else np.array(mom, dtype=np.float32, copy=True, order="C")
+    cd = np.zeros((mix1.effective_rounds() + 1, M), dtype=np.float64)
+    c1 = mix1.c()
+    rc = lib().fgdo_mix1_split(M, P, ld, 1 if dtype == "bf16" else 0, _ptr(tp), _ptr(x), _ptr(v), ctypes.byref(c1),
+                               1 if mix1_state else 0, _ptr(cd))
+    if rc:
+        raise ValueError(f"oracle Mix1 failed (rc={rc})")
+    return x, v, cd
+
+
+def outer_blocking(x, theta_prev, theta_local, mom, mix2: Mix, lr=0.7, mu=0.9, P=None, dtype=None, nesterov=True,
+                   subset=None, write_local=False):
+    """Second half of split execution.  Returns copies (theta', theta_local
+    after the optional write-back, v', cd[K2 + 2, M])."""
+    tp = np.array(theta_prev, copy=True, order="C")
+    tl = np.array(theta_local, copy=True, order="C")
+    xx = np.ascontiguousarray(x)
+    v = np.array(mom, dtype=np.float32, copy=True, order="C")
+    if dtype is None:
+        dtype = "bf16" if tp.dtype == np.uint16 else "f32"
+    M, ld = tp.shape
+    P = ld if P is None else P
+    cd = np.zeros((mix2.effective_rounds() + 2, M), dtype=np.float64)
+    c2 = mix2.c()
+    seg = subset_array(subset)
+    opts = _Opts(float(lr), float(mu), 1 if nesterov else 0, 0, 0 if seg is None else seg.shape[0], _ptr(seg))
+    rc = lib().fgdo_outer_blocking(M, P, ld, 1 if dtype == "bf16" else 0, _ptr(xx), _ptr(tp), _ptr(tl), _ptr(v),
+                                   ctypes.byref(c2), ctypes.byref(opts), 1 if write_local else 0, _ptr(cd))
+    if rc:
+        raise ValueError(f"oracle blocking step failed (rc={rc})")
+    return tp, tl, v, cd
 
 
 def consensus(x, P=None, dtype=None):

@@ -29,6 +29,14 @@
  *        - Mix2 subset: Mix2 acts only on the parameter indices inside a
  *          list of half-open segments [begin, end); elsewhere it is the
  *          identity, in every round.
+ *      Split execution (Appendix A, Algorithm 1: the non-blocking Mix1 is
+ *      launched at the start of the round and overlaps the inner loop; the
+ *      blocking Mix2 and the outer optimizer run at its end):
+ *        - fgdo_mix1_split stores x = Mix1(theta_prev) in the parameter
+ *          storage type (and, with the state mixed, v <- Mix1(v));
+ *        - fgdo_outer_blocking computes g0, Mix2 and the optimizer from
+ *          that stored x, and can write theta' back into theta_local as the
+ *          next round's inner starting point.
  *   5. Consensus distance S_m(u) = sum_p (u_m - mean_n u_n)^2 for every
  *      intermediate u (Sec. 4.4 L2 consensus distance; Appendix D.1 uses the
  *      mean of the squared norms, Sec. 4.4 the mean of the norms; both follow
@@ -456,6 +464,100 @@ done:
     free(inset);
     free(cd2);
     free(cd1);
+    return rc;
+}
+
+/* Split execution, first half: x = Mix1(theta_prev) rounded to the
+ * parameter storage type into x_out [M][ld]; with mix1_state, the momentum
+ * [M][ld] is replaced by Mix1 of itself (rounded to float).  cd: [(K1+1)][M]
+ * consensus rows x^0..x^K1 of the unrounded values, or NULL. */
+int fgdo_mix1_split(int32_t M, int64_t P, int64_t ld, int32_t dtype, const void *theta_prev, void *x_out,
+                    float *mom, const fgdo_mix *mix1, int32_t mix1_state, double *cd)
+{
+    if (M <= 0 || P < 0 || ld < P || (dtype != 0 && dtype != 1)) return FGDO_BAD_ARG;
+    if (!theta_prev || !x_out || (mix1_state && !mom)) return FGDO_BAD_ARG;
+    if (check_mix(M, mix1)) return FGDO_BAD_ARG;
+    int64_t n = (int64_t)M * P;
+    size_t bytes = (size_t)(n > 0 ? n : 1) * sizeof(double);
+    double *z = (double *)malloc(bytes), *x = (double *)malloc(bytes);
+    int rc = FGDO_OK;
+    if (!z || !x) {
+        rc = FGDO_NO_MEM;
+        goto done;
+    }
+    for (int32_t m = 0; m < M; ++m)
+        for (int64_t p = 0; p < P; ++p) z[(int64_t)m * P + p] = load_param(theta_prev, dtype, (int64_t)m * ld + p);
+    rc = fgdo_mix_apply(M, P, mix1, z, x, cd);
+    if (rc) goto done;
+    for (int32_t m = 0; m < M; ++m)
+        for (int64_t p = 0; p < P; ++p) store_param(x_out, dtype, (int64_t)m * ld + p, x[(int64_t)m * P + p]);
+    if (mix1_state) {
+        for (int32_t m = 0; m < M; ++m)
+            for (int64_t p = 0; p < P; ++p) z[(int64_t)m * P + p] = (double)mom[(int64_t)m * ld + p];
+        rc = fgdo_mix_apply(M, P, mix1, z, x, NULL);
+        if (rc) goto done;
+        for (int32_t m = 0; m < M; ++m)
+            for (int64_t p = 0; p < P; ++p) mom[(int64_t)m * ld + p] = (float)x[(int64_t)m * P + p];
+    }
+done:
+    free(z);
+    free(x);
+    return rc;
+}
+
+/* Split execution, second half (blocking): from the stored x [M][ld],
+ * g0 = theta_prev - theta_local, ghat = Mix2(g0) (on the subset if any), the
+ * optimizer update into theta_prev and mom; with write_local, theta_local
+ * receives theta' as stored.  cd: [(K2+2)][M] rows g^0..g^K2 and the stored
+ * theta', or NULL.  opt->mix1_state is ignored (the state is mixed by the
+ * first half). */
+int fgdo_outer_blocking(int32_t M, int64_t P, int64_t ld, int32_t dtype, const void *x_in, void *theta_prev,
+                        void *theta_local, float *mom, const fgdo_mix *mix2, const fgdo_opts *opt,
+                        int32_t write_local, double *cd)
+{
+    if (M <= 0 || P < 0 || ld < P || (dtype != 0 && dtype != 1)) return FGDO_BAD_ARG;
+    if (!x_in || !theta_prev || !theta_local || !mom || !opt) return FGDO_BAD_ARG;
+    if (check_mix(M, mix2)) return FGDO_BAD_ARG;
+    int64_t n = (int64_t)M * P;
+    size_t bytes = (size_t)(n > 0 ? n : 1) * sizeof(double);
+    double *g0 = (double *)malloc(bytes), *ghat = (double *)malloc(bytes), *theta_new = (double *)malloc(bytes);
+    uint8_t *inset = opt->n_seg > 0 ? (uint8_t *)malloc((size_t)(P > 0 ? P : 1)) : NULL;
+    int K2 = effective_rounds(mix2);
+    int rc = FGDO_OK;
+    if (!g0 || !ghat || !theta_new || (opt->n_seg > 0 && !inset)) {
+        rc = FGDO_NO_MEM;
+        goto done;
+    }
+    if (inset) {
+        rc = subset_flags(P, opt->n_seg, opt->seg, inset);
+        if (rc) goto done;
+    }
+    for (int32_t m = 0; m < M; ++m)
+        for (int64_t p = 0; p < P; ++p)
+            g0[(int64_t)m * P + p] = load_param(theta_prev, dtype, (int64_t)m * ld + p) -
+                                     load_param(theta_local, dtype, (int64_t)m * ld + p);
+    rc = fgdo_mix_apply_subset(M, P, mix2, inset, g0, ghat, cd);
+    if (rc) goto done;
+    {
+        double dmu = (double)opt->mu, dlr = (double)opt->lr;
+        for (int32_t m = 0; m < M; ++m)
+            for (int64_t p = 0; p < P; ++p) {
+                int64_t i = (int64_t)m * P + p, j = (int64_t)m * ld + p;
+                double g = ghat[i], x = load_param(x_in, dtype, j);
+                double v_new = dmu * (double)mom[j] + g;
+                double t_new = opt->nesterov ? x - dlr * (g + dmu * v_new) : x - dlr * v_new;
+                mom[j] = (float)v_new;
+                store_param(theta_prev, dtype, j, t_new);
+                theta_new[i] = load_param(theta_prev, dtype, j);
+                if (write_local) store_param(theta_local, dtype, j, t_new);
+            }
+    }
+    if (cd) consensus_sq(M, P, theta_new, cd + (int64_t)(K2 + 1) * M);
+done:
+    free(g0);
+    free(ghat);
+    free(theta_new);
+    free(inset);
     return rc;
 }
 

@@ -207,3 +207,72 @@ def test_subset_rejects_bad_segments(segs):
     tp, tl, v = tensors.numpy_inputs(M, P, seed=1)
     with pytest.raises(ValueError):
         oracle.outer_step(tp, tl, v, oracle.Mix("global"), oracle.Mix("global"), subset=segs)
+
+
+# ---------------------------------------------------------- split execution
+
+def _store(a, dtype):
+    """Rounded to the parameter storage type, back in float64 (torch's RNE casts)."""
+    t = torch.from_numpy(np.asarray(a, np.float64))
+    return (t.to(torch.bfloat16) if dtype == "bf16" else t.to(torch.float32)).to(torch.float64).numpy()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("state", [False, True])
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_split_halves_match_torch_from_stored_x(dtype, state, nesterov):
+    """Algorithm 1 split: x = W1^2 theta stored in the parameter type, the
+    state (optionally) replaced by W1^2 v in float32, then the blocking half
+    from the stored x with ghat = W2 g0 on a subset: worker m's result is
+    torch's SGD step from the stored x_m, gradient ghat_m, buffer v_m.
+    Consensus rows against brute-force sums."""
+    M, P = 8, 900
+    tp, tl, v = tensors.numpy_inputs(M, P, dtype=dtype, mom_std=1e-3, seed=47)
+    f = tensors.bf16_bits_to_f32 if dtype == "bf16" else (lambda a: a)
+    rp1, ci1, w1 = graphs.exponential_weights(M, hops=(1, 2, 4))
+    rp2, ci2, w2 = graphs.ring_weights(M)
+    m1 = oracle.Mix("csr", rp1, ci1, w1, rounds=2)
+    m2 = oracle.Mix("csr", rp2, ci2, w2, rounds=1)
+    segs = [(0, 300), (600, 901 - 1)]
+    x, v1, cd1 = oracle.mix1_split(tp, m1, mom=v, mix1_state=state)
+    tq, tlq, vq, cd2 = oracle.outer_blocking(x, tp, tl, v1 if state else v, m2, lr=LR, mu=MU, nesterov=nesterov,
+                                             subset=segs, write_local=True)
+
+    W1, W2 = dense_W(rp1, ci1, w1), dense_W(rp2, ci2, w2)
+    th = f(tp).astype(np.float64)
+    xd = W1 @ (W1 @ th)
+    np.testing.assert_array_equal(f(x).astype(np.float64), _store(xd, dtype))
+    for k, u in enumerate([th, W1 @ th, xd]):
+        np.testing.assert_allclose(cd1[k], ((u - u.mean(axis=0)) ** 2).sum(axis=1), rtol=1e-12)
+    vb = _store(W1 @ (W1 @ v.astype(np.float64)), "f32") if state else v.astype(np.float64)
+    if state:
+        np.testing.assert_array_equal(v1.astype(np.float64), vb)
+    g0 = th - f(tl).astype(np.float64)
+    inset = np.zeros(P, bool)
+    for b, e in segs:
+        inset[b:e] = True
+    gh = np.where(inset, W2 @ g0, g0)
+    for m in range(M):
+        want_t, want_v = torch_sgd(_store(xd[m], dtype), gh[m], vb[m], nesterov)
+        close(vq[m], want_v, ulps=4)
+        if dtype == "bf16":
+            want_bits = np.array([oracle.bf16_from_double(t) for t in want_t], dtype=np.uint16)
+            d = np.abs(want_bits.astype(np.int32) - tq[m].astype(np.int32))
+            assert d.max() <= 1  # torch's double result may sit on the other side of a tie
+        else:
+            close(tq[m], want_t, ulps=4)
+    assert np.array_equal(tlq, tq)  # theta' written back as the next inner start
+    np.testing.assert_allclose(cd2[0], ((g0 - g0.mean(axis=0)) ** 2).sum(axis=1), rtol=1e-12)
+    np.testing.assert_allclose(cd2[1], ((gh - gh.mean(axis=0)) ** 2).sum(axis=1), rtol=1e-12)
+    ts = f(tq).astype(np.float64)
+    np.testing.assert_allclose(cd2[2], ((ts - ts.mean(axis=0)) ** 2).sum(axis=1), rtol=1e-12)
+
+
+def test_split_without_write_back_keeps_theta_local():
+    M, P = 4, 128
+    tp, tl, v = tensors.numpy_inputs(M, P, mom_std=1e-3, seed=3)
+    x, _, _ = oracle.mix1_split(tp, oracle.Mix("global"))
+    _, tlq, _, _ = oracle.outer_blocking(x, tp, tl, v, oracle.Mix("global"))
+    assert np.array_equal(tlq, tl)
+    # A global Mix1 stores the same x for every worker.
+    assert np.all(x == x[0])
