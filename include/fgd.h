@@ -180,6 +180,54 @@ fgd_status fgd_num_cd_rows(const fgd_engine *e, int32_t *n_rows);
 fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
                           double *cd_out, void *stream);
 
+/* Split execution of a round (Appendix A, Algorithm 1): the non-blocking
+ * Mix1 is launched at the start of the round, typically on its own stream so
+ * that it overlaps the inner steps, and the blocking Mix2 and the outer
+ * optimizer run at the end of the round from the Mix1 output it stored.
+ * Compared with fgd_outer_step this moves M * P * 3 * elem_size more bytes
+ * (x written and read back, theta_prev read twice); the two halves give the
+ * same result as the fused step up to the rounding of x to the storage type.
+ * The caller orders the halves: the blocking half must not start before the
+ * Mix1 half of the same round is complete, and the next Mix1 half must not
+ * start before the blocking half that produced its theta_prev. */
+
+/* Mix1 half: x_out = Mix1(theta_prev), rounded to the storage type.
+ *   theta_prev  device [M][ld] param_dtype, read
+ *   x_out       device [M][ld] param_dtype, written; must not overlap theta_prev
+ *   momentum    device [M][ld] float32: with mix1_state it is replaced by
+ *               Mix1(momentum) (the state is mixed here, not in the blocking
+ *               half); otherwise ignored and may be NULL
+ *   cd_out      device double[K1 + 1][M] or NULL: rows x^0..x^K1 (consensus
+ *               of the unrounded Mix1 intermediates)
+ * Enqueued on `stream`. */
+fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *momentum, double *cd_out,
+                    void *stream);
+
+/* Blocking half: g0 = theta_prev - theta_local, ghat = Mix2(g0) (on the
+ * subset if one is set), v' = mu v + ghat, theta' = x - lr (ghat + mu v')
+ * (plain momentum: x - lr v'), with x read from the array fgd_mix1 stored.
+ *   x            device [M][ld] param_dtype, read
+ *   theta_prev   device [M][ld] param_dtype, read and overwritten with theta'
+ *   theta_local  device [M][ld] param_dtype, read; with write_local = 1 it
+ *                also receives theta' as stored (the next round's inner
+ *                starting point, y_0 = z)
+ *   momentum     device [M][ld] float32, read and overwritten with v'
+ *   cd_out       device double[K2 + 2][M] or NULL: rows g^0..g^K2 and the
+ *                stored theta'
+ * No two arrays may overlap.  Enqueued on `stream`. */
+fgd_status fgd_outer_step_blocking(fgd_engine *e, const void *x, void *theta_prev, void *theta_local, float *momentum,
+                                   double *cd_out, int32_t write_local, void *stream);
+
+/* Consensus rows of the two halves: K1 + 1 and K2 + 2 (GLOBAL_MEAN counts as
+ * one round, IDENTITY as zero).  Needs both slots set. */
+fgd_status fgd_num_cd_rows_split(const fgd_engine *e, int32_t *mix1_rows, int32_t *blocking_rows);
+
+/* Algorithmic minimum HBM traffic of the two halves:
+ *   Mix1 half      M * P * (2 * elem_size + (mix1_state ? 8 : 0))
+ *   blocking half  M * P * (4 * elem_size + 8 + (write_local ? elem_size : 0)) */
+fgd_status fgd_min_bytes_split(const fgd_engine *e, int32_t write_local, int64_t *mix1_bytes,
+                               int64_t *blocking_bytes);
+
 /* S_m = sum_p (x_m,p - mean_n x_n,p)^2 of a device [M][ld] array of the
  * given dtype, written to device double out[M], enqueued on `stream`
  * (Sec. 4.4; Appendix D.1). */

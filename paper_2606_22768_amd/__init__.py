@@ -64,6 +64,10 @@ def _load():
         "fgd_set_mix2_subset": (I32, [P, P, I32]),
         "fgd_num_cd_rows": (I32, [P, ctypes.POINTER(I32)]),
         "fgd_outer_step": (I32, [P, P, P, P, P, P]),
+        "fgd_mix1": (I32, [P, P, P, P, P, P]),
+        "fgd_outer_step_blocking": (I32, [P, P, P, P, P, P, I32, P]),
+        "fgd_num_cd_rows_split": (I32, [P, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+        "fgd_min_bytes_split": (I32, [P, I32, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
         "fgd_consensus_distance": (I32, [P, P, I32, P, P]),
         "fgd_get_effective_weights": (I32, [P, I32, I32, P]),
         "fgd_effective_weights": (I32, [I32, P, P, P, P, I32, P]),
@@ -170,6 +174,29 @@ def fgd_outer_step(h, theta_prev, theta_local, momentum, cd_out=None, stream=Non
                               _stream(stream)), "fgd_outer_step")
 
 
+def fgd_mix1(h, theta_prev, x_out, momentum=None, cd_out=None, stream=None):
+    _check(lib.fgd_mix1(h, _dev(theta_prev), _dev(x_out), _dev(momentum), _dev(cd_out), _stream(stream)), "fgd_mix1")
+
+
+def fgd_outer_step_blocking(h, x, theta_prev, theta_local, momentum, cd_out=None, write_local=False, stream=None):
+    _check(lib.fgd_outer_step_blocking(h, _dev(x), _dev(theta_prev), _dev(theta_local), _dev(momentum),
+                                       _dev(cd_out), 1 if write_local else 0, _stream(stream)),
+           "fgd_outer_step_blocking")
+
+
+def fgd_num_cd_rows_split(h):
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib.fgd_num_cd_rows_split(h, ctypes.byref(a), ctypes.byref(b)), "fgd_num_cd_rows_split")
+    return a.value, b.value
+
+
+def fgd_min_bytes_split(h, write_local=False):
+    a, b = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib.fgd_min_bytes_split(h, 1 if write_local else 0, ctypes.byref(a), ctypes.byref(b)),
+           "fgd_min_bytes_split")
+    return a.value, b.value
+
+
 def fgd_consensus_distance(h, x, dtype, out, stream=None):
     _check(lib.fgd_consensus_distance(h, _dev(x), DTYPES.get(dtype, dtype), _dev(out), _stream(stream)),
            "fgd_consensus_distance")
@@ -274,6 +301,29 @@ class Engine:
         self._check_rows(theta_local, "theta_local", self.dtype)
         self._check_rows(momentum, "momentum", "f32")
         fgd_outer_step(self.handle, theta_prev, theta_local, momentum, cd_out, stream)
+
+    def mix1(self, theta_prev, x_out, momentum=None, cd_out=None, stream=None):
+        """Mix1 half of split execution: x_out = Mix1(theta_prev) (and the
+        momentum mixed in place when the engine mixes the state)."""
+        self._check_rows(theta_prev, "theta_prev", self.dtype)
+        self._check_rows(x_out, "x_out", self.dtype)
+        if momentum is not None:
+            self._check_rows(momentum, "momentum", "f32")
+        fgd_mix1(self.handle, theta_prev, x_out, momentum, cd_out, stream)
+
+    def outer_step_blocking(self, x, theta_prev, theta_local, momentum, cd_out=None, write_local=False, stream=None):
+        """Blocking half of split execution, from the stored Mix1 output x."""
+        self._check_rows(x, "x", self.dtype)
+        self._check_rows(theta_prev, "theta_prev", self.dtype)
+        self._check_rows(theta_local, "theta_local", self.dtype)
+        self._check_rows(momentum, "momentum", "f32")
+        fgd_outer_step_blocking(self.handle, x, theta_prev, theta_local, momentum, cd_out, write_local, stream)
+
+    def num_cd_rows_split(self):
+        return fgd_num_cd_rows_split(self.handle)
+
+    def min_bytes_split(self, write_local=False):
+        return fgd_min_bytes_split(self.handle, write_local)
 
     def consensus_distance(self, x, out, stream=None, dtype=None):
         dtype = dtype or self.dtype

@@ -111,6 +111,11 @@ fgd::MixDev mix_dev(const fgd::MixTopology &t, const void *tables) {
     return d;
 }
 
+bool lookup_split(int M, int32_t dtype, int k1, int k2, bool subset, bool mix_state, fgd::SplitSet &ks) {
+    return dtype == FGD_BF16 ? fgd::split_kernels_bf16(M, k1, k2, subset, mix_state, &ks)
+                             : fgd::split_kernels_f32(M, k1, k2, subset, mix_state, &ks);
+}
+
 bool lookup(int M, int32_t dtype, int k1, int k2, bool mix_state, bool subset, fgd::KernelSet &ks) {
     if (mix_state)
         return dtype == FGD_BF16 ? fgd::kernels_bf16_ms(M, k1, k2, subset, &ks)
@@ -221,6 +226,45 @@ void release(fgd_engine *e) {
     for (auto ev : e->ev_stop) (void)hipEventDestroy(ev);
 }
 
+// Step parameters every kernel of a step shares.
+void fill_common(const fgd_engine *e, int ring, int v, fgd::StepParams &p) {
+    const fgd_config &c = e->cfg;
+    p.P = c.num_params;
+    p.ld = c.ld;
+    p.ntiles = tiles_of(c.num_params, v);
+    p.M = c.num_workers;
+    p.lr = c.outer_lr;
+    p.mu = c.momentum;
+    p.nesterov = c.nesterov;
+    const void *t1, *t2;
+    const int64_t *seg;
+    table_ptrs(e, ring, t1, t2, seg);
+    p.mix1 = mix_dev(e->slot[0], t1);
+    p.mix2 = mix_dev(e->slot[1], t2);
+    p.n_seg = static_cast<int32_t>(e->subset.size() / 2);
+    p.seg = seg;
+}
+
+// LDS rows for the table slots a kernel mixes with (use1 / use2: Mix1 / Mix2).
+int32_t lds_rows_for(const fgd_engine *e, bool use1, bool use2) {
+    const bool t1 = use1 && e->slot[0].kind == 2, t2 = use2 && e->slot[1].kind == 2;
+    const bool padded = (t1 && e->slot[0].padded) || (t2 && e->slot[1].padded);
+    return (t1 || t2) ? e->cfg.num_workers + (padded ? 1 : 0) : 0;
+}
+
+// Checks a device [M][ld] array: non-NULL and 16-byte aligned.
+bool bad_rows(const void *p) { return !p || !aligned16(p); }
+
+// True when the [M][ld] spans of a (element size ea) and b (eb) overlap.
+bool rows_overlap(const fgd_engine *e, const void *a, int ea, const void *b, int eb) {
+    const fgd_config &c = e->cfg;
+    if (c.num_params == 0) return false;
+    uintptr_t a0, a1, b0, b1;
+    span(a, c.num_workers, c.ld, c.num_params, ea, a0, a1);
+    span(b, c.num_workers, c.ld, c.num_params, eb, b0, b1);
+    return overlap(a0, a1, b0, b1);
+}
+
 }  // namespace
 
 extern "C" {
@@ -291,7 +335,9 @@ fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
             if (err == hipSuccess) err = hipHostMalloc(&e->h_topo[r], e->topo_capacity, hipHostMallocDefault);
             if (err == hipSuccess) err = hipEventCreateWithFlags(&e->topo_done[r], hipEventDisableTiming);
         }
-        if (err == hipSuccess) err = hipMalloc(&e->d_partials, e->partials_capacity * sizeof(double));
+        // Two regions: the step (fused or blocking half) and the Mix1 half of
+        // split execution, which may be enqueued on another stream.
+        if (err == hipSuccess) err = hipMalloc(&e->d_partials, 2 * e->partials_capacity * sizeof(double));
         if (err != hipSuccess) {
             release(e);
             delete e;
@@ -476,6 +522,131 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
         if (herr != hipSuccess) return hip_fail(herr, "recording a timing event");
         ++e->timed;
     }
+    herr = hipEventRecord(e->topo_done[ring], stream);
+    if (herr != hipSuccess) return hip_fail(herr, "recording the topology event");
+    e->topo_pending[ring] = true;
+    if (cd_out) return launch_finalize(e->d_partials, grid, p.n_cd * c.num_workers, cd_out, stream);
+    return FGD_OK;
+}
+
+fgd_status fgd_num_cd_rows_split(const fgd_engine *e, int32_t *mix1_rows, int32_t *blocking_rows) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (!mix1_rows || !blocking_rows) return fail(FGD_ERR_INVALID_ARG, "NULL output");
+    if (!e->slot_set[0] || !e->slot_set[1]) return fail(FGD_ERR_STATE, "both Mix slots must be set");
+    *mix1_rows = e->slot[0].effective_rounds() + 1;
+    *blocking_rows = e->slot[1].effective_rounds() + 2;
+    return FGD_OK;
+}
+
+fgd_status fgd_min_bytes_split(const fgd_engine *e, int32_t write_local, int64_t *mix1_bytes,
+                               int64_t *blocking_bytes) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (!mix1_bytes || !blocking_bytes) return fail(FGD_ERR_INVALID_ARG, "NULL output");
+    const int64_t n = static_cast<int64_t>(e->cfg.num_workers) * e->cfg.num_params;
+    const int64_t ep = elem_size(e->cfg.param_dtype);
+    *mix1_bytes = n * (2 * ep + (e->cfg.mix1_state ? 8 : 0));
+    *blocking_bytes = n * (4 * ep + 8 + (write_local ? ep : 0));
+    return FGD_OK;
+}
+
+fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *momentum, double *cd_out,
+                    void *stream_handle) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (e->host_only) return fail(FGD_ERR_STATE, "host-only engine cannot run a step");
+    if (!e->slot_set[0] || !e->slot_set[1]) return fail(FGD_ERR_STATE, "both Mix slots must be set before a step");
+    const fgd_config &c = e->cfg;
+    const int es = elem_size(c.param_dtype);
+    if (bad_rows(theta_prev) || bad_rows(x_out))
+        return fail(FGD_ERR_INVALID_ARG, "theta_prev and x_out must be non-NULL and 16-byte aligned");
+    if (c.mix1_state && bad_rows(momentum))
+        return fail(FGD_ERR_INVALID_ARG, "the state is mixed: momentum must be non-NULL and 16-byte aligned");
+    if (cd_out && (reinterpret_cast<uintptr_t>(cd_out) & 7u)) return fail(FGD_ERR_INVALID_ARG, "cd_out must be 8-byte aligned");
+    if (rows_overlap(e, theta_prev, es, x_out, es) ||
+        (c.mix1_state && (rows_overlap(e, momentum, 4, x_out, es) || rows_overlap(e, momentum, 4, theta_prev, es))))
+        return fail(FGD_ERR_INVALID_ARG, "theta_prev, x_out and momentum must not overlap");
+    hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    fgd::SplitSet ks;
+    if (!lookup_split(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, false, c.mix1_state != 0, ks))
+        return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
+    hipError_t herr = hipSetDevice(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    int ring = 0;
+    if (fgd_status st = ensure_topology(e, stream, ring)) return st;
+
+    fgd::StepParams p{};
+    fill_common(e, ring, ks.v, p);
+    p.theta_prev = theta_prev;
+    p.x_out = x_out;
+    p.mom = momentum;
+    p.mom_out = momentum;
+    p.n_cd = e->slot[0].effective_rounds() + 1;
+    p.lds_rows = lds_rows_for(e, true, false);
+    size_t lds = static_cast<size_t>(p.lds_rows) * fgd::kBlock * ks.v * sizeof(float);
+    if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
+    int grid = 0;
+    if (fgd_status st = grid_for(e, ks.mix1, lds, p.ntiles, grid, ks.blocks_per_cu)) return st;
+    double *partials = e->d_partials + e->partials_capacity;
+    if (cd_out) {
+        if (static_cast<size_t>(grid) * p.n_cd * c.num_workers > e->partials_capacity)
+            return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
+        p.cd_partials = partials;
+    }
+    if (fgd_status st = launch(ks.mix1, grid, lds, stream, &p)) return st;
+    herr = hipEventRecord(e->topo_done[ring], stream);
+    if (herr != hipSuccess) return hip_fail(herr, "recording the topology event");
+    e->topo_pending[ring] = true;
+    if (cd_out) return launch_finalize(partials, grid, p.n_cd * c.num_workers, cd_out, stream);
+    return FGD_OK;
+}
+
+fgd_status fgd_outer_step_blocking(fgd_engine *e, const void *x, void *theta_prev, void *theta_local, float *momentum,
+                                   double *cd_out, int32_t write_local, void *stream_handle) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (e->host_only) return fail(FGD_ERR_STATE, "host-only engine cannot run a step");
+    if (!e->slot_set[0] || !e->slot_set[1]) return fail(FGD_ERR_STATE, "both Mix slots must be set before a step");
+    const fgd_config &c = e->cfg;
+    const int es = elem_size(c.param_dtype);
+    if (write_local != 0 && write_local != 1) return fail(FGD_ERR_INVALID_ARG, "write_local must be 0 or 1");
+    if (bad_rows(x) || bad_rows(theta_prev) || bad_rows(theta_local) || bad_rows(momentum))
+        return fail(FGD_ERR_INVALID_ARG, "device arrays must be non-NULL and 16-byte aligned");
+    if (cd_out && (reinterpret_cast<uintptr_t>(cd_out) & 7u)) return fail(FGD_ERR_INVALID_ARG, "cd_out must be 8-byte aligned");
+    if (rows_overlap(e, x, es, theta_prev, es) || rows_overlap(e, x, es, theta_local, es) ||
+        rows_overlap(e, x, es, momentum, 4) || rows_overlap(e, theta_prev, es, theta_local, es) ||
+        rows_overlap(e, theta_prev, es, momentum, 4) || rows_overlap(e, theta_local, es, momentum, 4))
+        return fail(FGD_ERR_INVALID_ARG, "x, theta_prev, theta_local and momentum must not overlap");
+    if (!e->subset.empty() && e->slot[1].kind != 2) return fail(FGD_ERR_UNSUPPORTED, "a Mix2 subset needs a CSR Mix2");
+    hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    fgd::SplitSet ks;
+    if (!lookup_split(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, !e->subset.empty(), false, ks))
+        return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
+    hipError_t herr = hipSetDevice(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    int ring = 0;
+    if (fgd_status st = ensure_topology(e, stream, ring)) return st;
+
+    fgd::StepParams p{};
+    fill_common(e, ring, ks.v, p);
+    p.theta_prev = theta_prev;
+    p.theta_out = theta_prev;
+    p.theta_local = theta_local;
+    p.mom = momentum;
+    p.mom_out = momentum;
+    p.x = x;
+    p.local_out = write_local ? theta_local : nullptr;
+    p.n_cd = e->slot[1].effective_rounds() + 2;
+    p.lds_rows = lds_rows_for(e, false, true);
+    size_t lds = static_cast<size_t>(p.lds_rows) * fgd::kBlock * ks.v * sizeof(float);
+    if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
+    int grid = 0;
+    if (fgd_status st = grid_for(e, ks.blocking, lds, p.ntiles, grid, ks.blocks_per_cu)) return st;
+    if (cd_out) {
+        if (static_cast<size_t>(grid) * p.n_cd * c.num_workers > e->partials_capacity)
+            return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
+        p.cd_partials = e->d_partials;
+    }
+    if (fgd_status st = launch(ks.blocking, grid, lds, stream, &p)) return st;
     herr = hipEventRecord(e->topo_done[ring], stream);
     if (herr != hipSuccess) return hip_fail(herr, "recording the topology event");
     e->topo_pending[ring] = true;

@@ -81,6 +81,10 @@ struct StepParams {
     int32_t n_seg, pad_;      // Mix2 subset: number of segments (0: Mix2 everywhere)
     const int64_t *seg;       // [n_seg][2] ascending half-open [begin, end) parameter ranges
     MixDev mix1, mix2;
+    // Split execution (the Mix1 half and the blocking half of a round):
+    const void *x;            // blocking half: the stored Mix1 output, [M][ld] storage type
+    void *x_out;              // Mix1 half: where it stores x
+    void *local_out;          // blocking half: theta_local, receives theta' (nullptr: no write-back)
 };
 
 struct ConsensusParams {
@@ -381,7 +385,10 @@ __device__ inline void cd_accumulate(const float (&u)[MMAX][V], int M, double *a
 // ------------------------------------------------------------------ mixing
 
 // Mix kinds as template arguments; kAny reads the kind at run time.
+// kStored (Mix1 only): x is read from the array a Mix1 launch stored (the
+// blocking half of split execution).
 constexpr int kAny = 3;
+constexpr int kStored = 4;
 
 // The tables are read through the constant address space: they are never
 // written by the kernel, and this lets every (column, weight) pair arrive in
@@ -554,13 +561,13 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
     // the centres of every consensus row of the slot.
     float xbar[V], gbar[V];
     row_mean<MMAX, EXACT, V>(u2, M, gbar);
-    row_mean<MMAX, EXACT, V>(u1, M, xbar);
-    if (c.cd_acc) {
-        cd_accumulate_about<MMAX, EXACT, V>(u2, gbar, M, c.cd_acc, c.lane);
-        cd_accumulate_about<MMAX, EXACT, V>(u1, xbar, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
+    if (c.cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u2, gbar, M, c.cd_acc, c.lane);
+    if constexpr (K1 != kStored) {
+        row_mean<MMAX, EXACT, V>(u1, M, xbar);
+        if (c.cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u1, xbar, M, c.cd_acc + (c.n2 + 1) * kCdStride, c.lane);
+        mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, c.rows, c.tid,
+                                      c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane, 0u);
     }
-    mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u1, xbar, c.rows, c.tid,
-                                  c.cd_acc ? c.cd_acc + (c.n2 + 2) * kCdStride : nullptr, kCdStride, c.lane, 0u);
     // A tile wholly outside a Mix2 subset runs the rounds too, with every
     // element kept: one code path keeps the register budget of the kernel.
     mix_apply<MMAX, EXACT, V, K2>(a.mix2, M, u2, gbar, c.rows, c.tid, c.cd_acc ? c.cd_acc + 1 * kCdStride : nullptr,
@@ -576,14 +583,15 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
     const bool nesterov = a.nesterov != 0;
 
     // v' = mu v + g ; theta' = x - lr (g + mu v') or x - lr v'; stores row m.
-    auto finish_row = [&](int m, float (&vr)[V]) {
+    // xs: the row's stored x (kStored only).
+    auto finish_row = [&](int m, float (&vr)[V], const float (&xs)[V]) {
         float stored[V];
         if ((EXACT || m < M) && (FULL || nv > 0)) {
             float t[V];
 #pragma unroll
             for (int e = 0; e < V; ++e) {
                 const float g = K2 == kGlobal ? gbar[e] : u2[m][e];
-                const float x = K1 == kGlobal ? xbar[e] : u1[m][e];
+                const float x = K1 == kStored ? xs[e] : (K1 == kGlobal ? xbar[e] : u1[m][e]);
                 vr[e] = fmaf(mu, vr[e], g);
                 const float step = nesterov ? fmaf(mu, vr[e], g) : vr[e];
                 t[e] = fmaf(-lr, step, x);
@@ -596,6 +604,14 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
             } else {
                 F32Io<V>::store_part(rv, off_v, nv, vr);
                 PIO::store_part(rp, off_p, nv, t, stored);
+            }
+            if constexpr (K1 == kStored) {
+                if (a.local_out) {  // theta' (already in storage precision) as the next inner start
+                    float again[V];
+                    const rsrc_t rl = row_rsrc(a.local_out, m * a.ld + tb, kE);
+                    if (FULL || nv == V) PIO::store(rl, off_p, stored, again);
+                    else PIO::store_part(rl, off_p, nv, stored, again);
+                }
             }
         } else {
 #pragma unroll
@@ -631,27 +647,33 @@ __device__ __forceinline__ void step_tile(const StepParams &a, const TileCtx &c,
             mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, vm, vbar, c.rows, c.tid, nullptr, 0, c.lane, 0u);
         }
 #pragma unroll
-        for (int m = 0; m < MMAX; ++m) finish_row(m, vm[m]);
+        for (int m = 0; m < MMAX; ++m) finish_row(m, vm[m], vm[m]);
     } else {
-        // A group of rows at a time bounds the momentum registers.
+        // A group of rows at a time bounds the momentum (and stored x) registers.
         constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
+        constexpr int GX = K1 == kStored ? G : 1;
 #pragma unroll
         for (int m0 = 0; m0 < MMAX; m0 += G) {
             float vm[G][V];
+            float xm[GX][V];
             if (FULL || nv > 0) {
 #pragma unroll
                 for (int j = 0; j < G; ++j) {
                     const int m = m0 + j;
-                    if (m < MMAX && (EXACT || m < M)) F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[j]);
+                    if (m < MMAX && (EXACT || m < M)) {
+                        F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[j]);
+                        if constexpr (K1 == kStored) PIO::load(row_rsrc(a.x, m * a.ld + tb, kE), off_p, xm[j]);
+                    }
                 }
             }
 #pragma unroll
             for (int j = 0; j < G; ++j)
-                if (m0 + j < MMAX) finish_row(m0 + j, vm[j]);
+                if (m0 + j < MMAX) finish_row(m0 + j, vm[j], xm[GX == 1 ? 0 : j]);
         }
     }
     if (c.cd_acc) {
-        double *acc = c.cd_acc + (c.n2 + c.n1 + 2) * kCdStride;
+        // The stored theta' row follows the Mix2 rows, then (fused step) the Mix1 rows.
+        double *acc = c.cd_acc + (K1 == kStored ? c.n2 + 1 : c.n2 + c.n1 + 2) * kCdStride;
         if constexpr (kStoreInU2) cd_accumulate<MMAX, EXACT, V>(u2, M, acc, c.lane);
         else if constexpr (kStoreInU1) cd_accumulate<MMAX, EXACT, V>(u1, M, acc, c.lane);
         else cd_accumulate<MMAX, EXACT, V>(sep, M, acc, c.lane);
@@ -727,6 +749,119 @@ void outer_step_kernel(StepParams a) {
         else step_tile<MMAX, EXACT, V, PIO, K1, K2, MS, false>(a, c, tb, lo, keep);
     }
 
+    if (c.cd_acc) {
+        __syncthreads();
+        const double *base = reinterpret_cast<const double *>(smem + rows_bytes);
+        for (int i = c.tid; i < a.n_cd * c.M; i += kBlock) {
+            const int r = i / c.M, m = i % c.M;
+            double s = 0.0;
+#pragma unroll
+            for (int w = 0; w < kWavesPerBlock; ++w) s += base[r * kCdStride + w * MP + m];
+            a.cd_partials[(static_cast<int64_t>(blockIdx.x) * a.n_cd + r) * c.M + m] = s;
+        }
+    }
+}
+
+// ------------------------------------------------ split execution: Mix1 half
+
+// x = Mix1(theta_prev) stored in the parameter type (Appendix A, Algorithm
+// 1: the non-blocking mix launched at the start of a round), with consensus
+// rows x^0..x^K1; MS: the momentum is replaced by Mix1 of itself.
+template <int MMAX, bool EXACT, int V, class PIO, int K1, bool MS, bool FULL>
+__device__ __forceinline__ void mix1_tile(const StepParams &a, const TileCtx &c, int64_t tb, uint32_t lo) {
+    constexpr int MP = pow2_at_least(MMAX);
+    constexpr int kCdStride = kWavesPerBlock * MP;
+    constexpr int kE = PIO::kElem;
+    const int M = c.M;
+    int nv = V;
+    if constexpr (!FULL) {
+        const int64_t rem = a.P - tb - lo;
+        nv = rem >= V ? V : (rem > 0 ? static_cast<int>(rem) : 0);
+    }
+    const uint32_t off_p = lo * kE, off_v = lo * 4;
+    float u[MMAX][V];
+    if (FULL || nv > 0) {
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m)
+            if (EXACT || m < M) PIO::load(row_rsrc(a.theta_prev, m * a.ld + tb, kE), off_p, u[m]);
+    }
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m)
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            if (!((EXACT || m < M) && (FULL || v < nv))) u[m][v] = 0.0f;
+    float xbar[V];
+    row_mean<MMAX, EXACT, V>(u, M, xbar);
+    if (c.cd_acc) cd_accumulate_about<MMAX, EXACT, V>(u, xbar, M, c.cd_acc, c.lane);
+    mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, u, xbar, c.rows, c.tid, c.cd_acc ? c.cd_acc + kCdStride : nullptr,
+                                  kCdStride, c.lane, 0u);
+    if (FULL || nv > 0) {
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+            if (EXACT || m < M) {
+                float stored[V];
+                const rsrc_t rx = row_rsrc(a.x_out, m * a.ld + tb, kE);
+                if (FULL || nv == V) PIO::store(rx, off_p, K1 == kGlobal ? xbar : u[m], stored);
+                else PIO::store_part(rx, off_p, nv, K1 == kGlobal ? xbar : u[m], stored);
+            }
+        }
+    }
+    if constexpr (MS) {
+        float vm[MMAX][V];
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+            if ((EXACT || m < M) && (FULL || nv > 0)) F32Io<V>::load(row_rsrc(a.mom, m * a.ld + tb, 4), off_v, vm[m]);
+            else {
+#pragma unroll
+                for (int e = 0; e < V; ++e) vm[m][e] = 0.0f;
+            }
+        }
+        float vbar[V];
+        row_mean<MMAX, EXACT, V>(vm, M, vbar);
+        mix_apply<MMAX, EXACT, V, K1>(a.mix1, M, vm, vbar, c.rows, c.tid, nullptr, 0, c.lane, 0u);
+        if (FULL || nv > 0) {
+#pragma unroll
+            for (int m = 0; m < MMAX; ++m) {
+                if (EXACT || m < M) {
+                    const rsrc_t rv = row_rsrc(a.mom_out, m * a.ld + tb, 4);
+                    if (FULL || nv == V) F32Io<V>::store(rv, off_v, K1 == kGlobal ? vbar : vm[m]);
+                    else F32Io<V>::store_part(rv, off_v, nv, K1 == kGlobal ? vbar : vm[m]);
+                }
+            }
+        }
+    }
+}
+
+template <int MMAX, bool EXACT, int V, class PIO, int K1, bool MS>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(waves_per_simd_target(MMAX))))
+void mix1_kernel(StepParams a) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    constexpr int MP = pow2_at_least(MMAX);
+    constexpr int kCdStride = kWavesPerBlock * MP;
+    constexpr int64_t kTile = static_cast<int64_t>(kBlock) * V;
+    TileCtx c;
+    c.M = EXACT ? MMAX : a.M;
+    c.tid = threadIdx.x;
+    c.lane = c.tid & (kWave - 1);
+    const int wave = c.tid / kWave;
+    c.rows = reinterpret_cast<float *>(smem);
+    const int64_t rows_bytes = static_cast<int64_t>(a.lds_rows) * kBlock * V * 4;
+    c.cd_acc = a.cd_partials ? reinterpret_cast<double *>(smem + rows_bytes) + wave * MP : nullptr;
+    c.n1 = c.n2 = 0;
+    if (a.lds_rows > c.M) {
+        float *z = c.rows + (static_cast<int64_t>(c.M) * kBlock + c.tid) * V;
+#pragma unroll
+        for (int v = 0; v < V; ++v) z[v] = 0.0f;
+    }
+    if (c.cd_acc) {
+        for (int i = c.lane; i < a.n_cd * MP; i += kWave) c.cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
+    }
+    const uint32_t lo = static_cast<uint32_t>(c.tid) * V;
+    for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+        const int64_t tb = tile * kTile;
+        if (tb + kTile <= a.P) mix1_tile<MMAX, EXACT, V, PIO, K1, MS, true>(a, c, tb, lo);
+        else mix1_tile<MMAX, EXACT, V, PIO, K1, MS, false>(a, c, tb, lo);
+    }
     if (c.cd_acc) {
         __syncthreads();
         const double *base = reinterpret_cast<const double *>(smem + rows_bytes);
@@ -863,6 +998,39 @@ KernelSet make_kernel_set_ms(int k1, int k2, bool subset) {
     return ks;
 }
 
+// Split-execution kernels of one instantiation: the Mix1 half (global mean
+// specialised when M is exact, run-time kinds otherwise) and the blocking
+// half (CSR Mix2 specialised when M is exact, with and without a subset).
+struct SplitSet {
+    const void *mix1;
+    const void *blocking;
+    int v;
+    int mmax;
+    int blocks_per_cu;
+};
+
+template <template <int> class PIOT, int MMAX, bool EXACT, int V>
+SplitSet make_split_set(int k1, int k2, bool subset, bool mix_state) {
+    using P = PIOT<V>;
+    SplitSet ks;
+    ks.mix1 = mix_state ? reinterpret_cast<const void *>(&mix1_kernel<MMAX, EXACT, V, P, kAny, true>)
+                        : reinterpret_cast<const void *>(&mix1_kernel<MMAX, EXACT, V, P, kAny, false>);
+    ks.blocking = reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kStored, kAny, kSubset>);
+    if constexpr (EXACT) {
+        if (k1 == kGlobal)
+            ks.mix1 = mix_state ? reinterpret_cast<const void *>(&mix1_kernel<MMAX, EXACT, V, P, kGlobal, true>)
+                                : reinterpret_cast<const void *>(&mix1_kernel<MMAX, EXACT, V, P, kGlobal, false>);
+        if (k2 == kTable)
+            ks.blocking = subset ? reinterpret_cast<const void *>(
+                                       &outer_step_kernel<MMAX, EXACT, V, P, kStored, kTable, kSubset>)
+                                 : reinterpret_cast<const void *>(&outer_step_kernel<MMAX, EXACT, V, P, kStored, kTable, 0>);
+    }
+    ks.v = V;
+    ks.mmax = MMAX;
+    ks.blocks_per_cu = step_blocks_per_cu(MMAX);
+    return ks;
+}
+
 // Elements per lane per row: 16-byte float32 accesses up to 8 workers; bf16
 // parameters use 8-byte accesses (4 elements) so that momentum still moves in
 // 16-byte accesses and the register and LDS footprint per lane stays small.
@@ -871,24 +1039,24 @@ constexpr int lanes_v_bf16(int mmax) {
     return mmax <= 8 ? FGD_V_BF16_M8 : (mmax == 16 ? 4 : (mmax == 32 ? 2 : 1));
 }
 
-// Calls F::get<MMAX, EXACT>(k1, k2) for the instantiation that serves M
+// Calls F::get<MMAX, EXACT>(args...) for the instantiation that serves M
 // workers: exact for M in {1, 2, 4, 8, 16, 32, 64}, else the next power of
 // two with M read at run time.
-template <class F>
-bool select_workers(int M, int k1, int k2, bool subset, KernelSet *out) {
+template <class F, class Out, class... A>
+bool select_workers(int M, Out *out, A... args) {
     if (M < 1 || M > 64) return false;
-    if (M == 1) *out = F::template get<1, true>(k1, k2, subset);
-    else if (M == 2) *out = F::template get<2, true>(k1, k2, subset);
-    else if (M == 3) *out = F::template get<4, false>(k1, k2, subset);
-    else if (M == 4) *out = F::template get<4, true>(k1, k2, subset);
-    else if (M < 8) *out = F::template get<8, false>(k1, k2, subset);
-    else if (M == 8) *out = F::template get<8, true>(k1, k2, subset);
-    else if (M < 16) *out = F::template get<16, false>(k1, k2, subset);
-    else if (M == 16) *out = F::template get<16, true>(k1, k2, subset);
-    else if (M < 32) *out = F::template get<32, false>(k1, k2, subset);
-    else if (M == 32) *out = F::template get<32, true>(k1, k2, subset);
-    else if (M < 64) *out = F::template get<64, false>(k1, k2, subset);
-    else *out = F::template get<64, true>(k1, k2, subset);
+    if (M == 1) *out = F::template get<1, true>(args...);
+    else if (M == 2) *out = F::template get<2, true>(args...);
+    else if (M == 3) *out = F::template get<4, false>(args...);
+    else if (M == 4) *out = F::template get<4, true>(args...);
+    else if (M < 8) *out = F::template get<8, false>(args...);
+    else if (M == 8) *out = F::template get<8, true>(args...);
+    else if (M < 16) *out = F::template get<16, false>(args...);
+    else if (M == 16) *out = F::template get<16, true>(args...);
+    else if (M < 32) *out = F::template get<32, false>(args...);
+    else if (M == 32) *out = F::template get<32, true>(args...);
+    else if (M < 64) *out = F::template get<64, false>(args...);
+    else *out = F::template get<64, true>(args...);
     return true;
 }
 
@@ -901,5 +1069,8 @@ bool kernels_bf16(int M, int k1, int k2, bool subset, KernelSet *out);
 // Step kernels that also mix the optimizer state with Mix1.
 bool kernels_f32_ms(int M, int k1, int k2, bool subset, KernelSet *out);
 bool kernels_bf16_ms(int M, int k1, int k2, bool subset, KernelSet *out);
+// Split-execution kernels.
+bool split_kernels_f32(int M, int k1, int k2, bool subset, bool mix_state, SplitSet *out);
+bool split_kernels_bf16(int M, int k1, int k2, bool subset, bool mix_state, SplitSet *out);
 
 }  // namespace fgd

@@ -14,7 +14,7 @@ struct Sets {
 }  // namespace
 
 bool kernels_bf16_ms(int M, int k1, int k2, bool subset, KernelSet *out) {
-    return select_workers<Sets>(M, k1, k2, subset, out);
+    return select_workers<Sets>(M, out, k1, k2, subset);
 }
 
 }  // namespace fgd

@@ -13,7 +13,7 @@ struct Sets {
 }  // namespace
 
 bool kernels_f32(int M, int k1, int k2, bool subset, KernelSet *out) {
-    return select_workers<Sets>(M, k1, k2, subset, out);
+    return select_workers<Sets>(M, out, k1, k2, subset);
 }
 
 }  // namespace fgd
