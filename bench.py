@@ -112,6 +112,94 @@ def cpu_baseline(sl, w, topo1, topo2):
             "params_workers_per_s": round(M * p_slice / dt, 1), "host_cpu": model, "host_nproc": ncpu}
 
 
+def split_round_bench(args, eng, torch, tp, tl, v, w, step_topos):
+    """Split execution of a round (Appendix A, Algorithm 1): the Mix1 half is
+    launched on a side stream at the start of the round and overlaps a
+    stand-in inner loop (bf16 matrix products on the main stream); the
+    blocking half follows once both are done.  Reports each half alone, the
+    inner loop alone and the overlapped round, and how much of the Mix1 half
+    the inner loop hides.  One JSON line on stdout."""
+    M, P = w["M"], w["P"]
+    main_s = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    x = torch.empty_like(tp)
+    n1, n2 = eng.num_cd_rows_split()
+    cd1 = torch.zeros((n1, M), dtype=torch.float64, device=tp.device)
+    cd2 = torch.zeros((n2, M), dtype=torch.float64, device=tp.device)
+    b1, b2 = eng.min_bytes_split(write_local=True)
+    vmix = v if w.get("mix1_state") else None
+    A = torch.randn(8192, 8192, device=tp.device, dtype=torch.bfloat16)
+    B = torch.randn(8192, 8192, device=tp.device, dtype=torch.bfloat16)
+    C = torch.empty_like(A)
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    def set_masks(i):
+        if step_topos is not None:
+            eng.set_topology_dict("mix2", step_topos[i % len(step_topos)])
+
+    def timed(fn, stream, reps):
+        e0, e1 = ev(), ev()
+        e0.record(stream)
+        for i in range(reps):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    print("[bench] split: halves alone", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        eng.mix1(tp, x, vmix, cd1, main_s, num_blocks=args.mix1_blocks)
+        set_masks(i)
+        eng.outer_step_blocking(x, tp, tl, v, cd2, write_local=True, stream=main_s)
+    torch.cuda.synchronize()
+    nb = args.mix1_blocks
+    t_mix1 = timed(lambda i: eng.mix1(tp, x, vmix, cd1, main_s, num_blocks=nb), main_s, args.steps)
+    t_block = timed(lambda i: (set_masks(i), eng.outer_step_blocking(x, tp, tl, v, cd2, write_local=True,
+                                                                     stream=main_s)), main_s, args.steps)
+    timed(lambda i: torch.matmul(A, B, out=C), main_s, 3)  # library set-up outside the timing
+    t_gemm = timed(lambda i: torch.matmul(A, B, out=C), main_s, 10)
+    n_gemm = max(1, int(2.0 * t_mix1 / t_gemm + 0.999))
+    t_inner = timed(lambda i: [torch.matmul(A, B, out=C) for _ in range(n_gemm)], main_s, 5)
+
+    print("[bench] split: overlapped rounds", file=sys.stderr, flush=True)
+    rounds = []
+    for r in range(args.steps):
+        e0, e1 = ev(), ev()
+        e0.record(main_s)
+        side.wait_stream(main_s)
+        with torch.cuda.stream(side):
+            eng.mix1(tp, x, vmix, cd1, side, num_blocks=nb)
+            done = torch.cuda.Event()
+            done.record(side)
+        for _ in range(n_gemm):
+            torch.matmul(A, B, out=C)
+        main_s.wait_event(done)
+        set_masks(r)
+        eng.outer_step_blocking(x, tp, tl, v, cd2, write_local=True, stream=main_s)
+        e1.record(main_s)
+        rounds.append((e0, e1))
+    torch.cuda.synchronize()
+    t_round = sorted(a.elapsed_time(b) for a, b in rounds)[len(rounds) // 2]
+    exposed = max(0.0, t_round - t_inner - t_block)
+    out = {
+        "metric": "split outer step: Mix1 half hidden under the inner loop; blocking-half HBM GB/s",
+        "mode": "split", "workload": args.workload, "steps": args.steps, "warmup": args.warmup,
+        "mix1_ms": round(t_mix1, 4), "mix1_gbs": round(b1 / (t_mix1 * 1e-3) / 1e9, 1),
+        "blocking_ms": round(t_block, 4), "blocking_gbs": round(b2 / (t_block * 1e-3) / 1e9, 1),
+        "blocking_frac_of_peak": round(b2 / (t_block * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "bytes": {"mix1": b1, "blocking": b2}, "inner_standin": f"{n_gemm} bf16 GEMMs 8192^3 per round",
+        "mix1_blocks": nb or "one per CU",
+        "inner_ms": round(t_inner, 4), "round_ms_median": round(t_round, 4), "exposed_mix1_ms": round(exposed, 4),
+        "mix1_hidden_fraction": round(1.0 - min(exposed, t_mix1) / t_mix1, 4),
+        "config": {"workers": M, "params_per_worker": P, "dtype": w["dtype"], "write_back_theta_local": True,
+                   "mix1_also_on_momentum": bool(w.get("mix1_state"))},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -121,6 +209,11 @@ def main():
     ap.add_argument("--cpu-slice", type=int, default=1 << 25, help="parameters per worker in the CPU sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
+    ap.add_argument("--mode", choices=["fused", "split"], default="fused",
+                    help="fused: one-pass outer step (the benchmark); split: Mix1 half on a side stream "
+                         "overlapping a stand-in inner loop, then the blocking half")
+    ap.add_argument("--mix1-blocks", type=int, default=0,
+                    help="split mode: blocks of the Mix1 half (0: one per CU)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -169,6 +262,11 @@ def main():
         if step_topos is not None:
             eng.set_topology_dict("mix2", step_topos[i])
         eng.outer_step(tp, tl, v, cd, stream)
+
+    if args.mode == "split":
+        split_round_bench(args, eng, torch, tp, tl, v, w, step_topos)
+        eng.close()
+        return
 
     print("[bench] warmup", file=sys.stderr, flush=True)
     for i in range(args.warmup):

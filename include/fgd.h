@@ -199,9 +199,15 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
  *               half); otherwise ignored and may be NULL
  *   cd_out      device double[K1 + 1][M] or NULL: rows x^0..x^K1 (consensus
  *               of the unrounded Mix1 intermediates)
- * Enqueued on `stream`. */
+ *   num_blocks  0: one block per compute unit; n > 0: at most n blocks, so
+ *               that a Mix1 overlapping other kernels occupies fewer CUs.
+ *               Blocks take chunks of the parameter range from a counter, so
+ *               an uneven placement next to other kernels balances itself;
+ *               the result does not depend on num_blocks.
+ * Enqueued on `stream`.  Two Mix1 launches of one engine must not overlap
+ * (they share the engine's counter and consensus scratch). */
 fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *momentum, double *cd_out,
-                    void *stream);
+                    int32_t num_blocks, void *stream);
 
 /* Blocking half: g0 = theta_prev - theta_local, ghat = Mix2(g0) (on the
  * subset if one is set), v' = mu v + ghat, theta' = x - lr (ghat + mu v')

@@ -64,7 +64,7 @@ def _load():
         "fgd_set_mix2_subset": (I32, [P, P, I32]),
         "fgd_num_cd_rows": (I32, [P, ctypes.POINTER(I32)]),
         "fgd_outer_step": (I32, [P, P, P, P, P, P]),
-        "fgd_mix1": (I32, [P, P, P, P, P, P]),
+        "fgd_mix1": (I32, [P, P, P, P, P, I32, P]),
         "fgd_outer_step_blocking": (I32, [P, P, P, P, P, P, I32, P]),
         "fgd_num_cd_rows_split": (I32, [P, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
         "fgd_min_bytes_split": (I32, [P, I32, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
@@ -174,8 +174,9 @@ def fgd_outer_step(h, theta_prev, theta_local, momentum, cd_out=None, stream=Non
                               _stream(stream)), "fgd_outer_step")
 
 
-def fgd_mix1(h, theta_prev, x_out, momentum=None, cd_out=None, stream=None):
-    _check(lib.fgd_mix1(h, _dev(theta_prev), _dev(x_out), _dev(momentum), _dev(cd_out), _stream(stream)), "fgd_mix1")
+def fgd_mix1(h, theta_prev, x_out, momentum=None, cd_out=None, num_blocks=0, stream=None):
+    _check(lib.fgd_mix1(h, _dev(theta_prev), _dev(x_out), _dev(momentum), _dev(cd_out), int(num_blocks),
+                        _stream(stream)), "fgd_mix1")
 
 
 def fgd_outer_step_blocking(h, x, theta_prev, theta_local, momentum, cd_out=None, write_local=False, stream=None):
@@ -302,14 +303,14 @@ class Engine:
         self._check_rows(momentum, "momentum", "f32")
         fgd_outer_step(self.handle, theta_prev, theta_local, momentum, cd_out, stream)
 
-    def mix1(self, theta_prev, x_out, momentum=None, cd_out=None, stream=None):
+    def mix1(self, theta_prev, x_out, momentum=None, cd_out=None, stream=None, num_blocks=0):
         """Mix1 half of split execution: x_out = Mix1(theta_prev) (and the
         momentum mixed in place when the engine mixes the state)."""
         self._check_rows(theta_prev, "theta_prev", self.dtype)
         self._check_rows(x_out, "x_out", self.dtype)
         if momentum is not None:
             self._check_rows(momentum, "momentum", "f32")
-        fgd_mix1(self.handle, theta_prev, x_out, momentum, cd_out, stream)
+        fgd_mix1(self.handle, theta_prev, x_out, momentum, cd_out, num_blocks, stream)
 
     def outer_step_blocking(self, x, theta_prev, theta_local, momentum, cd_out=None, write_local=False, stream=None):
         """Blocking half of split execution, from the stored Mix1 output x."""

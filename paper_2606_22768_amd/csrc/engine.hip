@@ -50,6 +50,7 @@ constexpr int kTopoRing = 8;
 #endif
 constexpr int kMaxBlocksPerCu = FGD_MAX_BLOCKS_PER_CU;
 constexpr int kTimingPool = 4096;
+constexpr int64_t kMix1Chunks = 4096;  // chunks the Mix1 half's tiles are cut into (at most)
 
 }  // namespace
 
@@ -73,7 +74,9 @@ struct fgd_engine {
     uint64_t topo_current_version = ~0ull;
     hipStream_t topo_stream = nullptr;
     double *d_partials = nullptr;
-    size_t partials_capacity = 0;  // doubles
+    size_t partials_capacity = 0;  // doubles, per step kernel
+    double *d_chunk_partials = nullptr;  // Mix1 half: [kMix1Chunks][n_cd][M]
+    int *d_counter = nullptr;            // Mix1 half: chunk counter
 
     // Kernel timing.
     bool timing = false;
@@ -222,6 +225,8 @@ void release(fgd_engine *e) {
         if (e->topo_done[r]) (void)hipEventDestroy(e->topo_done[r]);
     }
     if (e->d_partials) (void)hipFree(e->d_partials);
+    if (e->d_chunk_partials) (void)hipFree(e->d_chunk_partials);
+    if (e->d_counter) (void)hipFree(e->d_counter);
     for (auto ev : e->ev_start) (void)hipEventDestroy(ev);
     for (auto ev : e->ev_stop) (void)hipEventDestroy(ev);
 }
@@ -335,9 +340,13 @@ fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
             if (err == hipSuccess) err = hipHostMalloc(&e->h_topo[r], e->topo_capacity, hipHostMallocDefault);
             if (err == hipSuccess) err = hipEventCreateWithFlags(&e->topo_done[r], hipEventDisableTiming);
         }
-        // Two regions: the step (fused or blocking half) and the Mix1 half of
-        // split execution, which may be enqueued on another stream.
-        if (err == hipSuccess) err = hipMalloc(&e->d_partials, 2 * e->partials_capacity * sizeof(double));
+        if (err == hipSuccess) err = hipMalloc(&e->d_partials, e->partials_capacity * sizeof(double));
+        // The Mix1 half of split execution has its own consensus scratch and
+        // counter: it may be enqueued on another stream.
+        if (err == hipSuccess)
+            err = hipMalloc(&e->d_chunk_partials,
+                            static_cast<size_t>(kMix1Chunks) * (FGD_MAX_ROUNDS + 1) * M * sizeof(double));
+        if (err == hipSuccess) err = hipMalloc(&e->d_counter, 64);
         if (err != hipSuccess) {
             release(e);
             delete e;
@@ -550,7 +559,7 @@ fgd_status fgd_min_bytes_split(const fgd_engine *e, int32_t write_local, int64_t
 }
 
 fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *momentum, double *cd_out,
-                    void *stream_handle) {
+                    int32_t num_blocks, void *stream_handle) {
     g_last_error.clear();
     if (fgd_status st = check_engine(e)) return st;
     if (e->host_only) return fail(FGD_ERR_STATE, "host-only engine cannot run a step");
@@ -562,6 +571,7 @@ fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *m
     if (c.mix1_state && bad_rows(momentum))
         return fail(FGD_ERR_INVALID_ARG, "the state is mixed: momentum must be non-NULL and 16-byte aligned");
     if (cd_out && (reinterpret_cast<uintptr_t>(cd_out) & 7u)) return fail(FGD_ERR_INVALID_ARG, "cd_out must be 8-byte aligned");
+    if (num_blocks < 0) return fail(FGD_ERR_INVALID_ARG, "num_blocks must be >= 0");
     if (rows_overlap(e, theta_prev, es, x_out, es) ||
         (c.mix1_state && (rows_overlap(e, momentum, 4, x_out, es) || rows_overlap(e, momentum, 4, theta_prev, es))))
         return fail(FGD_ERR_INVALID_ARG, "theta_prev, x_out and momentum must not overlap");
@@ -586,17 +596,20 @@ fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *m
     if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
     int grid = 0;
     if (fgd_status st = grid_for(e, ks.mix1, lds, p.ntiles, grid, ks.blocks_per_cu)) return st;
-    double *partials = e->d_partials + e->partials_capacity;
-    if (cd_out) {
-        if (static_cast<size_t>(grid) * p.n_cd * c.num_workers > e->partials_capacity)
-            return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
-        p.cd_partials = partials;
-    }
+    if (num_blocks > 0) grid = std::min(grid, num_blocks);
+    p.chunk_tiles = std::max<int64_t>(1, (p.ntiles + kMix1Chunks - 1) / kMix1Chunks);
+    p.nchunks = (p.ntiles + p.chunk_tiles - 1) / p.chunk_tiles;
+    p.chunk_counter = e->d_counter;
+    if (cd_out) p.cd_partials = e->d_chunk_partials;
+    hipLaunchKernelGGL(fgd::counter_reset_kernel, dim3(1), dim3(64), 0, stream, e->d_counter);
+    herr = hipGetLastError();
+    if (herr != hipSuccess) return hip_fail(herr, "counter reset launch");
     if (fgd_status st = launch(ks.mix1, grid, lds, stream, &p)) return st;
     herr = hipEventRecord(e->topo_done[ring], stream);
     if (herr != hipSuccess) return hip_fail(herr, "recording the topology event");
     e->topo_pending[ring] = true;
-    if (cd_out) return launch_finalize(partials, grid, p.n_cd * c.num_workers, cd_out, stream);
+    if (cd_out) return launch_finalize(e->d_chunk_partials, static_cast<int>(p.nchunks), p.n_cd * c.num_workers,
+                                       cd_out, stream);
     return FGD_OK;
 }
 

@@ -85,6 +85,9 @@ struct StepParams {
     const void *x;            // blocking half: the stored Mix1 output, [M][ld] storage type
     void *x_out;              // Mix1 half: where it stores x
     void *local_out;          // blocking half: theta_local, receives theta' (nullptr: no write-back)
+    int *chunk_counter;       // Mix1 half: next chunk to take (0 at launch)
+    int64_t nchunks;          // Mix1 half: chunks of chunk_tiles tiles; cd_partials is [nchunks][n_cd][M]
+    int64_t chunk_tiles;
 };
 
 struct ConsensusParams {
@@ -832,10 +835,18 @@ __device__ __forceinline__ void mix1_tile(const StepParams &a, const TileCtx &c,
     }
 }
 
+// The Mix1 half is meant to run beside other kernels (the inner loop), where
+// a grid of resident blocks can be placed unevenly: blocks dispatched while
+// another kernel holds most CUs pile up on the few that are free.  So blocks
+// take fixed chunks of tiles from a counter instead of a fixed stride, and
+// each chunk leaves its own consensus partials, summed in chunk order: the
+// work balances itself and the result does not depend on which block took
+// which chunk.
 template <int MMAX, bool EXACT, int V, class PIO, int K1, bool MS>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(waves_per_simd_target(MMAX))))
 void mix1_kernel(StepParams a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    __shared__ int64_t s_chunk;
     constexpr int MP = pow2_at_least(MMAX);
     constexpr int kCdStride = kWavesPerBlock * MP;
     constexpr int64_t kTile = static_cast<int64_t>(kBlock) * V;
@@ -853,27 +864,41 @@ void mix1_kernel(StepParams a) {
 #pragma unroll
         for (int v = 0; v < V; ++v) z[v] = 0.0f;
     }
-    if (c.cd_acc) {
-        for (int i = c.lane; i < a.n_cd * MP; i += kWave) c.cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
-    }
     const uint32_t lo = static_cast<uint32_t>(c.tid) * V;
-    for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
-        const int64_t tb = tile * kTile;
-        if (tb + kTile <= a.P) mix1_tile<MMAX, EXACT, V, PIO, K1, MS, true>(a, c, tb, lo);
-        else mix1_tile<MMAX, EXACT, V, PIO, K1, MS, false>(a, c, tb, lo);
-    }
-    if (c.cd_acc) {
+    for (;;) {
+        if (c.tid == 0) s_chunk = atomicAdd(a.chunk_counter, 1);
         __syncthreads();
-        const double *base = reinterpret_cast<const double *>(smem + rows_bytes);
-        for (int i = c.tid; i < a.n_cd * c.M; i += kBlock) {
-            const int r = i / c.M, m = i % c.M;
-            double s = 0.0;
+        const int64_t chunk = s_chunk;
+        __syncthreads();  // every thread has its copy before thread 0 takes the next chunk
+        if (chunk >= a.nchunks) break;
+        if (c.cd_acc) {
+            for (int i = c.lane; i < a.n_cd * MP; i += kWave) c.cd_acc[(i / MP) * kCdStride + i % MP] = 0.0;
+        }
+        const int64_t t0 = chunk * a.chunk_tiles;
+        const int64_t t1 = t0 + a.chunk_tiles < a.ntiles ? t0 + a.chunk_tiles : a.ntiles;
+        for (int64_t tile = t0; tile < t1; ++tile) {
+            const int64_t tb = tile * kTile;
+            if (tb + kTile <= a.P) mix1_tile<MMAX, EXACT, V, PIO, K1, MS, true>(a, c, tb, lo);
+            else mix1_tile<MMAX, EXACT, V, PIO, K1, MS, false>(a, c, tb, lo);
+        }
+        if (c.cd_acc) {
+            __syncthreads();
+            const double *base = reinterpret_cast<const double *>(smem + rows_bytes);
+            for (int i = c.tid; i < a.n_cd * c.M; i += kBlock) {
+                const int r = i / c.M, m = i % c.M;
+                double s = 0.0;
 #pragma unroll
-            for (int w = 0; w < kWavesPerBlock; ++w) s += base[r * kCdStride + w * MP + m];
-            a.cd_partials[(static_cast<int64_t>(blockIdx.x) * a.n_cd + r) * c.M + m] = s;
+                for (int w = 0; w < kWavesPerBlock; ++w) s += base[r * kCdStride + w * MP + m];
+                a.cd_partials[(chunk * a.n_cd + r) * c.M + m] = s;
+            }
+            __syncthreads();  // partials read before the accumulators are cleared for the next chunk
         }
     }
 }
+
+// Sets the chunk counter of a Mix1 launch to 0 (one thread; stream-ordered
+// before the launch).
+__global__ void counter_reset_kernel(int *counter);
 
 // ------------------------------------------------- standalone consensus
 

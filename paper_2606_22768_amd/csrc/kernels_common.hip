@@ -22,6 +22,10 @@ __global__ __launch_bounds__(256) void finalize_kernel(const double *partials, i
     if (t == 0) out[i] = s[0];
 }
 
+__global__ void counter_reset_kernel(int *counter) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) counter[0] = 0;
+}
+
 // Each block iteration moves 4 vectors of 16 bytes per thread; all four loads
 // are issued before the stores.
 __global__ __launch_bounds__(256) void copy_kernel(const u32x4 *src, u32x4 *dst, int64_t n) {

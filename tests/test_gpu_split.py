@@ -160,6 +160,34 @@ def test_split_round_on_two_streams(env):
         eng.close()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_mix1_result_independent_of_block_count(env, dtype):
+    """The Mix1 half takes chunks from a counter; x, the mixed momentum and
+    the consensus rows are bit-identical for any number of blocks."""
+    fgd, torch = env
+    M, P = 8, 300_001
+    ld = pa.aligned_ld(P)
+    tp, _, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, mom_std=1e-3, seed=67)
+    t1 = pa.topo(RING_MH, M, 2, 5)
+    eng = fgd.Engine(M, P, ld, dtype, device=0, mix1_state=True)
+    try:
+        eng.set_topology_dict("mix1", t1)
+        eng.set_topology("mix2", "identity")
+        outs = []
+        for nb in (0, 1, 7, 100, 5000):
+            g_tp, g_v = _dev_rows(torch, tp, dtype), torch.from_numpy(v).cuda()
+            g_x = torch.zeros_like(g_tp)
+            cd = torch.zeros((eng.num_cd_rows_split()[0], M), dtype=torch.float64, device="cuda")
+            eng.mix1(g_tp, g_x, g_v, cd, num_blocks=nb)
+            torch.cuda.synchronize()
+            outs.append((_host_rows(torch, g_x, dtype), g_v.cpu().numpy(), cd.cpu().numpy()))
+        for o in outs[1:]:
+            for a, b in zip(outs[0], o):
+                assert np.array_equal(a, b)
+    finally:
+        eng.close()
+
+
 def test_split_rejections(env):
     fgd, torch = env
     M, P = 4, 1024
@@ -174,6 +202,9 @@ def test_split_rejections(env):
         assert e.value.status == fgd.FGD_ERR_INVALID_ARG
         with pytest.raises(fgd.FgdError) as e:   # x aliases theta_prev
             fgd.fgd_mix1(eng.handle, a, a, v)
+        assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+        with pytest.raises(fgd.FgdError) as e:   # negative block count
+            fgd.fgd_mix1(eng.handle, a, b, v, None, -1)
         assert e.value.status == fgd.FGD_ERR_INVALID_ARG
         with pytest.raises(fgd.FgdError) as e:   # x aliases theta_local
             fgd.fgd_outer_step_blocking(eng.handle, b, a, b, v)
