@@ -276,3 +276,78 @@ def test_split_without_write_back_keeps_theta_local():
     assert np.array_equal(tlq, tl)
     # A global Mix1 stores the same x for every worker.
     assert np.all(x == x[0])
+
+
+# --------------------------------------------------------------- JS distance
+
+import scipy.spatial.distance  # noqa: E402
+
+from oracle import js as ojs  # noqa: E402
+
+
+def _logits(rng, K, scale=2.0):
+    return rng.standard_normal(K) * scale
+
+
+@pytest.mark.parametrize("K", [7, 100, 1000])
+def test_js_full_vocabulary_matches_scipy(K):
+    """k = K: the restricted sum is the full JS divergence, and d equals
+    scipy's jensenshannon(p, q, base=2) of the two softmax distributions."""
+    rng = np.random.default_rng(K)
+    for _ in range(5):
+        za = _logits(rng, K)
+        zw = za + rng.standard_normal(K) * 0.3
+        p = np.exp(zw - zw.max()); p /= p.sum()
+        q = np.exp(za - za.max()); q /= q.sum()
+        want = scipy.spatial.distance.jensenshannon(p, q, base=2)
+        assert abs(ojs.js_distance_token(zw, za, K) - want) <= 1e-12
+
+
+def test_js_identical_is_zero_and_disjoint_is_one():
+    rng = np.random.default_rng(3)
+    za = _logits(rng, 500)
+    assert ojs.js_distance_token(za, za, 100) == 0.0
+    assert ojs.js_distance_token(za + 3.0, za, 500) <= 1e-7  # logits shifted: same distribution
+    # Distributions concentrated on different tokens: distance 1 (normalized maximum).
+    a = np.full(50, -1e4); a[3] = 0.0
+    b = np.full(50, -1e4); b[17] = 0.0
+    assert abs(ojs.js_distance_token(a, b, 50) - 1.0) <= 1e-12
+
+
+def test_js_restricted_sum_is_monotone_in_k():
+    """Every term is non-negative: d grows with k and reaches the full value."""
+    rng = np.random.default_rng(9)
+    K = 800
+    za = _logits(rng, K)
+    zw = za + rng.standard_normal(K) * 0.5
+    ds = [ojs.js_distance_token(zw, za, k) for k in (1, 10, 100, 400, K)]
+    assert all(a <= b + 1e-15 for a, b in zip(ds, ds[1:]))
+    p = np.exp(zw - zw.max()); p /= p.sum()
+    q = np.exp(za - za.max()); q /= q.sum()
+    assert abs(ds[-1] - scipy.spatial.distance.jensenshannon(p, q, base=2)) <= 1e-12
+
+
+def test_js_top_k_by_brute_force_with_ties():
+    """The top-k set against a brute-force selection by repeated argmax
+    (first occurrence wins, so ties go to the lower index)."""
+    rng = np.random.default_rng(5)
+    z = np.round(rng.standard_normal(300) * 2, 1)  # many exact ties
+    for k in (1, 5, 37, 100, 300):
+        left = list(z)
+        picked = []
+        for _ in range(k):
+            i = int(np.argmax(left))
+            picked.append(i)
+            left[i] = -np.inf
+        assert np.array_equal(ojs.top_k_indices(z, k), np.sort(picked))
+
+
+def test_js_distances_shapes_and_means():
+    rng = np.random.default_rng(2)
+    M, U, K = 3, 4, 64
+    za = rng.standard_normal((U, K))
+    zw = za[None] + rng.standard_normal((M, U, K)) * 0.2
+    d, mean, tops = ojs.js_distances(zw, za, k=10)
+    assert d.shape == (M, U) and mean.shape == (M,) and tops.shape == (U, 10)
+    np.testing.assert_allclose(mean, d.mean(axis=1), rtol=0, atol=0)
+    assert np.all((d > 0) & (d < 1))
