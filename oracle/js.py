@@ -47,8 +47,13 @@ def js_distance_token(z_worker, z_avg, k):
     la = za - logsumexp(za)
     t = top_k_indices(za, k)
     lp, la = lp[t], la[t]
-    lmix = np.logaddexp(lp, la) - LOG2
-    js = 0.5 * np.sum(np.exp(lp) * (lp - lmix)) + 0.5 * np.sum(np.exp(la) * (la - lmix))
+    with np.errstate(invalid="ignore"):
+        lmix = np.logaddexp(lp, la) - LOG2
+        # A token of probability 0 on one side contributes 0 to that side's
+        # KL term (0 log 0 = 0); masked tokens have logit -inf.
+        tp = np.where(np.isneginf(lp), 0.0, np.exp(lp) * (lp - lmix))
+        ta = np.where(np.isneginf(la), 0.0, np.exp(la) * (la - lmix))
+    js = 0.5 * np.sum(tp) + 0.5 * np.sum(ta)
     return float(np.sqrt(max(js, 0.0) / LOG2))
 
 

@@ -314,6 +314,23 @@ def test_js_identical_is_zero_and_disjoint_is_one():
     assert abs(ojs.js_distance_token(a, b, 50) - 1.0) <= 1e-12
 
 
+def test_js_masked_tokens_contribute_nothing():
+    """A token of probability 0 on one side adds nothing to that side's KL
+    term (0 log 0 = 0): masking tokens with -inf logits equals scipy's JS on
+    distributions with those probabilities set to 0."""
+    rng = np.random.default_rng(12)
+    K = 300
+    za, zw = _logits(rng, K), _logits(rng, K)
+    za[::7] = -np.inf
+    zw[::5] = -np.inf
+    p = np.exp(zw - zw[np.isfinite(zw)].max()); p /= p.sum()
+    q = np.exp(za - za[np.isfinite(za)].max()); q /= q.sum()
+    want = scipy.spatial.distance.jensenshannon(p, q, base=2)
+    assert abs(ojs.js_distance_token(zw, za, K) - want) <= 1e-12
+    both = np.full(K, -np.inf); both[:3] = [0.0, 1.0, 2.0]
+    assert ojs.js_distance_token(both, both, K) == 0.0
+
+
 def test_js_restricted_sum_is_monotone_in_k():
     """Every term is non-negative: d grows with k and reaches the full value."""
     rng = np.random.default_rng(9)
