@@ -112,6 +112,66 @@ def cpu_baseline(sl, w, topo1, topo2):
             "params_workers_per_s": round(M * p_slice / dt, 1), "host_cpu": model, "host_nproc": ncpu}
 
 
+JS_WORKLOAD = dict(M=8, U=2048, K=128256, dtype="bf16", k=100, seed=0)
+
+
+def js_bench(args, fgd, torch):
+    """Jensen--Shannon functional distance (Appendix D.2): M workers' and the
+    averaged model's logits over U tokens of a K-token vocabulary, resident in
+    HBM; a step is one fgd_js_distance call (distances and their means)."""
+    from synth import logits as slog
+
+    w = JS_WORKLOAD
+    M, U, K, k = w["M"], w["U"], w["K"], w["k"]
+    es = 2 if w["dtype"] == "bf16" else 4
+    print(f"[bench] generating JS logits M={M} U={U} K={K}", file=sys.stderr, flush=True)
+    A, W = slog.torch_logits(M, U, K, K, w["dtype"], seed=w["seed"])
+    d = torch.empty((M, U), dtype=torch.float64, device=A.device)
+    mean = torch.empty(M, dtype=torch.float64, device=A.device)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        fgd.fgd_js_distance(A, W, w["dtype"], M, U, K, K, k, d, mean, None, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    nbytes = (M + 1) * U * K * es
+    exps = (M + 1) * U * K  # one float64 exp per logit (plus one per vector when the running max grows)
+    ms = elapsed * 1e3 / args.steps
+    out = {"metric": "JS distance: logits HBM GB/s and float64 exp/s", "mode": "js", "value": round(nbytes / ms / 1e6, 2),
+           "unit": "GB/s", "ms_per_step": round(ms, 4), "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
+           "step_ms_min": round(step_ms[0], 4), "steps": args.steps, "warmup": args.warmup,
+           "pct_of_hbm_peak": round(100 * nbytes / ms / 1e6 / HBM_PEAK_GBS, 2),
+           "f64_exp_per_s": round(exps / (ms * 1e-3), 1), "tokens_workers_per_s": round(M * U / (ms * 1e-3), 1),
+           "cd_js": float(mean.mean().item()),
+           "config": {"workload": f"js_m{M}_u{U}_v{K}_{w['dtype']}", "workers": M, "tokens": U, "vocab": K,
+                      "top_k": k, "dtype": w["dtype"], "bytes_per_step": nbytes},
+           "kernel_source_hash": kernel_source_hash()}
+    if not args.no_cpu_baseline:
+        from oracle import js as ojs
+
+        n = 4
+        za = A[:n].float().cpu().numpy()
+        zw = W[:, :n].float().cpu().numpy()
+        t0 = time.perf_counter()
+        ojs.js_distances(zw, za, k)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round((M + 1) * n * K * es / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+                               "kind": "oracle", "sample": f"first {n} of {U} tokens, all {M} workers, {dt:.2f} s",
+                               "tokens_workers_per_s": round(M * n / dt, 2)}
+    print(json.dumps(out))
+
+
 def split_round_bench(args, eng, torch, tp, tl, v, w, step_topos):
     """Split execution of a round (Appendix A, Algorithm 1): the Mix1 half is
     launched on a side stream at the start of the round and overlaps a
@@ -209,9 +269,10 @@ def main():
     ap.add_argument("--cpu-slice", type=int, default=1 << 25, help="parameters per worker in the CPU sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
-    ap.add_argument("--mode", choices=["fused", "split"], default="fused",
+    ap.add_argument("--mode", choices=["fused", "split", "js"], default="fused",
                     help="fused: one-pass outer step (the benchmark); split: Mix1 half on a side stream "
-                         "overlapping a stand-in inner loop, then the blocking half")
+                         "overlapping a stand-in inner loop, then the blocking half; js: Jensen-Shannon "
+                         "distance of 8 workers over 2048 tokens of a 128256-token vocabulary (bf16 logits)")
     ap.add_argument("--mix1-blocks", type=int, default=0,
                     help="split mode: blocks of the Mix1 half (0: one per CU)")
     args = ap.parse_args()
@@ -230,6 +291,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a HIP device", file=sys.stderr)
         sys.exit(1)
+    if args.mode == "js":
+        js_bench(args, fgd, torch)
+        return
     w = configs.WORKLOADS[args.workload]
     M, P, dtype = w["M"], w["P"], w["dtype"]
     ld = -(-P // 8) * 8

@@ -260,6 +260,38 @@ fgd_status fgd_min_bytes_per_step(const fgd_engine *e, int64_t *bytes);
 fgd_status fgd_enable_timing(fgd_engine *e, int32_t enable);
 fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count);
 
+#define FGD_MAX_JS_TOPK 1024    /* largest top_k of fgd_js_distance */
+#define FGD_MAX_JS_WORKERS 4096 /* largest num_workers of fgd_js_distance */
+
+/* Jensen--Shannon functional distance (Sec. 4.4; Appendix D.2) between
+ * every worker's predicted token distribution and the parameter-averaged
+ * model's, from their logits on a fixed batch of tokens.  Per worker m and
+ * token u, in float64 and the log domain: log p = z - logsumexp(z) over the
+ * full vocabulary for the worker and for the averaged model; T(u) = the
+ * top_k tokens of the averaged model (the paper uses 100; equal logits: the
+ * lower token index first); JS = 1/2 sum_{i in T} p_m,i log(p_m,i / mix_i)
+ * + 1/2 sum_{i in T} pbar_i log(pbar_i / mix_i), mix = (p_m + pbar) / 2;
+ * d_m(u) = sqrt(max(JS, 0) / log 2).  The probabilities are those of the full
+ * softmax; only the sum is restricted to T (a lower bound of the full JS,
+ * equal to it at top_k = vocab).  No engine is needed.
+ *   logits_avg      device [U][ldk] dtype: the averaged model's logits
+ *   logits_workers  device [M][U][ldk] dtype: worker m's row for token u
+ *                   starts at element (m * U + u) * ldk
+ *   dtype           FGD_F32 or FGD_BF16; logits must not be NaN or +inf
+ *                   (-inf, a masked token, is allowed)
+ *   num_workers     M in [1, FGD_MAX_JS_WORKERS]; num_tokens U >= 1
+ *   vocab, ldk      K <= ldk; ldk * elem_size a multiple of 16 (16-byte
+ *                   aligned rows); elements [K, ldk) are read, never used
+ *   top_k           in [1, min(K, FGD_MAX_JS_TOPK)]
+ *   d_out           device double[M][U]: d_m(u)
+ *   mean_out        device double[M] or NULL: the mean of d_m(u) over u
+ *                   (the paper's CD_JS is the mean of these M values)
+ *   topk_out        device int32[U][top_k] or NULL: T(u) in ascending order
+ * Enqueued on `stream`; deterministic. */
+fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, int32_t dtype, int32_t num_workers,
+                           int64_t num_tokens, int64_t vocab, int64_t ldk, int32_t top_k, double *d_out,
+                           double *mean_out, int32_t *topk_out, void *stream);
+
 /* Plain device copy of `bytes` bytes (16-byte aligned pointers, bytes % 16 ==
  * 0) on `stream`: the streaming reference against which the step's
  * bandwidth and traffic counters are read. */

@@ -25,6 +25,7 @@ FGD_MIX1, FGD_MIX2 = 1, 2
 FGD_W_IDENTITY, FGD_W_GLOBAL_MEAN, FGD_W_CSR = 0, 1, 2
 FGD_REWEIGHT_NONE, FGD_REWEIGHT_METROPOLIS, FGD_REWEIGHT_SELF = 0, 1, 2
 FGD_MAX_WORKERS, FGD_MAX_ROUNDS, FGD_MAX_SUBSET_SEGMENTS = 64, 8, 4096
+FGD_MAX_JS_TOPK, FGD_MAX_JS_WORKERS = 1024, 4096
 
 DTYPES = {"f32": FGD_F32, "bf16": FGD_BF16}
 KINDS = {"identity": FGD_W_IDENTITY, "global": FGD_W_GLOBAL_MEAN, "csr": FGD_W_CSR}
@@ -75,6 +76,7 @@ def _load():
         "fgd_enable_timing": (I32, [P, I32]),
         "fgd_read_timing": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
         "fgd_stream_copy": (I32, [P, P, I64, P]),
+        "fgd_js_distance": (I32, [P, P, I32, I32, I64, I64, I64, I32, P, P, P, P]),
         "fgd_status_string": (ctypes.c_char_p, [I32]),
         "fgd_last_error": (ctypes.c_char_p, []),
     }
@@ -234,6 +236,35 @@ def fgd_read_timing(h):
     ms, n = ctypes.c_double(), ctypes.c_int64()
     _check(lib.fgd_read_timing(h, ctypes.byref(ms), ctypes.byref(n)), "fgd_read_timing")
     return ms.value, n.value
+
+
+def fgd_js_distance(logits_avg, logits_workers, dtype, num_workers, num_tokens, vocab, ldk, top_k, d_out,
+                    mean_out=None, topk_out=None, stream=None):
+    _check(lib.fgd_js_distance(_dev(logits_avg), _dev(logits_workers), DTYPES.get(dtype, dtype), int(num_workers),
+                               int(num_tokens), int(vocab), int(ldk), int(top_k), _dev(d_out), _dev(mean_out),
+                               _dev(topk_out), _stream(stream)), "fgd_js_distance")
+
+
+def js_distance(logits_avg, logits_workers, top_k=100, vocab=None, d_out=None, mean_out=None, topk_out=None,
+                stream=None):
+    """Tensor-level call: logits_avg [U][ldk], logits_workers [M][U][ldk]
+    (float32 or bfloat16, rows contiguous); returns (d [M][U], mean [M])."""
+    import torch
+
+    dtype = {torch.float32: "f32", torch.bfloat16: "bf16"}[logits_avg.dtype]
+    if logits_workers.dtype != logits_avg.dtype:
+        raise TypeError("logits_avg and logits_workers must share a dtype")
+    U, ldk = logits_avg.shape
+    M = logits_workers.shape[0]
+    if tuple(logits_workers.shape) != (M, U, ldk) or not logits_workers.is_contiguous() \
+            or not logits_avg.is_contiguous():
+        raise ValueError("expected contiguous logits_avg [U][ldk] and logits_workers [M][U][ldk]")
+    K = ldk if vocab is None else int(vocab)
+    dev = logits_avg.device
+    d_out = torch.empty((M, U), dtype=torch.float64, device=dev) if d_out is None else d_out
+    mean_out = torch.empty(M, dtype=torch.float64, device=dev) if mean_out is None else mean_out
+    fgd_js_distance(logits_avg, logits_workers, dtype, M, U, K, ldk, top_k, d_out, mean_out, topk_out, stream)
+    return d_out, mean_out
 
 
 def fgd_stream_copy(dst, src, nbytes, stream=None):

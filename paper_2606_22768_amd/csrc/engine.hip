@@ -721,6 +721,33 @@ fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count) {
     return FGD_OK;
 }
 
+fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, int32_t dtype, int32_t num_workers,
+                           int64_t num_tokens, int64_t vocab, int64_t ldk, int32_t top_k, double *d_out,
+                           double *mean_out, int32_t *topk_out, void *stream_handle) {
+    g_last_error.clear();
+    if (dtype != FGD_F32 && dtype != FGD_BF16) return fail(FGD_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+    const int es = elem_size(dtype);
+    if (!logits_avg || !logits_workers || !d_out) return fail(FGD_ERR_INVALID_ARG, "NULL array");
+    if (!aligned16(logits_avg) || !aligned16(logits_workers))
+        return fail(FGD_ERR_INVALID_ARG, "logit arrays must be 16-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(d_out) & 7u) || (mean_out && (reinterpret_cast<uintptr_t>(mean_out) & 7u)) ||
+        (topk_out && (reinterpret_cast<uintptr_t>(topk_out) & 3u)))
+        return fail(FGD_ERR_INVALID_ARG, "outputs must be aligned to their element size");
+    if (num_workers < 1 || num_workers > FGD_MAX_JS_WORKERS)
+        return fail(FGD_ERR_INVALID_ARG, "num_workers %d is outside [1, %d]", num_workers, FGD_MAX_JS_WORKERS);
+    if (num_tokens < 1 || num_tokens > INT32_MAX) return fail(FGD_ERR_INVALID_ARG, "num_tokens must be in [1, 2^31)");
+    if (vocab < 1 || ldk < vocab) return fail(FGD_ERR_INVALID_ARG, "need 1 <= vocab <= ldk");
+    if ((ldk * es) % 16 != 0 || ldk * es > INT32_MAX)
+        return fail(FGD_ERR_INVALID_ARG, "rows must be a multiple of 16 bytes and below 2 GB");
+    if (top_k < 1 || top_k > FGD_MAX_JS_TOPK || top_k > vocab)
+        return fail(FGD_ERR_INVALID_ARG, "top_k %d is outside [1, min(vocab, %d)]", top_k, FGD_MAX_JS_TOPK);
+    hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    if (!fgd::js_launch(logits_avg, logits_workers, dtype == FGD_BF16, num_workers, num_tokens, vocab, ldk, top_k,
+                        d_out, mean_out, topk_out, stream))
+        return fail(FGD_ERR_HIP, "JS distance launch failed");
+    return FGD_OK;
+}
+
 fgd_status fgd_stream_copy(void *dst, const void *src, int64_t bytes, void *stream_handle) {
     g_last_error.clear();
     if (!dst || !src || bytes < 0 || bytes % 16 != 0 || !aligned16(dst) || !aligned16(src))

@@ -1097,5 +1097,9 @@ bool kernels_bf16_ms(int M, int k1, int k2, bool subset, KernelSet *out);
 // Split-execution kernels.
 bool split_kernels_f32(int M, int k1, int k2, bool subset, bool mix_state, SplitSet *out);
 bool split_kernels_bf16(int M, int k1, int k2, bool subset, bool mix_state, SplitSet *out);
+// Jensen--Shannon distance (js.hip): launches the per-token kernel and, when
+// mean_out is given, the per-worker mean; false if a launch failed.
+bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
+               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, hipStream_t stream);
 
 }  // namespace fgd

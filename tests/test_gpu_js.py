@@ -1,0 +1,131 @@
+"""GPU parity of the Jensen--Shannon functional distance (Sec. 4.4;
+Appendix D.2) against the float64 oracle, through the C ABI.
+
+The selected token sets are integer results and must match exactly (both
+sides compare the stored logits, ties to the lower index); the distances
+are float64 on both sides with different summation orders and exp/log
+implementations, so they are held to 1e-10 absolute (their rounding error
+is of order 1e-14, see the tolerance derivation in the design notes).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import js as ojs
+from synth import logits as slog
+from synth import tensors
+
+pytestmark = pytest.mark.gpu
+
+D_ATOL = 1e-10
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2606_22768_amd as fgd
+
+    return fgd, torch
+
+
+def _values(a, dtype):
+    return tensors.bf16_bits_to_f32(a) if dtype == "bf16" else a
+
+
+def _run(fgd, torch, A, W, dtype, K, k):
+    U, ldk = A.shape
+    M = W.shape[0]
+    conv = (lambda x: torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)) if dtype == "bf16" \
+        else (lambda x: torch.from_numpy(x).cuda())
+    gA, gW = conv(A), conv(W)
+    d = torch.full((M, U), float("nan"), dtype=torch.float64, device="cuda")
+    mean = torch.full((M,), float("nan"), dtype=torch.float64, device="cuda")
+    tops = torch.full((U, k), -1, dtype=torch.int32, device="cuda")
+    fgd.fgd_js_distance(gA, gW, dtype, M, U, K, ldk, k, d, mean, tops)
+    torch.cuda.synchronize()
+    return d.cpu().numpy(), mean.cpu().numpy(), tops.cpu().numpy()
+
+
+def _check(fgd, torch, A, W, dtype, K, k):
+    d, mean, tops = _run(fgd, torch, A, W, dtype, K, k)
+    za = _values(A, dtype)[:, :K]
+    zw = _values(W, dtype)[:, :, :K]
+    rd, rmean, rtops = ojs.js_distances(zw, za, k)
+    assert np.array_equal(tops, rtops), "top-k token sets differ"
+    np.testing.assert_allclose(d, rd, rtol=0, atol=D_ATOL)
+    np.testing.assert_allclose(mean, rmean, rtol=0, atol=D_ATOL)
+    return d
+
+
+CASES = [
+    # (M, U, K, ldk, dtype, k)
+    (8, 5, 1000, 1000, "f32", 100),
+    (8, 5, 1000, 1008, "bf16", 100),
+    (3, 7, 5003, 5008, "f32", 100),          # ragged vocabulary
+    (3, 7, 5003, 5008, "bf16", 37),
+    (1, 4, 32000, 32000, "bf16", 100),       # bf16: many exact ties among the logits
+    (2, 3, 7, 8, "f32", 7),                  # full vocabulary (k = K)
+    (2, 3, 500, 504, "bf16", 500),
+    (4, 2, 20000, 20000, "f32", 1024),       # largest k
+    (5, 3, 3000, 3000, "bf16", 1),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"M{c[0]}-U{c[1]}-K{c[2]}-{c[4]}-k{c[5]}")
+def test_js_parity(env, case):
+    fgd, torch = env
+    M, U, K, ldk, dtype, k = case
+    print(f"[js] {case}", flush=True)
+    A, W = slog.numpy_logits(M, U, K, ldk, dtype, seed=K + M)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+def test_js_ties_across_the_threshold(env):
+    """Logits on a coarse grid: the k-th largest value is shared by many
+    tokens, so the selection must split a tie (lower indices first)."""
+    fgd, torch = env
+    M, U, K, k = 3, 6, 4000, 100
+    rng = np.random.default_rng(71)
+    za = np.round(rng.standard_normal((U, K)) * 2).astype(np.float32)  # integers: huge ties
+    zw = (za[None] + rng.standard_normal((M, U, K)).astype(np.float32) * np.float32(0.3)).astype(np.float32)
+    _check(fgd, torch, za, zw, "f32", K, k)
+    zb = np.zeros((U, K), np.float32)  # all equal: the first k tokens
+    d, _, tops = _run(fgd, torch, zb, np.zeros((M, U, K), np.float32), "f32", K, k)
+    assert np.array_equal(tops, np.tile(np.arange(k, dtype=np.int32), (U, 1)))
+    assert np.all(d == 0.0)
+
+
+def test_js_masked_tokens_and_signed_zero(env):
+    """-inf logits (masked tokens) take no probability; -0 and +0 compare
+    equal in the selection."""
+    fgd, torch = env
+    M, U, K, k = 2, 4, 2000, 100
+    A, W = slog.numpy_logits(M, U, K, K, "f32", seed=5)
+    A[:, ::3] = -np.inf
+    W[:, :, ::5] = -np.inf
+    A[:, 7], A[:, 8] = -0.0, 0.0
+    _check(fgd, torch, A, W, "f32", K, k)
+
+
+def test_js_identical_workers_are_zero(env):
+    fgd, torch = env
+    A, W = slog.numpy_logits(4, 3, 3000, 3000, "bf16", seed=9, noise=0.0)
+    d, mean, _ = _run(fgd, torch, A, W, "bf16", 3000, 100)
+    assert np.all(d == 0.0) and np.all(mean == 0.0)
+
+
+def test_js_rejections(env):
+    fgd, torch = env
+    A = torch.zeros((2, 64), device="cuda")
+    W = torch.zeros((3, 2, 64), device="cuda")
+    d = torch.zeros((3, 2), dtype=torch.float64, device="cuda")
+    for kw in (dict(top_k=0), dict(top_k=65), dict(top_k=2000), dict(ldk=62, vocab=60), dict(vocab=65),
+               dict(num_tokens=0), dict(dtype=7), dict(num_workers=0)):
+        args = dict(dtype="f32", num_workers=3, num_tokens=2, vocab=64, ldk=64, top_k=10)
+        args.update(kw)
+        with pytest.raises(fgd.FgdError) as e:
+            fgd.fgd_js_distance(A, W, args["dtype"], args["num_workers"], args["num_tokens"], args["vocab"],
+                                args["ldk"], args["top_k"], d)
+        assert e.value.status == fgd.FGD_ERR_INVALID_ARG
