@@ -129,3 +129,31 @@ def test_js_rejections(env):
             fgd.fgd_js_distance(A, W, args["dtype"], args["num_workers"], args["num_tokens"], args["vocab"],
                                 args["ldk"], args["top_k"], d)
         assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+
+
+def test_js_full_size_sampled_tokens(env):
+    """The benchmark's size (8 workers, 2048 tokens, 128256-token vocabulary,
+    bf16): the distances and top-k sets of sampled tokens against the oracle
+    (every token is independent, so the oracle on the sampled rows is exact
+    parity for them), plus the mean over all tokens against the engine's own
+    per-token distances summed in float64."""
+    fgd, torch = env
+    M, U, K, k = 8, 2048, 128256, 100
+    print("[js] full size: generating logits", flush=True)
+    A, W = slog.torch_logits(M, U, K, K, "bf16", seed=0)
+    d = torch.empty((M, U), dtype=torch.float64, device="cuda")
+    mean = torch.empty(M, dtype=torch.float64, device="cuda")
+    tops = torch.empty((U, k), dtype=torch.int32, device="cuda")
+    fgd.fgd_js_distance(A, W, "bf16", M, U, K, K, k, d, mean, tops)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    sample = np.unique(np.concatenate([[0, U - 1], rng.integers(0, U, 14)]))
+    za = A[sample].float().cpu().numpy()
+    zw = W[:, sample].float().cpu().numpy()
+    rd, _, rtops = ojs.js_distances(zw, za, k)
+    assert np.array_equal(tops.cpu().numpy()[sample], rtops)
+    np.testing.assert_allclose(d.cpu().numpy()[:, sample], rd, rtol=0, atol=D_ATOL)
+    dh = d.cpu().numpy()
+    np.testing.assert_allclose(mean.cpu().numpy(), dh.mean(axis=1), rtol=1e-13)
+    assert np.all((dh > 0) & (dh < 1))
+    print(f"[js] full size: CD_JS = {dh.mean():.6f}", flush=True)
