@@ -254,3 +254,55 @@ def test_subset_limits():
         assert fgd.lib.fgd_set_mix2_subset(eng.handle, None, -1) == fgd.FGD_ERR_INVALID_ARG
     finally:
         eng.close()
+
+
+def test_header_compiles_as_c99_and_links(tmp_path):
+    """include/fgd.h is a plain C header: a C99 program that includes it,
+    links libfgd.so and calls host-only entry points (a host-only engine and
+    the stand-alone weight computation) builds with -Wall -Werror -pedantic
+    and runs.  No GPU is touched."""
+    src = tmp_path / "abi_check.c"
+    src.write_text(r"""
+#include <stdio.h>
+#include <string.h>
+#include "fgd.h"
+int main(void) {
+    fgd_config c;
+    fgd_engine *e = NULL;
+    int32_t rp[4] = {0, 2, 5, 7}, ci[7] = {0, 1, 0, 1, 2, 1, 2};
+    float w[7], out[7];
+    int32_t rows = 0;
+    memset(&c, 0, sizeof c);
+    c.struct_size = sizeof c;
+    c.num_workers = 3;
+    c.num_params = 64;
+    c.ld = 64;
+    c.param_dtype = FGD_F32;
+    c.state_dtype = FGD_F32;
+    c.outer_lr = 0.7f;
+    c.momentum = 0.9f;
+    c.nesterov = 1;
+    c.device = -1;
+    if (fgd_create(&c, &e) != FGD_OK) { printf("create: %s\n", fgd_last_error()); return 1; }
+    if (fgd_set_topology(e, FGD_MIX1, FGD_W_GLOBAL_MEAN, NULL, NULL, NULL, 1, NULL, FGD_REWEIGHT_NONE) != FGD_OK) return 2;
+    if (fgd_set_topology(e, FGD_MIX2, FGD_W_CSR, rp, ci, NULL, 2, NULL, FGD_REWEIGHT_METROPOLIS) != FGD_OK) return 3;
+    if (fgd_num_cd_rows(e, &rows) != FGD_OK || rows != 2 + 1 + 1 + 1 + 1) return 4;
+    if (fgd_get_effective_weights(e, FGD_MIX2, 1, w) != FGD_OK) return 5;
+    if (fgd_effective_weights(3, rp, ci, NULL, NULL, FGD_REWEIGHT_METROPOLIS, out) != FGD_OK) return 6;
+    if (memcmp(w, out, sizeof w) != 0) return 7;
+    if (fgd_outer_step(e, NULL, NULL, NULL, NULL, NULL) != FGD_ERR_STATE) return 8;  /* host-only engine */
+    if (strcmp(fgd_status_string(FGD_ERR_TOPOLOGY), "FGD_ERR_TOPOLOGY") != 0) return 9;
+    fgd_destroy(e);
+    printf("ok %g %g %g\n", w[0], w[1], w[2]);
+    return 0;
+}
+""")
+    exe = tmp_path / "abi_check"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    libdir = os.path.dirname(fgd.LIB_PATH)
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", inc, str(src), "-o", str(exe),
+                    "-L", libdir, "-lfgd", f"-Wl,-rpath,{libdir}"], check=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
+    # Path graph 0-1-2, Metropolis: degrees 1, 2, 1 -> w01 = w12 = 1/3, w00 = w22 = 2/3, w11 = 1/3.
+    assert r.stdout.split()[:4] == ["ok", f"{np.float32(2 / 3):g}", f"{np.float32(1 / 3):g}", f"{np.float32(1 / 3):g}"]
