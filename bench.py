@@ -285,6 +285,9 @@ def main():
 
     import torch
 
+    import __graft_entry__
+
+    __graft_entry__.ensure_built()  # builds only when no library is present
     import paper_2606_22768_amd as fgd
     from synth import configs, tensors
 
