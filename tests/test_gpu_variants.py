@@ -136,3 +136,48 @@ def test_subset_needs_csr_mix2(env):
         assert ei.value.status == fgd.FGD_ERR_UNSUPPORTED
     finally:
         eng.close()
+
+
+def _random_case(i):
+    """A seeded random configuration: worker count, size, storage, mixing kinds
+    and rounds, masks and reweighting, optimizer form, state mix, subset."""
+    rng = np.random.default_rng(1000 + i)
+    M = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 9, 12, 16, 17, 24, 32, 33, 48, 64]))
+    P = int(rng.integers(1, 6000))
+    dtype = str(rng.choice(["f32", "bf16"]))
+
+    def spec():
+        c = rng.integers(0, 6)
+        if c == 0:
+            return ID, 0
+        if c == 1:
+            return G, 1
+        if c == 2:
+            return ("complete",), int(rng.integers(1, 3))
+        if c == 3:
+            return ("er_mh", float(rng.uniform(0.1, 0.9)), float(rng.uniform(0, 0.5))), int(rng.integers(1, 4))
+        if c == 4:
+            return ("ring_self", float(rng.uniform(0, 0.5))), int(rng.integers(1, 4))
+        return ("matching",), int(rng.integers(1, 3))
+
+    (s1, k1), (s2, k2) = spec(), spec()
+    if M < 3 and s2[0] in ("ring_self",):
+        s2, k2 = G, 1
+    if M < 3 and s1[0] in ("ring_self",):
+        s1, k1 = G, 1
+    subset = None
+    csr2 = s2[0] not in ("identity", "global")
+    if csr2 and rng.random() < 0.5:
+        cuts = np.sort(rng.choice(np.arange(0, P + 1), size=min(P + 1, 2 * int(rng.integers(1, 4))), replace=False))
+        subset = [(int(a), int(b)) for a, b in zip(cuts[0::2], cuts[1::2]) if b > a] or None
+    return dict(M=M, P=P, dtype=dtype, s1=s1, k1=k1, s2=s2, k2=k2, nesterov=bool(rng.random() < 0.7),
+                state=bool(rng.random() < 0.3), subset=subset)
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_random_configurations(env, i):
+    fgd, torch = env
+    c = _random_case(i)
+    print(f"[variants] random case {i}: {c}", flush=True)
+    pa.run_case(fgd, torch, c["M"], c["P"], c["dtype"], c["s1"], c["k1"], c["s2"], c["k2"], seed=100 + i,
+                mom_std=1e-3, nesterov=c["nesterov"], mix1_state=c["state"], subset=c["subset"])
