@@ -215,3 +215,52 @@ def test_split_rejections(env):
         assert e.value.status == fgd.FGD_ERR_UNSUPPORTED
     finally:
         eng.close()
+
+
+def test_topology_ring_wraps_across_streams(env):
+    """Twelve rounds on one engine that alternate the fused step and the split
+    halves on two streams, with new edge masks every round: each round
+    re-uploads the tables (a new mask, or a different stream), so the eight
+    topology slots wrap several times while earlier launches may still be in
+    flight.  Before each round the engine's arrays are loaded with the
+    oracle's state (no engine output reaches the oracle); every round is
+    checked."""
+    fgd, torch = env
+    M, P, dtype = 8, 20_011, "f32"
+    ld = pa.aligned_ld(P)
+    tp, tl, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, mom_std=1e-3, seed=73)
+    t1 = pa.topo(G, M, 1)
+    m1 = oracle.Mix.from_topology(t1)
+    eng = fgd.Engine(M, P, ld, dtype, device=0)
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    try:
+        eng.set_topology_dict("mix1", t1)
+        g_tp, g_tl, g_v = (torch.from_numpy(a).cuda() for a in (tp, tl, v))
+        g_x = torch.empty_like(g_tp)
+        cur_t, cur_v = tp, v
+        scale = float(np.abs(tp).max())
+        for r in range(12):
+            t2 = pa.topo(RING_MH, M, 1, seed=0, step=r)
+            m2 = oracle.Mix.from_topology(t2)
+            eng.set_topology_dict("mix2", t2)
+            g_tp.copy_(torch.from_numpy(cur_t))
+            g_v.copy_(torch.from_numpy(cur_v))
+            if r % 2 == 0:
+                ref_t, ref_v, _ = oracle.outer_step(cur_t, tl, cur_v, m1, m2, P=P)
+                eng.outer_step(g_tp, g_tl, g_v, None, main)
+            else:
+                ref_x, _, _ = oracle.mix1_split(cur_t, m1, P=P)
+                ref_t, _, ref_v, _ = oracle.outer_blocking(ref_x, cur_t, tl, cur_v, m2, P=P)
+                side.wait_stream(main)
+                with torch.cuda.stream(side):
+                    eng.mix1(g_tp, g_x, None, None, side)
+                    done = torch.cuda.Event()
+                    done.record(side)
+                main.wait_event(done)
+                eng.outer_step_blocking(g_x, g_tp, g_tl, g_v, None, stream=main)
+            torch.cuda.synchronize()
+            pa.compare_outputs(dtype, g_tp.cpu().numpy(), ref_t, g_v.cpu().numpy(), ref_v, P, scale)
+            cur_t, cur_v = ref_t, ref_v
+    finally:
+        eng.close()
