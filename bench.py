@@ -32,14 +32,23 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 METRIC = "outer-step HBM GB/s and % of MI355X HBM peak; params·workers/sec"
 
 
-def kernel_source_hash():
-    """Hash of the HIP sources; traffic counters are valid only for this hash."""
+def kernel_source_hash(component="step"):
+    """Hash of the HIP sources of one component: "step" (the fused step, the
+    split halves, consensus, finalize and copy kernels and their launches:
+    every source but the JS distance's) or "js" (the JS distance kernels and
+    the header they include).  Traffic counters are valid only for the hash
+    they were taken with."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_22768_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+        if not name.endswith((".hip", ".hpp")):
+            continue
+        if component == "js" and name not in ("js.hip", "kernels.hpp"):
+            continue
+        if component == "step" and name == "js.hip":
+            continue
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 
@@ -146,7 +155,7 @@ def js_bench(args, fgd, torch):
     elapsed = time.perf_counter() - t0
     step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
     nbytes = (M + 1) * U * K * es
-    exps = (M + 1) * U * K  # one float64 exp per logit (plus one per vector when the running max grows)
+    exps = (M + 1) * U * K  # one float64 exp per logit (plus one, rarely, when a lane's shift moves)
     ms = elapsed * 1e3 / args.steps
     out = {"metric": "JS distance: logits HBM GB/s and float64 exp/s", "mode": "js", "value": round(nbytes / ms / 1e6, 2),
            "unit": "GB/s", "ms_per_step": round(ms, 4), "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
@@ -156,7 +165,7 @@ def js_bench(args, fgd, torch):
            "cd_js": float(mean.mean().item()),
            "config": {"workload": f"js_m{M}_u{U}_v{K}_{w['dtype']}", "workers": M, "tokens": U, "vocab": K,
                       "top_k": k, "dtype": w["dtype"], "bytes_per_step": nbytes},
-           "kernel_source_hash": kernel_source_hash()}
+           "kernel_source_hash": kernel_source_hash("js")}
     if not args.no_cpu_baseline:
         from oracle import js as ojs
 

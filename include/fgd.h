@@ -283,7 +283,8 @@ fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count);
  *   vocab, ldk      K <= ldk; ldk * elem_size a multiple of 16 (16-byte
  *                   aligned rows); elements [K, ldk) are read, never used
  *   top_k           in [1, min(K, FGD_MAX_JS_TOPK)]
- *   d_out           device double[M][U]: d_m(u)
+ *   d_out           device double[M][U]: d_m(u) (between the call's two
+ *                   kernels it holds the workers' log-sum-exps)
  *   mean_out        device double[M] or NULL: the mean of d_m(u) over u
  *                   (the paper's CD_JS is the mean of these M values)
  *   topk_out        device int32[U][top_k] or NULL: T(u) in ascending order

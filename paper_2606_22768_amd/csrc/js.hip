@@ -2,23 +2,32 @@
 // predicted token distribution and the parameter-averaged model's
 // (Sec. 4.4, JS distance; Appendix D.2, JS functional disagreement).
 //
-// For token u (one block per token), in float64 and in the log domain:
-//   lse_a        = log sum_i exp(zbar_i)              averaged model's row
-//   T            = the k largest zbar_i (ties: lower index first), found by a
-//                  radix select over order-preserving integer keys of the
-//                  stored logits (exact comparisons: no rounding decides it)
-//   for every worker m:
-//     lse_m      = log sum_i exp(z_m,i)               a streaming pass over the row
-//     JS_m       = sum over i in T of the per-token terms
-//                  1/2 p (lp - lmix) + 1/2 q (lq - lmix), lp = z_m,i - lse_m,
-//                  lq = zbar_i - lse_a, lmix = log((p + q) / 2)
-//     d_m(u)     = sqrt(max(JS_m, 0) / log 2)
+// For token u, in float64 and in the log domain:
+//   lse_m      = log sum_i exp(z_m,i)               every worker row
+//   lse_a      = log sum_i exp(zbar_i)              the averaged model's row
+//   T          = the k largest zbar_i (ties: lower index first), found by a
+//                radix select over order-preserving integer keys of the
+//                stored logits (exact comparisons: no rounding decides it)
+//   JS_m       = sum over i in T of the per-token terms
+//                1/2 p (lp - lmix) + 1/2 q (lq - lmix), lp = z_m,i - lse_m,
+//                lq = zbar_i - lse_a, lmix = log((p + q) / 2)
+//   d_m(u)     = sqrt(max(JS_m, 0) / log 2)
 // Probabilities are those of the full softmax; only the sum is restricted to
-// T.  The log-sum-exp of a row is an online (max, scaled sum) reduction, one
-// float64 exp per element plus one per 16-byte vector when the running max
-// grows; every reduction has a fixed order, so results are deterministic.
-// The selected indices are rank-sorted so that the JS sum runs in index
-// order.
+// T.  Two kernels: js_lse_kernel takes one (token, worker) row per block, so
+// the bulk of the work (M of the M + 1 rows) spreads over M * U blocks, and
+// parks lse_m in d_out; js_kernel takes one token per block: the averaged
+// row, the selection and the JS terms, and overwrites d_out with d_m(u).
+//
+// The log-sum-exp of a row is a (shift, scaled sum) reduction: the shift is
+// a lane's first finite value and moves only when a later value exceeds it
+// by more than kLseSlack, so every exponent is at most kLseSlack and the
+// sums cannot overflow.  exp is a table-driven float64 exp (Tang's method:
+// ACM TOMS 15(2), 1989): x = (256 n + j) ln2/256 + r with |r| <= ln2/512,
+// exp(x) = 2^n 2^(j/256) (1 + q(r)), q the degree-4 Taylor polynomial of
+// e^r - 1 (truncation below 0.4 ulp), 2^(j/256) from a table in LDS; within
+// 2 ulp of the correctly rounded value.  Every reduction has a fixed order,
+// so results are deterministic.  The selected indices are rank-sorted so
+// that the JS sum runs in index order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -50,6 +59,10 @@ struct JsF32 {
             key[j] = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
         }
     }
+    __device__ static void values(u32x4 t, float (&v)[kPer]) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = __uint_as_float(t[j]);
+    }
     __device__ static float at(rsrc_t r, int64_t i) {
         return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, static_cast<uint32_t>(i * 4), 0, 0));
     }
@@ -64,6 +77,13 @@ struct JsBF16 {
             if ((h & 0x7FFFu) == 0) h = 0;
             v[j] = __uint_as_float(h << 16);
             key[j] = (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u);
+        }
+    }
+    __device__ static void values(u32x4 t, float (&v)[kPer]) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = __uint_as_float(t[j] << 16);
+            v[2 * j + 1] = __uint_as_float(t[j] & 0xFFFF0000u);
         }
     }
     __device__ static float at(rsrc_t r, int64_t i) {
@@ -122,164 +142,446 @@ __device__ inline double block_sum(double x, double *red) {
     return t;
 }
 
-// One 16-byte vector of a row: values, keys and how many lie below K.
+// ------------------------------------------------------------ float64 exp
+// 2^(j/256) for j = 0..255, each the double nearest to the exact value.
+constexpr int kTabBits = 8;
+constexpr int kTab = 1 << kTabBits;
+static_assert(kTab <= kBlock, "one thread per table entry loads the LDS copy");
+__constant__ double kExp2Frac[kTab] = {
+    0x1.0000000000000p+0, 0x1.00b1afa5abcbfp+0, 0x1.0163da9fb3335p+0, 0x1.02168143b0281p+0,
+    0x1.02c9a3e778061p+0, 0x1.037d42e11bbccp+0, 0x1.04315e86e7f85p+0, 0x1.04e5f72f654b1p+0,
+    0x1.059b0d3158574p+0, 0x1.0650a0e3c1f89p+0, 0x1.0706b29ddf6dep+0, 0x1.07bd42b72a836p+0,
+    0x1.0874518759bc8p+0, 0x1.092bdf66607e0p+0, 0x1.09e3ecac6f383p+0, 0x1.0a9c79b1f3919p+0,
+    0x1.0b5586cf9890fp+0, 0x1.0c0f145e46c85p+0, 0x1.0cc922b7247f7p+0, 0x1.0d83b23395decp+0,
+    0x1.0e3ec32d3d1a2p+0, 0x1.0efa55fdfa9c5p+0, 0x1.0fb66affed31bp+0, 0x1.1073028d7233ep+0,
+    0x1.11301d0125b51p+0, 0x1.11edbab5e2ab6p+0, 0x1.12abdc06c31ccp+0, 0x1.136a814f204abp+0,
+    0x1.1429aaea92de0p+0, 0x1.14e95934f312ep+0, 0x1.15a98c8a58e51p+0, 0x1.166a45471c3c2p+0,
+    0x1.172b83c7d517bp+0, 0x1.17ed48695bbc0p+0, 0x1.18af9388c8deap+0, 0x1.1972658375d2fp+0,
+    0x1.1a35beb6fcb75p+0, 0x1.1af99f8138a1cp+0, 0x1.1bbe084045cd4p+0, 0x1.1c82f95281c6bp+0,
+    0x1.1d4873168b9aap+0, 0x1.1e0e75eb44027p+0, 0x1.1ed5022fcd91dp+0, 0x1.1f9c18438ce4dp+0,
+    0x1.2063b88628cd6p+0, 0x1.212be3578a819p+0, 0x1.21f49917ddc96p+0, 0x1.22bdda27912d1p+0,
+    0x1.2387a6e756238p+0, 0x1.2451ffb82140ap+0, 0x1.251ce4fb2a63fp+0, 0x1.25e85711ece75p+0,
+    0x1.26b4565e27cddp+0, 0x1.2780e341ddf29p+0, 0x1.284dfe1f56381p+0, 0x1.291ba7591bb70p+0,
+    0x1.29e9df51fdee1p+0, 0x1.2ab8a66d10f13p+0, 0x1.2b87fd0dad990p+0, 0x1.2c57e39771b2fp+0,
+    0x1.2d285a6e4030bp+0, 0x1.2df961f641589p+0, 0x1.2ecafa93e2f56p+0, 0x1.2f9d24abd886bp+0,
+    0x1.306fe0a31b715p+0, 0x1.31432edeeb2fdp+0, 0x1.32170fc4cd831p+0, 0x1.32eb83ba8ea32p+0,
+    0x1.33c08b26416ffp+0, 0x1.3496266e3fa2dp+0, 0x1.356c55f929ff1p+0, 0x1.36431a2de883bp+0,
+    0x1.371a7373aa9cbp+0, 0x1.37f26231e754ap+0, 0x1.38cae6d05d866p+0, 0x1.39a401b7140efp+0,
+    0x1.3a7db34e59ff7p+0, 0x1.3b57fbfec6cf4p+0, 0x1.3c32dc313a8e5p+0, 0x1.3d0e544ede173p+0,
+    0x1.3dea64c123422p+0, 0x1.3ec70df1c5175p+0, 0x1.3fa4504ac801cp+0, 0x1.40822c367a024p+0,
+    0x1.4160a21f72e2ap+0, 0x1.423fb2709468ap+0, 0x1.431f5d950a897p+0, 0x1.43ffa3f84b9d4p+0,
+    0x1.44e086061892dp+0, 0x1.45c2042a7d232p+0, 0x1.46a41ed1d0057p+0, 0x1.4786d668b3237p+0,
+    0x1.486a2b5c13cd0p+0, 0x1.494e1e192aed2p+0, 0x1.4a32af0d7d3dep+0, 0x1.4b17dea6db7d7p+0,
+    0x1.4bfdad5362a27p+0, 0x1.4ce41b817c114p+0, 0x1.4dcb299fddd0dp+0, 0x1.4eb2d81d8abffp+0,
+    0x1.4f9b2769d2ca7p+0, 0x1.508417f4531eep+0, 0x1.516daa2cf6642p+0, 0x1.5257de83f4eefp+0,
+    0x1.5342b569d4f82p+0, 0x1.542e2f4f6ad27p+0, 0x1.551a4ca5d920fp+0, 0x1.56070dde910d2p+0,
+    0x1.56f4736b527dap+0, 0x1.57e27dbe2c4cfp+0, 0x1.58d12d497c7fdp+0, 0x1.59c0827ff07ccp+0,
+    0x1.5ab07dd485429p+0, 0x1.5ba11fba87a03p+0, 0x1.5c9268a5946b7p+0, 0x1.5d84590998b93p+0,
+    0x1.5e76f15ad2148p+0, 0x1.5f6a320dceb71p+0, 0x1.605e1b976dc09p+0, 0x1.6152ae6cdf6f4p+0,
+    0x1.6247eb03a5585p+0, 0x1.633dd1d1929fdp+0, 0x1.6434634ccc320p+0, 0x1.652b9febc8fb7p+0,
+    0x1.6623882552225p+0, 0x1.671c1c70833f6p+0, 0x1.68155d44ca973p+0, 0x1.690f4b19e9538p+0,
+    0x1.6a09e667f3bcdp+0, 0x1.6b052fa75173ep+0, 0x1.6c012750bdabfp+0, 0x1.6cfdcddd47645p+0,
+    0x1.6dfb23c651a2fp+0, 0x1.6ef9298593ae5p+0, 0x1.6ff7df9519484p+0, 0x1.70f7466f42e87p+0,
+    0x1.71f75e8ec5f74p+0, 0x1.72f8286ead08ap+0, 0x1.73f9a48a58174p+0, 0x1.74fbd35d7cbfdp+0,
+    0x1.75feb564267c9p+0, 0x1.77024b1ab6e09p+0, 0x1.780694fde5d3fp+0, 0x1.790b938ac1cf6p+0,
+    0x1.7a11473eb0187p+0, 0x1.7b17b0976cfdbp+0, 0x1.7c1ed0130c132p+0, 0x1.7d26a62ff86f0p+0,
+    0x1.7e2f336cf4e62p+0, 0x1.7f3878491c491p+0, 0x1.80427543e1a12p+0, 0x1.814d2add106d9p+0,
+    0x1.82589994cce13p+0, 0x1.8364c1eb941f7p+0, 0x1.8471a4623c7adp+0, 0x1.857f4179f5b21p+0,
+    0x1.868d99b4492edp+0, 0x1.879cad931a436p+0, 0x1.88ac7d98a6699p+0, 0x1.89bd0a478580fp+0,
+    0x1.8ace5422aa0dbp+0, 0x1.8be05bad61778p+0, 0x1.8cf3216b5448cp+0, 0x1.8e06a5e0866d9p+0,
+    0x1.8f1ae99157736p+0, 0x1.902fed0282c8ap+0, 0x1.9145b0b91ffc6p+0, 0x1.925c353aa2fe2p+0,
+    0x1.93737b0cdc5e5p+0, 0x1.948b82b5f98e5p+0, 0x1.95a44cbc8520fp+0, 0x1.96bdd9a7670b3p+0,
+    0x1.97d829fde4e50p+0, 0x1.98f33e47a22a2p+0, 0x1.9a0f170ca07bap+0, 0x1.9b2bb4d53fe0dp+0,
+    0x1.9c49182a3f090p+0, 0x1.9d674194bb8d5p+0, 0x1.9e86319e32323p+0, 0x1.9fa5e8d07f29ep+0,
+    0x1.a0c667b5de565p+0, 0x1.a1e7aed8eb8bbp+0, 0x1.a309bec4a2d33p+0, 0x1.a42c980460ad8p+0,
+    0x1.a5503b23e255dp+0, 0x1.a674a8af46052p+0, 0x1.a799e1330b358p+0, 0x1.a8bfe53c12e59p+0,
+    0x1.a9e6b5579fdbfp+0, 0x1.ab0e521356ebap+0, 0x1.ac36bbfd3f37ap+0, 0x1.ad5ff3a3c2774p+0,
+    0x1.ae89f995ad3adp+0, 0x1.afb4ce622f2ffp+0, 0x1.b0e07298db666p+0, 0x1.b20ce6c9a8952p+0,
+    0x1.b33a2b84f15fbp+0, 0x1.b468415b749b1p+0, 0x1.b59728de5593ap+0, 0x1.b6c6e29f1c52ap+0,
+    0x1.b7f76f2fb5e47p+0, 0x1.b928cf22749e4p+0, 0x1.ba5b030a1064ap+0, 0x1.bb8e0b79a6f1fp+0,
+    0x1.bcc1e904bc1d2p+0, 0x1.bdf69c3f3a207p+0, 0x1.bf2c25bd71e09p+0, 0x1.c06286141b33dp+0,
+    0x1.c199bdd85529cp+0, 0x1.c2d1cd9fa652cp+0, 0x1.c40ab5fffd07ap+0, 0x1.c544778fafb22p+0,
+    0x1.c67f12e57d14bp+0, 0x1.c7ba88988c933p+0, 0x1.c8f6d9406e7b5p+0, 0x1.ca3405751c4dbp+0,
+    0x1.cb720dcef9069p+0, 0x1.ccb0f2e6d1675p+0, 0x1.cdf0b555dc3fap+0, 0x1.cf3155b5bab74p+0,
+    0x1.d072d4a07897cp+0, 0x1.d1b532b08c968p+0, 0x1.d2f87080d89f2p+0, 0x1.d43c8eacaa1d6p+0,
+    0x1.d5818dcfba487p+0, 0x1.d6c76e862e6d3p+0, 0x1.d80e316c98398p+0, 0x1.d955d71ff6075p+0,
+    0x1.da9e603db3285p+0, 0x1.dbe7cd63a8315p+0, 0x1.dd321f301b460p+0, 0x1.de7d5641c0658p+0,
+    0x1.dfc97337b9b5fp+0, 0x1.e11676b197d17p+0, 0x1.e264614f5a129p+0, 0x1.e3b333b16ee12p+0,
+    0x1.e502ee78b3ff6p+0, 0x1.e653924676d76p+0, 0x1.e7a51fbc74c83p+0, 0x1.e8f7977cdb740p+0,
+    0x1.ea4afa2a490dap+0, 0x1.eb9f4867cca6ep+0, 0x1.ecf482d8e67f1p+0, 0x1.ee4aaa2188510p+0,
+    0x1.efa1bee615a27p+0, 0x1.f0f9c1cb6412ap+0, 0x1.f252b376bba97p+0, 0x1.f3ac948dd7274p+0,
+    0x1.f50765b6e4540p+0, 0x1.f6632798844f8p+0, 0x1.f7bfdad9cbe14p+0, 0x1.f91d802243c89p+0,
+    0x1.fa7c1819e90d8p+0, 0x1.fbdba3692d514p+0, 0x1.fd3c22b8f71f1p+0, 0x1.fe9d96b2a23d9p+0,
+};
+
+// The polynomial steps are written as three-address v_fma_f64 with the
+// wave-uniform constant in scalar registers: the compiler's two-address
+// v_fmac form would copy a constant register before every use.
+__device__ __forceinline__ double fma_vvs(double a, double b, double c) {  // a * b + c, c uniform
+    double d;
+    asm("v_fma_f64 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "s"(c));
+    return d;
+}
+__device__ __forceinline__ double fma_vsv(double a, double b, double c) {  // a * b + c, b uniform
+    double d;
+    asm("v_fma_f64 %0, %1, %2, %3" : "=v"(d) : "v"(a), "s"(b), "v"(c));
+    return d;
+}
+__device__ __forceinline__ double fnma_vsv(double a, double b, double c) {  // c - a * b, b uniform
+    double d;
+    asm("v_fma_f64 %0, -%1, %2, %3" : "=v"(d) : "v"(a), "s"(b), "v"(c));
+    return d;
+}
+
+constexpr double kExpRound = 0x1.8p52;                   // adding it rounds to an integer, kept in the low word
+constexpr double kExpInvL = 0x1.71547652b82fep+8;        // 256 / ln 2
+constexpr double kExpL1 = 0x1.62e42fee00000p-9;          // ln2 / 256, high part (n * kExpL1 is exact)
+constexpr double kExpL2 = 0x1.a39ef35793c76p-41;         // ln2 / 256 - kExpL1
+constexpr double kExpFloor = -746.0;                     // exp(-746) rounds to 0
+
+// exp(x) for x <= 700 (and x = -inf); `tab` is kExp2Frac in LDS.
+__device__ __forceinline__ double exp_table(double x, const double *tab) {
+    x = fmax(x, kExpFloor);
+    const double y = fma_vsv(x, kExpInvL, kExpRound);
+    const int n = __double2loint(y);                     // round(x * 256 / ln2)
+    const double nd = y - kExpRound;
+    const double r = fnma_vsv(nd, kExpL2, fnma_vsv(nd, kExpL1, x));
+    double p = fma_vsv(r, 1.0 / 24.0, 1.0 / 6.0);
+    p = fma_vvs(p, r, 0.5);
+    p = fma_vvs(p, r, 1.0);
+    const double q = p * r;                              // e^r - 1
+    const double t = tab[n & (kTab - 1)];
+    return ldexp(fma(t, q, t), n >> kTabBits);
+}
+
+// ------------------------------------------------------------ log-sum-exp
+constexpr double kLseSlack = 64.0;     // largest exponent a sum may take
+constexpr double kLseEmpty = -1e300;   // shift of a lane that has seen no finite value
+
+// Values of one 16-byte vector of a row; those at or past K read as -inf,
+// which the log-sum-exp ignores exactly.
+template <class E>
+__device__ inline void load_values(rsrc_t r, int64_t i0, int64_t K, float (&v)[E::kPer]) {
+    const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy);
+    E::values(t, v);
+    if (i0 + E::kPer > K) {
+#pragma unroll
+        for (int j = 0; j < E::kPer; ++j)
+            if (i0 + j >= K) v[j] = -INFINITY;
+    }
+}
+
+// Values and keys of one vector and how many lie below K (values past K read
+// as -inf; key users test the count).
 template <class E>
 __device__ inline int load_vec(rsrc_t r, int64_t i0, int64_t K, float (&v)[E::kPer], uint32_t (&key)[E::kPer]) {
     const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy);
     E::unpack(t, v, key);
     const int64_t left = K - i0;
-    return left >= E::kPer ? E::kPer : static_cast<int>(left);
+    const int n = left >= E::kPer ? E::kPer : static_cast<int>(left);
+    if (n < E::kPer) {
+#pragma unroll
+        for (int j = 0; j < E::kPer; ++j)
+            if (j >= n) v[j] = -INFINITY;
+    }
+    return n;
 }
 
-// Online (max, scaled sum) over the valid values of one vector.
+// Adds one vector to a lane's (shift m, sum s = sum exp(x - m)).  The terms
+// are summed pairwise before they join the running sum.
 template <int N>
-__device__ inline void lse_add(double &m, double &s, const float (&v)[N], int n) {
-    float vm = -INFINITY;
+__device__ inline void lse_add(double &m, double &s, const float (&v)[N], const double *tab) {
+    float vm = v[0];
 #pragma unroll
-    for (int j = 0; j < N; ++j)
-        if (j < n) vm = fmaxf(vm, v[j]);
-    if (vm == -INFINITY) return;
+    for (int j = 1; j < N; ++j) vm = fmaxf(vm, v[j]);
     const double dm = vm;
-    if (dm > m) {
-        s = m == -INFINITY ? 0.0 : s * exp(m - dm);
+    if (dm > m + kLseSlack) {
+        s *= exp(m - dm);
         m = dm;
     }
+    double e[N];
 #pragma unroll
-    for (int j = 0; j < N; ++j)
-        if (j < n) s += exp(static_cast<double>(v[j]) - m);
+    for (int j = 0; j < N; ++j) e[j] = exp_table(static_cast<double>(v[j]) - m, tab);
+#pragma unroll
+    for (int w = 1; w < N; w *= 2)
+#pragma unroll
+        for (int j = 0; j + w < N; j += 2 * w) e[j] += e[j + w];
+    s += e[0];
 }
 
+// lse of one worker row (token blockIdx.x, worker blockIdx.y) into
+// d_out[w][u].
+template <class E>
+__global__ __launch_bounds__(kBlock) void js_lse_kernel(JsParams a) {
+    constexpr int P = E::kPer;
+    constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;
+    __shared__ double tab[kTab];
+    __shared__ double red[2 * kWavesPerBlock];
+    const int tid = threadIdx.x;
+    if (tid < kTab) tab[tid] = kExp2Frac[tid];
+    __syncthreads();
+    const int64_t row = static_cast<int64_t>(blockIdx.y) * a.U + blockIdx.x;
+    const rsrc_t r = js_row(a.workers, row, a.ldk, E::kElem);
+    double m = kLseEmpty, s = 0.0;
+    for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
+        float v[P];
+        load_values<E>(r, i0, a.K, v);
+        lse_add<P>(m, s, v, tab);
+    }
+    const double lse = block_lse(m, s, red);
+    if (tid == 0) a.d_out[row] = lse;
+}
+
+// One token's term of the JS sum from the two log-probabilities; a side of
+// probability 0 adds nothing (0 log 0 = 0).
+__device__ inline double js_term(double lp, double lq) {
+    constexpr double kLog2 = 0.69314718055994530942;
+    const double hi = lp > lq ? lp : lq, lo = lp > lq ? lq : lp;
+    if (hi == -INFINITY) return 0.0;  // probability 0 on both sides
+    const double lmix = hi + log1p(exp(lo - hi)) - kLog2;
+    double t = 0.0;
+    if (lp != -INFINITY) t += 0.5 * exp(lp) * (lp - lmix);
+    if (lq != -INFINITY) t += 0.5 * exp(lq) * (lq - lmix);
+    return t;
+}
+
+// Block-wide sums of N values per thread in a fixed order: thread j < N
+// returns the sum of everyone's x[j]; the others return 0.
+template <int N>
+__device__ inline double block_sum_n(double (&x)[N], double *red) {
+    for (int o = kWave / 2; o > 0; o >>= 1)
+#pragma unroll
+        for (int j = 0; j < N; ++j) x[j] += shfl_xor_d(x[j], o);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    __syncthreads();
+    if (lane == 0)
+#pragma unroll
+        for (int j = 0; j < N; ++j) red[wave * N + j] = x[j];
+    __syncthreads();
+    double t = 0.0;
+    if (threadIdx.x < N) {
+        t = red[threadIdx.x];
+        for (int w = 1; w < kWavesPerBlock; ++w) t += red[w * N + threadIdx.x];
+    }
+    return t;
+}
+
+constexpr int kJsGroup = 8;  // workers whose logits are gathered together
+
+// One token per block: the averaged row's log-sum-exp and top-k set, then
+// JS_m for every worker from the lse_m that js_lse_kernel left in d_out.
+//
+// Selection.  Fast path (k <= kBlock): the k-th largest of the threads'
+// largest keys, T0, is at most the k-th largest key of the row, so the
+// selected tokens are among the candidates with key >= T0 (on these inputs
+// a few hundred); they are collected in LDS and each takes its exact rank
+// under (key descending, index ascending).  Otherwise (k > kBlock, or more
+// candidates than fit): a radix select, 8 key bits per pass from the top,
+// then a collection pass that splits the tie at the threshold in index
+// order.
 template <class E>
 __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
     constexpr int P = E::kPer;
     constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;  // elements per block sweep
+    constexpr int kCand = kJsMaxTopK;                              // candidate capacity
     __shared__ uint32_t hist[256];
-    __shared__ int32_t sel_idx[kJsMaxTopK], sorted_idx[kJsMaxTopK];
+    __shared__ int32_t sel_idx[kJsMaxTopK];
     __shared__ float sel_val[kJsMaxTopK];
-    __shared__ double la[kJsMaxTopK];
+    __shared__ union {
+        struct {
+            int32_t idx[kCand];
+            uint32_t key[kCand];
+            float val[kCand];
+        } cand;  // fast selection
+        struct {
+            int32_t idx[kJsMaxTopK];
+            double la[kJsMaxTopK];
+        } out;   // the selected tokens in index order, log pbar
+    } sm;
     __shared__ double red[2 * kWavesPerBlock];
-    __shared__ uint32_t s_prefix;
+    __shared__ double red_n[kJsGroup * kWavesPerBlock];
+    __shared__ uint32_t s_tkey[kBlock];
+    __shared__ uint32_t s_prefix, s_thr;
     __shared__ int s_need, s_count_eq, s_nsel;
     __shared__ int s_scan[kBlock];
+    __shared__ double tab[kTab];
 
     const int tid = threadIdx.x;
     const int64_t u = blockIdx.x;
     const int k = a.k;
     const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
-
-    // Pass 1 over the averaged row: log-sum-exp and the histogram of the top
-    // key byte.
-    if (tid < 256) hist[tid] = 0;
+    if (tid < kTab) tab[tid] = kExp2Frac[tid];
     __syncthreads();
-    double m = -INFINITY, s = 0.0;
+
+    // Pass 1 over the averaged row: log-sum-exp and this thread's largest key
+    // (key 0 lies below the key of every value).
+    double m = kLseEmpty, s = 0.0;
+    uint32_t kmax = 0;
     for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
         float v[P];
         uint32_t key[P];
         const int n = load_vec<E>(ra, i0, a.K, v, key);
-        lse_add<P>(m, s, v, n);
+        lse_add<P>(m, s, v, tab);
 #pragma unroll
-        for (int j = 0; j < P; ++j)
-            if (j < n) atomicAdd(&hist[key[j] >> (E::kKeyBits - 8)], 1u);
+        for (int j = 0; j < P; ++j) kmax = max(kmax, j < n ? key[j] : 0u);
     }
     const double lse_a = block_lse(m, s, red);
 
-    // Radix select of the k-th largest key, 8 bits per pass from the top.
-    uint32_t prefix = 0;
-    int need = k;
-    for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
-        const int shift = E::kKeyBits - 8 * (pass + 1);
-        if (pass > 0) {
-            if (tid < 256) hist[tid] = 0;
+    bool fast = k <= kBlock;
+    if (fast) {
+        // T0: the thread maxima ranked with ties by thread index form a
+        // permutation, so exactly one thread holds rank k - 1.
+        s_tkey[tid] = kmax;
+        if (tid == 0) s_nsel = 0;
+        __syncthreads();
+        int r = 0;
+        for (int j = 0; j < kBlock; ++j) {
+            const uint32_t o = s_tkey[j];
+            r += (o > kmax || (o == kmax && j < tid)) ? 1 : 0;
+        }
+        if (r == k - 1) s_thr = kmax;
+        __syncthreads();
+        const uint32_t T0 = s_thr;
+        for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
+            float v[P];
+            uint32_t key[P];
+            const int n = load_vec<E>(ra, i0, a.K, v, key);
+#pragma unroll
+            for (int j = 0; j < P; ++j) {
+                if (j < n && key[j] >= T0) {
+                    const int slot = atomicAdd(&s_nsel, 1);
+                    if (slot < kCand) {
+                        sm.cand.idx[slot] = static_cast<int32_t>(i0 + j);
+                        sm.cand.key[slot] = key[j];
+                        sm.cand.val[slot] = v[j];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        const int C = s_nsel;
+        fast = C <= kCand;  // the same in every thread
+        if (fast) {
+            for (int c = tid; c < C; c += kBlock) {
+                const uint32_t kc = sm.cand.key[c];
+                const int32_t ic = sm.cand.idx[c];
+                int rank = 0;
+                for (int j = 0; j < C; ++j) {
+                    const uint32_t kj = sm.cand.key[j];
+                    rank += (kj > kc || (kj == kc && sm.cand.idx[j] < ic)) ? 1 : 0;
+                }
+                if (rank < k) {
+                    sel_idx[rank] = ic;
+                    sel_val[rank] = sm.cand.val[c];
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    if (!fast) {
+        // Radix select of the k-th largest key, 8 bits per pass from the top.
+        uint32_t prefix = 0;
+        int need = k;
+        for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
+            const int shift = E::kKeyBits - 8 * (pass + 1);
+            hist[tid] = 0;
             __syncthreads();
             for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
                 float v[P];
                 uint32_t key[P];
                 const int n = load_vec<E>(ra, i0, a.K, v, key);
+                if (pass == 0) {
 #pragma unroll
-                for (int j = 0; j < P; ++j)
-                    if (j < n && (key[j] >> (shift + 8)) == prefix) atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
-            }
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int above = 0, bin = 255;
-            for (; bin > 0; --bin) {
-                if (above + static_cast<int>(hist[bin]) >= need) break;
-                above += hist[bin];
-            }
-            s_prefix = (prefix << 8) | static_cast<uint32_t>(bin);
-            s_need = need - above;
-            s_count_eq = hist[bin];
-        }
-        __syncthreads();
-        prefix = s_prefix;
-        need = s_need;
-    }
-    const uint32_t T = prefix;
-    const int need_eq = need;
-    const bool take_all_eq = s_count_eq == need_eq;
-
-    // Collect the keys above T (and those equal to T when all of them are
-    // taken); the list order does not matter, it is sorted below.
-    if (tid == 0) s_nsel = 0;
-    __syncthreads();
-    for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
-        float v[P];
-        uint32_t key[P];
-        const int n = load_vec<E>(ra, i0, a.K, v, key);
+                    for (int j = 0; j < P; ++j)
+                        if (j < n) atomicAdd(&hist[key[j] >> shift], 1u);
+                } else {
 #pragma unroll
-        for (int j = 0; j < P; ++j) {
-            if (j < n && (key[j] > T || (take_all_eq && key[j] == T))) {
-                const int slot = atomicAdd(&s_nsel, 1);
-                sel_idx[slot] = static_cast<int32_t>(i0 + j);
-                sel_val[slot] = v[j];
+                    for (int j = 0; j < P; ++j)
+                        if (j < n && (key[j] >> (shift + 8)) == prefix) atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
+                }
             }
-        }
-    }
-    __syncthreads();
-    if (!take_all_eq) {
-        // Ties straddle the threshold: take the equal keys in index order,
-        // one block sweep at a time, until need_eq are taken.
-        int remaining = need_eq;
-        for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
-            const int64_t i0 = base + static_cast<int64_t>(tid) * P;
-            float v[P];
-            uint32_t key[P];
-            int n = 0, cnt = 0;
-            if (i0 < a.K) {
-                n = load_vec<E>(ra, i0, a.K, v, key);
-#pragma unroll
-                for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
-            }
-            s_scan[tid] = cnt;
             __syncthreads();
             if (tid == 0) {
-                int run = 0;
-                for (int t = 0; t < kBlock; ++t) {
-                    const int c = s_scan[t];
-                    s_scan[t] = run;
-                    run += c;
+                int above = 0, bin = 255;
+                for (; bin > 0; --bin) {
+                    if (above + static_cast<int>(hist[bin]) >= need) break;
+                    above += hist[bin];
                 }
+                s_prefix = (prefix << 8) | static_cast<uint32_t>(bin);
+                s_need = need - above;
+                s_count_eq = hist[bin];
             }
             __syncthreads();
-            int rank = s_scan[tid];
-            if (i0 < a.K) {
+            prefix = s_prefix;
+            need = s_need;
+        }
+        const uint32_t T = prefix;
+        const int need_eq = need;
+        const bool take_all_eq = s_count_eq == need_eq;
+
+        // Collect the keys above T (and those equal to T when all of them are
+        // taken); the list order does not matter, it is sorted below.
+        if (tid == 0) s_nsel = 0;
+        __syncthreads();
+        for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
+            float v[P];
+            uint32_t key[P];
+            const int n = load_vec<E>(ra, i0, a.K, v, key);
 #pragma unroll
-                for (int j = 0; j < P; ++j) {
-                    if (j < n && key[j] == T) {
-                        if (rank < remaining) {
-                            const int slot = atomicAdd(&s_nsel, 1);
-                            sel_idx[slot] = static_cast<int32_t>(i0 + j);
-                            sel_val[slot] = v[j];
-                        }
-                        ++rank;
+            for (int j = 0; j < P; ++j) {
+                if (j < n && (key[j] > T || (take_all_eq && key[j] == T))) {
+                    const int slot = atomicAdd(&s_nsel, 1);
+                    sel_idx[slot] = static_cast<int32_t>(i0 + j);
+                    sel_val[slot] = v[j];
+                }
+            }
+        }
+        __syncthreads();
+        if (!take_all_eq) {
+            // Ties straddle the threshold: take the equal keys in index order,
+            // one block sweep at a time, until need_eq are taken.
+            int remaining = need_eq;
+            for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
+                const int64_t i0 = base + static_cast<int64_t>(tid) * P;
+                float v[P];
+                uint32_t key[P];
+                int n = 0, cnt = 0;
+                if (i0 < a.K) {
+                    n = load_vec<E>(ra, i0, a.K, v, key);
+#pragma unroll
+                    for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
+                }
+                s_scan[tid] = cnt;
+                __syncthreads();
+                if (tid == 0) {
+                    int run = 0;
+                    for (int t = 0; t < kBlock; ++t) {
+                        const int c = s_scan[t];
+                        s_scan[t] = run;
+                        run += c;
                     }
                 }
+                __syncthreads();
+                int rank = s_scan[tid];
+                if (i0 < a.K) {
+#pragma unroll
+                    for (int j = 0; j < P; ++j) {
+                        if (j < n && key[j] == T) {
+                            if (rank < remaining) {
+                                const int slot = atomicAdd(&s_nsel, 1);
+                                sel_idx[slot] = static_cast<int32_t>(i0 + j);
+                                sel_val[slot] = v[j];
+                            }
+                            ++rank;
+                        }
+                    }
+                }
+                __syncthreads();
+                const int taken_total = s_nsel;
+                remaining = k - taken_total;
+                __syncthreads();
             }
-            __syncthreads();
-            const int taken_total = s_nsel;
-            remaining = k - taken_total;
-            __syncthreads();
         }
     }
 
@@ -289,37 +591,40 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
         const int32_t my = sel_idx[t];
         int r = 0;
         for (int j = 0; j < k; ++j) r += sel_idx[j] < my ? 1 : 0;
-        sorted_idx[r] = my;
-        la[r] = static_cast<double>(sel_val[t]) - lse_a;
+        sm.out.idx[r] = my;
+        sm.out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
     }
     __syncthreads();
     if (a.topk_out)
-        for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = sorted_idx[t];
+        for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = sm.out.idx[t];
 
+    // JS terms, kJsGroup workers at a time so that their gathers overlap.
     constexpr double kLog2 = 0.69314718055994530942;
-    for (int w = 0; w < a.M; ++w) {
-        const rsrc_t rw = js_row(a.workers, static_cast<int64_t>(w) * a.U + u, a.ldk, E::kElem);
-        double mw = -INFINITY, sw = 0.0;
-        for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
-            float v[P];
-            uint32_t key[P];
-            const int n = load_vec<E>(rw, i0, a.K, v, key);
-            lse_add<P>(mw, sw, v, n);
+    for (int w0 = 0; w0 < a.M; w0 += kJsGroup) {
+        const int nw = a.M - w0 < kJsGroup ? a.M - w0 : kJsGroup;
+        rsrc_t rw[kJsGroup];
+        double lse_w[kJsGroup], part[kJsGroup];
+#pragma unroll
+        for (int j = 0; j < kJsGroup; ++j) {
+            // lse_m, parked in d_out by js_lse_kernel; read before the
+            // barriers of block_sum_n, overwritten with d_m(u) after them.
+            const int64_t row = static_cast<int64_t>(w0 + (j < nw ? j : 0)) * a.U + u;
+            rw[j] = js_row(a.workers, row, a.ldk, E::kElem);
+            lse_w[j] = a.d_out[row];
+            part[j] = 0.0;
         }
-        const double lse_w = block_lse(mw, sw, red);
-        double part = 0.0;
         for (int t = tid; t < k; t += kBlock) {
-            const double lp = static_cast<double>(E::at(rw, sorted_idx[t])) - lse_w;
-            const double lq = la[t];
-            const double hi = lp > lq ? lp : lq, lo = lp > lq ? lq : lp;
-            if (hi == -INFINITY) continue;  // probability 0 on both sides
-            const double lmix = hi + log1p(exp(lo - hi)) - kLog2;
-            // A side of probability 0 adds nothing (0 log 0 = 0).
-            if (lp != -INFINITY) part += 0.5 * exp(lp) * (lp - lmix);
-            if (lq != -INFINITY) part += 0.5 * exp(lq) * (lq - lmix);
+            const int32_t idx = sm.out.idx[t];
+            const double lq = sm.out.la[t];
+            float z[kJsGroup];
+#pragma unroll
+            for (int j = 0; j < kJsGroup; ++j) z[j] = E::at(rw[j], idx);
+#pragma unroll
+            for (int j = 0; j < kJsGroup; ++j)
+                if (j < nw) part[j] += js_term(static_cast<double>(z[j]) - lse_w[j], lq);
         }
-        const double js = block_sum(part, red);
-        if (tid == 0) a.d_out[static_cast<int64_t>(w) * a.U + u] = sqrt((js > 0.0 ? js : 0.0) / kLog2);
+        const double js = block_sum_n<kJsGroup>(part, red_n);
+        if (tid < nw) a.d_out[static_cast<int64_t>(w0 + tid) * a.U + u] = sqrt((js > 0.0 ? js : 0.0) / kLog2);
     }
 }
 
@@ -341,8 +646,14 @@ __global__ __launch_bounds__(256) void js_mean_kernel(const double *d, int64_t U
 bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
                int32_t k, double *d_out, double *mean_out, int32_t *topk_out, hipStream_t stream) {
     JsParams p{avg, workers, d_out, topk_out, U, K, ldk, M, k};
-    if (bf16) hipLaunchKernelGGL(js_kernel<JsBF16>, dim3(static_cast<unsigned>(U)), dim3(kBlock), 0, stream, p);
-    else hipLaunchKernelGGL(js_kernel<JsF32>, dim3(static_cast<unsigned>(U)), dim3(kBlock), 0, stream, p);
+    const dim3 rows(static_cast<unsigned>(U), static_cast<unsigned>(M));
+    if (bf16) {
+        hipLaunchKernelGGL(js_lse_kernel<JsBF16>, rows, dim3(kBlock), 0, stream, p);
+        hipLaunchKernelGGL(js_kernel<JsBF16>, dim3(static_cast<unsigned>(U)), dim3(kBlock), 0, stream, p);
+    } else {
+        hipLaunchKernelGGL(js_lse_kernel<JsF32>, rows, dim3(kBlock), 0, stream, p);
+        hipLaunchKernelGGL(js_kernel<JsF32>, dim3(static_cast<unsigned>(U)), dim3(kBlock), 0, stream, p);
+    }
     if (hipGetLastError() != hipSuccess) return false;
     if (mean_out) {
         hipLaunchKernelGGL(js_mean_kernel, dim3(M), dim3(256), 0, stream, d_out, U, mean_out);

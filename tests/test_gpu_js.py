@@ -157,3 +157,24 @@ def test_js_full_size_sampled_tokens(env):
     np.testing.assert_allclose(mean.cpu().numpy(), dh.mean(axis=1), rtol=1e-13)
     assert np.all((dh > 0) & (dh < 1))
     print(f"[js] full size: CD_JS = {dh.mean():.6f}", flush=True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_wide_logit_range(env, dtype):
+    """Logits spread over hundreds of units: later values exceed a lane's
+    running shift by more than the exponent slack (the rescale path), and
+    most terms fall into the underflow range of exp."""
+    fgd, torch = env
+    M, U, K, k = 3, 4, 20000, 100
+    A, W = slog.numpy_logits(M, U, K, K, "f32", seed=23, scale=60.0, head_boost=200.0)
+    ramp = np.linspace(-900.0, 900.0, K, dtype=np.float32)
+    A[1] += ramp                          # rising: the shift moves at almost every vector
+    W[:, 1] += ramp
+    A[2] -= ramp                          # falling: the first vector holds the maximum
+    W[:, 2] -= ramp
+    if dtype == "bf16":
+        import torch as _t
+
+        A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+        W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    _check(fgd, torch, A, W, dtype, K, k)
