@@ -42,6 +42,10 @@
  *  - `stream` is a hipStream_t (NULL = the device's null stream).  Compute
  *    calls are asynchronous with respect to the host.
  *  - An engine is not thread-safe; use one engine per host thread.
+ *  - Engine calls run on the engine's device (fgd_config.device): they make
+ *    it current for their duration and restore the caller's current device
+ *    before returning.  The engine-free calls (fgd_js_distance,
+ *    fgd_stream_copy) run on the caller's current device.
  */
 #ifndef FGD_H
 #define FGD_H

@@ -327,12 +327,22 @@ class Engine:
             raise ValueError(f"{name}: expected shape [{self.M}, >= {self.P}], got {tuple(t.shape)}")
         if t.stride(1) != 1 or (self.M > 1 and t.stride(0) != self.ld):
             raise ValueError(f"{name}: rows must be contiguous with row stride ld = {self.ld}")
+        if not t.is_cuda or t.device.index != self.device:
+            raise ValueError(f"{name}: expected a tensor on cuda:{self.device}, got {t.device}")
+
+    def _stream(self, stream):
+        """The given stream, or torch's current stream on the engine's device."""
+        if stream is not None:
+            return stream
+        import torch
+
+        return torch.cuda.current_stream(self.device)
 
     def outer_step(self, theta_prev, theta_local, momentum, cd_out=None, stream=None):
         self._check_rows(theta_prev, "theta_prev", self.dtype)
         self._check_rows(theta_local, "theta_local", self.dtype)
         self._check_rows(momentum, "momentum", "f32")
-        fgd_outer_step(self.handle, theta_prev, theta_local, momentum, cd_out, stream)
+        fgd_outer_step(self.handle, theta_prev, theta_local, momentum, cd_out, self._stream(stream))
 
     def mix1(self, theta_prev, x_out, momentum=None, cd_out=None, stream=None, num_blocks=0):
         """Mix1 half of split execution: x_out = Mix1(theta_prev) (and the
@@ -341,7 +351,7 @@ class Engine:
         self._check_rows(x_out, "x_out", self.dtype)
         if momentum is not None:
             self._check_rows(momentum, "momentum", "f32")
-        fgd_mix1(self.handle, theta_prev, x_out, momentum, cd_out, num_blocks, stream)
+        fgd_mix1(self.handle, theta_prev, x_out, momentum, cd_out, num_blocks, self._stream(stream))
 
     def outer_step_blocking(self, x, theta_prev, theta_local, momentum, cd_out=None, write_local=False, stream=None):
         """Blocking half of split execution, from the stored Mix1 output x."""
@@ -349,7 +359,8 @@ class Engine:
         self._check_rows(theta_prev, "theta_prev", self.dtype)
         self._check_rows(theta_local, "theta_local", self.dtype)
         self._check_rows(momentum, "momentum", "f32")
-        fgd_outer_step_blocking(self.handle, x, theta_prev, theta_local, momentum, cd_out, write_local, stream)
+        fgd_outer_step_blocking(self.handle, x, theta_prev, theta_local, momentum, cd_out, write_local,
+                                self._stream(stream))
 
     def num_cd_rows_split(self):
         return fgd_num_cd_rows_split(self.handle)
@@ -360,7 +371,7 @@ class Engine:
     def consensus_distance(self, x, out, stream=None, dtype=None):
         dtype = dtype or self.dtype
         self._check_rows(x, "x", dtype)
-        fgd_consensus_distance(self.handle, x, dtype, out, stream)
+        fgd_consensus_distance(self.handle, x, dtype, out, self._stream(stream))
 
     def effective_weights(self, which, rnd):
         return fgd_get_effective_weights(self.handle, which, rnd, self._nnz[MIXES[which]])

@@ -33,6 +33,29 @@ fgd_status hip_fail(hipError_t e, const char *what) {
     return fail(FGD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Makes a device current for one call and restores the caller's current
+// device on every return path, so no call leaves the thread switched.
+class DeviceGuard {
+  public:
+    DeviceGuard() = default;
+    DeviceGuard(const DeviceGuard &) = delete;
+    DeviceGuard &operator=(const DeviceGuard &) = delete;
+    ~DeviceGuard() {
+        if (switched_) (void)hipSetDevice(prev_);
+    }
+    hipError_t enter(int dev) {
+        hipError_t err = hipGetDevice(&prev_);
+        if (err != hipSuccess || prev_ == dev) return err;
+        err = hipSetDevice(dev);
+        switched_ = err == hipSuccess;
+        return err;
+    }
+
+  private:
+    int prev_ = 0;
+    bool switched_ = false;
+};
+
 fgd_status from_topo(fgd::TopoStatus s, const std::string &err) {
     if (s == fgd::TopoStatus::ok) return FGD_OK;
     g_last_error = err;
@@ -318,10 +341,11 @@ fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
     e->cfg = *cfg;
     e->host_only = cfg->device < 0;
     if (!e->host_only) {
-        hipError_t err = hipSetDevice(cfg->device);
+        DeviceGuard dg;
+        hipError_t err = dg.enter(cfg->device);
         if (err != hipSuccess) {
             delete e;
-            return hip_fail(err, "hipSetDevice");
+            return hip_fail(err, "selecting the engine's device");
         }
         err = hipDeviceGetAttribute(&e->num_cus, hipDeviceAttributeMultiprocessorCount, cfg->device);
         if (err != hipSuccess) {
@@ -361,7 +385,8 @@ fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
 fgd_status fgd_destroy(fgd_engine *e) {
     if (!e) return FGD_OK;
     if (!e->host_only) {
-        (void)hipSetDevice(e->cfg.device);
+        DeviceGuard dg;
+        (void)dg.enter(e->cfg.device);
         (void)hipDeviceSynchronize();
         release(e);
     }
@@ -471,8 +496,9 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     if (!lookup(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, c.mix1_state != 0,
                 !e->subset.empty(), ks))
         return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
-    hipError_t herr = hipSetDevice(c.device);
-    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    DeviceGuard dg;
+    hipError_t herr = dg.enter(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "selecting the engine's device");
 
     int ring = 0;
     if (fgd_status st = ensure_topology(e, stream, ring)) return st;
@@ -579,8 +605,9 @@ fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *m
     fgd::SplitSet ks;
     if (!lookup_split(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, false, c.mix1_state != 0, ks))
         return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
-    hipError_t herr = hipSetDevice(c.device);
-    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    DeviceGuard dg;
+    hipError_t herr = dg.enter(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "selecting the engine's device");
     int ring = 0;
     if (fgd_status st = ensure_topology(e, stream, ring)) return st;
 
@@ -634,8 +661,9 @@ fgd_status fgd_outer_step_blocking(fgd_engine *e, const void *x, void *theta_pre
     fgd::SplitSet ks;
     if (!lookup_split(c.num_workers, c.param_dtype, e->slot[0].kind, e->slot[1].kind, !e->subset.empty(), false, ks))
         return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
-    hipError_t herr = hipSetDevice(c.device);
-    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    DeviceGuard dg;
+    hipError_t herr = dg.enter(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "selecting the engine's device");
     int ring = 0;
     if (fgd_status st = ensure_topology(e, stream, ring)) return st;
 
@@ -679,8 +707,9 @@ fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, d
     if (reinterpret_cast<uintptr_t>(out) & 7u) return fail(FGD_ERR_INVALID_ARG, "out must be 8-byte aligned");
     fgd::KernelSet ks;
     if (!lookup(c.num_workers, dtype, 0, 0, false, false, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", c.num_workers);
-    hipError_t herr = hipSetDevice(c.device);
-    if (herr != hipSuccess) return hip_fail(herr, "hipSetDevice");
+    DeviceGuard dg;
+    hipError_t herr = dg.enter(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "selecting the engine's device");
     hipStream_t stream = static_cast<hipStream_t>(stream_handle);
     fgd::ConsensusParams p{};
     p.x = x;
