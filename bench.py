@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+RESTORE_EVERY = 20      # timed steps between restores of the pristine inputs
 METRIC = "outer-step HBM GB/s and % of MI355X HBM peak; params·workers/sec"
 
 
@@ -345,6 +346,17 @@ def main():
         eng.close()
         return
 
+    # Pristine copies of the arrays the step updates in place (allocated after
+    # the inputs, so they do not change where the inputs live): restored before
+    # the timed steps and between chunks of at most RESTORE_EVERY of them, so a
+    # long run does not carry its inputs toward denormals.  Not timed.
+    pristine = (tp.clone(), v.clone())
+
+    def restore():
+        tp.copy_(pristine[0])
+        v.copy_(pristine[1])
+        torch.cuda.synchronize()
+
     print("[bench] warmup", file=sys.stderr, flush=True)
     for i in range(args.warmup):
         step(i)
@@ -352,16 +364,22 @@ def main():
     eng.enable_timing(True)
     print("[bench] timed steps", file=sys.stderr, flush=True)
     # Events on the launch stream bracket every step (median and min per step).
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        step(args.warmup + i)
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    step_ms, elapsed, done = [], 0.0, 0
+    while done < args.steps:
+        n = min(RESTORE_EVERY, args.steps - done)
+        restore()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        t0 = time.perf_counter()
+        ev[0].record(stream)
+        for i in range(n):
+            step(args.warmup + done + i)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        elapsed += time.perf_counter() - t0
+        step_ms += [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+        done += n
+    step_ms.sort()
+    del pristine
     kernel_ms, n_kernels = eng.read_timing()
     eng.enable_timing(False)
 
