@@ -50,6 +50,10 @@ CASES = [
     (2, 17, "f32", G, 1, ("complete",), 1, None),
     (16, 5, "bf16", G, 1, EXP, 1, 8),                             # P smaller than one vector
     (7, 4099, "bf16", ("ring_self", 0.2), 1, ("er_mh", 0.5, 0.3), 2, 4104),
+    # The largest worker count with the most rounds in both slots: the most LDS rows and consensus rows (19).
+    (64, 600, "f32", REG4, 8, REG4, 8, None),
+    (64, 520, "bf16", ("er_mh", 0.1, 0.2), 8, ("ring_self", 0.3), 8, None),   # padded tables at 8 rounds
+    (48, 777, "f32", ("er_mh", 0.2, 0.1), 8, G, 1, None),
 ]
 
 
