@@ -46,6 +46,9 @@ CASES = [
     (8, 3079, "bf16", ID, 0, G, 1, False, None),                      # DiLoCo
     (5, 2051, "bf16", ("er_mh", 0.6, 0.2), 2, ("ring_self", 0.3), 1, False, [(7, 8), (100, 2000)]),
     (1, 999, "f32", G, 1, ID, 0, True, None),
+    # Most rounds at the largest worker count: the Mix1 half's per-chunk partials hold 9 rows, the blocking half 10.
+    (64, 600, "f32", REG4, 8, REG4, 8, True, [(0, 128), (300, 600)]),
+    (64, 520, "bf16", ("er_mh", 0.1, 0.2), 8, ("ring_self", 0.3), 8, False, None),
 ]
 
 
