@@ -73,6 +73,7 @@ def _load():
         "fgd_get_effective_weights": (I32, [P, I32, I32, P]),
         "fgd_effective_weights": (I32, [I32, P, P, P, P, I32, P]),
         "fgd_min_bytes_per_step": (I32, [P, ctypes.POINTER(I64)]),
+        "fgd_state_layout": (I32, [P, I32, I32, I64, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
         "fgd_enable_timing": (I32, [P, I32]),
         "fgd_read_timing": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
         "fgd_stream_copy": (I32, [P, P, I64, P]),
@@ -228,6 +229,15 @@ def fgd_min_bytes_per_step(h) -> int:
     return b.value
 
 
+def fgd_state_layout(h, spread=True, with_x=False, range_bytes=0):
+    """Returns ((theta_prev, theta_local, x, momentum) byte offsets, total bytes);
+    the x offset is -1 without x."""
+    offs, total = (ctypes.c_int64 * 4)(), ctypes.c_int64()
+    _check(lib.fgd_state_layout(h, 1 if spread else 0, 1 if with_x else 0, int(range_bytes), offs,
+                                ctypes.byref(total)), "fgd_state_layout")
+    return tuple(offs), total.value
+
+
 def fgd_enable_timing(h, enable=True):
     _check(lib.fgd_enable_timing(h, 1 if enable else 0), "fgd_enable_timing")
 
@@ -378,6 +388,27 @@ class Engine:
 
     def min_bytes_per_step(self):
         return fgd_min_bytes_per_step(self.handle)
+
+    def state_layout(self, spread=True, with_x=False, range_bytes=0):
+        return fgd_state_layout(self.handle, spread, with_x, range_bytes)
+
+    def alloc_state(self, spread=True, with_x=False, range_bytes=0):
+        """One device buffer laid out by fgd_state_layout and [M][ld] views of
+        it: dict(pool, theta_prev, theta_local, x (or None), momentum).  The
+        views share the pool's memory; their contents are uninitialised."""
+        import torch
+
+        offs, total = self.state_layout(spread, with_x, range_bytes)
+        pool = torch.empty(total, dtype=torch.uint8, device=f"cuda:{self.device}")
+        pdt = {"f32": torch.float32, "bf16": torch.bfloat16}[self.dtype]
+        es = 4 if self.dtype == "f32" else 2
+
+        def view(off, dt, size):
+            return pool[off:off + self.M * self.ld * size].view(dt).view(self.M, self.ld)
+
+        return {"pool": pool, "theta_prev": view(offs[0], pdt, es), "theta_local": view(offs[1], pdt, es),
+                "x": None if offs[2] < 0 else view(offs[2], pdt, es),
+                "momentum": view(offs[3], torch.float32, 4), "offsets": offs}
 
     def enable_timing(self, on=True):
         fgd_enable_timing(self.handle, on)

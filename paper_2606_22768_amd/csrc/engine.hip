@@ -469,6 +469,48 @@ fgd_status fgd_min_bytes_per_step(const fgd_engine *e, int64_t *bytes) {
     return FGD_OK;
 }
 
+fgd_status fgd_state_layout(const fgd_engine *e, int32_t spread, int32_t with_x, int64_t range_bytes,
+                            int64_t *offsets, int64_t *total_bytes) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (!offsets || !total_bytes) return fail(FGD_ERR_INVALID_ARG, "offsets and total_bytes must not be NULL");
+    if ((spread != 0 && spread != 1) || (with_x != 0 && with_x != 1))
+        return fail(FGD_ERR_INVALID_ARG, "spread and with_x must be 0 or 1");
+    constexpr int64_t kPage = int64_t{2} << 20;
+    if (range_bytes < 0 || range_bytes % kPage != 0)
+        return fail(FGD_ERR_INVALID_ARG, "range_bytes must be a non-negative multiple of 2 MiB");
+    const fgd_config &c = e->cfg;
+    // Every array is [M][ld]; the sizes below cannot overflow for any ld a
+    // device can hold, but a corrupt ld is rejected rather than wrapped.
+    if (c.ld > (int64_t{1} << 56) / c.num_workers) return fail(FGD_ERR_INVALID_ARG, "ld too large");
+    auto up = [](int64_t b) { return (b + kPage - 1) / kPage * kPage; };
+    const int64_t tb = up(c.num_workers * c.ld * elem_size(c.param_dtype));
+    const int64_t vb = c.num_workers * c.ld * 4;
+    int64_t end = 2 * tb;
+    offsets[0] = 0;
+    offsets[1] = tb;
+    offsets[2] = with_x ? end : -1;
+    if (with_x) end += tb;
+    int64_t mom = end;
+    if (spread) {
+        int64_t range = range_bytes;
+        if (range == 0) {
+            if (e->host_only) return fail(FGD_ERR_STATE, "a host-only engine needs an explicit range_bytes");
+            DeviceGuard dg;
+            hipError_t err = dg.enter(c.device);
+            size_t total = 0;
+            if (err == hipSuccess) err = hipDeviceTotalMem(&total, c.device);
+            if (err != hipSuccess) return hip_fail(err, "querying the device memory size");
+            constexpr int64_t kGiB = int64_t{1} << 30;
+            range = (static_cast<int64_t>(total / 3) + kGiB / 2) / kGiB * kGiB;
+        }
+        if (range >= end) mom = range;
+    }
+    offsets[3] = mom;
+    *total_bytes = mom + vb;
+    return FGD_OK;
+}
+
 fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
                           double *cd_out, void *stream_handle) {
     g_last_error.clear();

@@ -60,19 +60,29 @@ def bf16_bits_to_f32(b):
 
 
 def torch_inputs(M, P, ld=None, dtype="f32", prev_std=0.02, drift_std=1e-3, mom_std=1e-4, seed=0,
-                 device="cuda"):
+                 device="cuda", out=None):
     """Returns (theta_prev, theta_local, momentum) torch tensors [M][ld] on device.
 
     Row m is drawn from a generator seeded with seed * 1_000_003 + m so that
-    any row can be regenerated alone.
+    any row can be regenerated alone.  With ``out`` = (theta_prev,
+    theta_local, momentum), [M][ld] tensors of the right dtypes allocated by
+    the caller, those are filled (zeros outside [:, :P]) and returned.
     """
     import torch
 
     ld = P if ld is None else ld
     pdt = torch.float32 if dtype == "f32" else torch.bfloat16
-    tp = torch.zeros((M, ld), dtype=pdt, device=device)
-    tl = torch.zeros((M, ld), dtype=pdt, device=device)
-    v = torch.zeros((M, ld), dtype=torch.float32, device=device)
+    if out is None:
+        tp = torch.zeros((M, ld), dtype=pdt, device=device)
+        tl = torch.zeros((M, ld), dtype=pdt, device=device)
+        v = torch.zeros((M, ld), dtype=torch.float32, device=device)
+    else:
+        tp, tl, v = out
+        for t, dt in ((tp, pdt), (tl, pdt), (v, torch.float32)):
+            if t.shape != (M, ld) or t.dtype != dt:
+                raise ValueError(f"out tensor {tuple(t.shape)} {t.dtype}: expected ({M}, {ld}) {dt}")
+            t.zero_()
+        device = tp.device
     g = torch.Generator(device=device)
     for m in range(M):
         g.manual_seed(seed * 1_000_003 + m)

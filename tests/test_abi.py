@@ -256,6 +256,62 @@ def test_subset_limits():
         eng.close()
 
 
+MiB2, GiB = 2 << 20, 1 << 30
+
+
+@pytest.mark.parametrize("M,P,ld,dtype", [(8, 1_100_000_000, 1_100_000_000, "bf16"), (64, 124_000_000, 124_000_000, "f32"),
+                                          (16, 500_000_000, 500_000_000, "f32"), (4, 1000, 1000, "f32"),
+                                          (3, 8, 8, "bf16")])
+@pytest.mark.parametrize("with_x", [False, True])
+def test_state_layout_arithmetic(M, P, ld, dtype, with_x):
+    """fgd_state_layout: 2 MiB-aligned, non-overlapping [M][ld] arrays in the
+    documented order; spread puts the momentum at range_bytes whenever the
+    parameter arrays end within it, else packed."""
+    es = 2 if dtype == "bf16" else 4
+    eng = fgd.Engine(M, P, ld, dtype, device=-1)
+    try:
+        tb, vb = M * ld * es, M * ld * 4
+        up = lambda b: -(-b // MiB2) * MiB2
+        packed, ptotal = eng.state_layout(spread=False, with_x=with_x)
+        want = [0, up(tb), 2 * up(tb) if with_x else -1, (3 if with_x else 2) * up(tb)]
+        assert list(packed) == want
+        assert ptotal == want[3] + vb
+        for rng in (96 * GiB, 4 * MiB2, 2 * MiB2):
+            offs, total = eng.state_layout(spread=True, with_x=with_x, range_bytes=rng)
+            assert offs[:3] == packed[:3]
+            end = want[3]
+            assert offs[3] == (rng if rng >= end else end)
+            assert total == offs[3] + vb
+            spans = [(o, o + n) for o, n in zip(offs, (tb, tb, tb, vb)) if o >= 0]
+            for o, _ in spans:
+                assert o % MiB2 == 0
+            spans.sort()
+            assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+            assert spans[-1][1] == total
+        # spread = False ignores range_bytes
+        assert eng.state_layout(spread=False, with_x=with_x, range_bytes=96 * GiB) == (packed, ptotal)
+    finally:
+        eng.close()
+
+
+def test_state_layout_rejections():
+    eng = fgd.Engine(8, 1000, 1000, "f32", device=-1)
+    try:
+        offs, total = (ctypes.c_int64 * 4)(), ctypes.c_int64()
+        # a host-only engine cannot derive the range from a device
+        assert fgd.lib.fgd_state_layout(eng.handle, 1, 0, 0, offs, ctypes.byref(total)) == fgd.FGD_ERR_STATE
+        # packed needs no device
+        assert fgd.lib.fgd_state_layout(eng.handle, 0, 0, 0, offs, ctypes.byref(total)) == fgd.FGD_OK
+        for spread, wx, rng in ((2, 0, 0), (0, 2, 0), (1, 0, -MiB2), (1, 0, MiB2 + 16), (1, 0, 1 << 20)):
+            assert fgd.lib.fgd_state_layout(eng.handle, spread, wx, rng, offs, ctypes.byref(total)) == \
+                fgd.FGD_ERR_INVALID_ARG, (spread, wx, rng)
+        assert fgd.lib.fgd_state_layout(eng.handle, 0, 0, 0, None, ctypes.byref(total)) == fgd.FGD_ERR_INVALID_ARG
+        assert fgd.lib.fgd_state_layout(eng.handle, 0, 0, 0, offs, None) == fgd.FGD_ERR_INVALID_ARG
+        assert fgd.lib.fgd_state_layout(None, 0, 0, 0, offs, ctypes.byref(total)) == fgd.FGD_ERR_INVALID_ARG
+    finally:
+        eng.close()
+
+
 def test_header_compiles_as_c99_and_links(tmp_path):
     """include/fgd.h is a plain C header: a C99 program that includes it,
     links libfgd.so and calls host-only entry points (a host-only engine and

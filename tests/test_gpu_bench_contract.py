@@ -34,6 +34,7 @@ def test_fused_bench_line():
     assert d["unit"] == "GB/s" and d["higher_is_better"] is True and d["data"] == "synthetic"
     assert d["value"] > 0 and d["ms_per_step"] > 0
     assert d["config"]["workload"] == "tiny_m4_p1m_f32"
+    assert d["config"]["placement"].startswith("momentum one physical-memory range")  # the default, spread
     # 4 workers x 2^20 float32 parameters: 3 reads + 2 writes of 4 bytes per element-worker
     assert d["config"]["algorithmic_bytes_per_step"] == 4 * (1 << 20) * 20
     r = d["roofline"]
