@@ -331,11 +331,13 @@ def main():
         _, total = eng.state_layout(spread=True, with_x=split)
         need = total + M * ld * (es + 4) + 2 * int(args.copy_gb * 1e9) + 8 * P + (4 << 30)
         spread = need <= torch.cuda.mem_get_info(dev)[0]
+    free_before = torch.cuda.mem_get_info(dev)[0]
     st = eng.alloc_state(spread=spread, with_x=split)
     packed_mom = eng.state_layout(spread=False, with_x=split)[0][3]
     placement = ("momentum one physical-memory range (%.0f GiB) past theta_prev" % (st["offsets"][3] / 2**30)
                  if st["offsets"][3] != packed_mom else "packed")
-    print(f"[bench] generating {args.workload} inputs ({placement})", file=sys.stderr, flush=True)
+    print(f"[bench] generating {args.workload} inputs ({placement}; {free_before / 2**30:.1f} GiB free before the "
+          f"buffer)", file=sys.stderr, flush=True)
     tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
                                      mom_std=w["mom_std"], seed=w["seed"], device=dev,
                                      out=(st["theta_prev"], st["theta_local"], st["momentum"]))
