@@ -69,6 +69,37 @@ def test_step_parity(env, case):
     pa.run_case(fgd, torch, M, P, dtype, s1, k1, s2, k2, ld=ld, seed=M + P)
 
 
+# 32 and 64 workers (one or two parameters per lane, every worker's rows in
+# the lane's registers) with the kinds of the paper's configurations: ragged
+# tails, P below one tile, ld > P, padded tables.
+LARGE_M_CASES = [
+    (64, 3 * 4096 + 37, "f32", G, 1, REG4, 3, None),               # GlobalM1LocalM2
+    (64, 1000, "bf16", REG4, 1, REG4, 3, 1016),                    # LocalM1M2, ld > P
+    (64, 63, "f32", REG4, 1, REG4, 1, None),                       # P below one tile
+    (64, 640, "bf16", ("er_mh", 0.2, 0.3), 2, ("er_mh", 0.2, 0.3), 3, None),  # padded tables, exact tiles
+    (64, 333, "f32", ID, 0, G, 1, None),                           # DiLoCo
+    (32, 2049, "f32", G, 1, ("er_mh", 0.3, 0.2), 2, None),
+    (32, 130, "bf16", G, 1, ID, 0, None),                          # GlobalM1
+    (32, 4100, "bf16", ("ring_self", 0.2), 2, ("er_mh", 0.4, 0.1), 1, 4104),
+]
+
+
+@pytest.mark.parametrize("case", LARGE_M_CASES, ids=_id)
+def test_large_m_step_parity(env, case):
+    fgd, torch = env
+    M, P, dtype, s1, k1, s2, k2, ld = case
+    print(f"[parity-large-m] {_id(case)}", flush=True)
+    pa.run_case(fgd, torch, M, P, dtype, s1, k1, s2, k2, ld=ld, seed=M * 7 + P)
+
+
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_large_m_step_without_consensus_and_plain_momentum(env, nesterov):
+    fgd, torch = env
+    print(f"[parity-large-m] nesterov={nesterov} no consensus", flush=True)
+    pa.run_case(fgd, torch, 64, 2 * 4096 + 5, "f32", REG4, 1, REG4, 3, with_cd=False, nesterov=nesterov, seed=11)
+    pa.run_case(fgd, torch, 32, 1500, "bf16", G, 1, ("er_mh", 0.3, 0.2), 1, nesterov=nesterov, seed=12)
+
+
 def test_tiny_workload_full(env):
     """The 4-worker, 1,048,576-parameter float32 workload in full (global
     Mix1, ring Mix2, zero momentum)."""
