@@ -271,7 +271,12 @@ fgd_status fgd_min_bytes_per_step(const fgd_engine *e, int64_t *bytes);
  *                1: theta_prev, theta_local (and x) packed from offset 0 and
  *                the momentum at offset range_bytes, one range further, when
  *                the packed arrays end within the first range_bytes (else
- *                packed).  The gap between them is free for the caller.
+ *                packed).  The gap between them is free for the caller.  A
+ *                spread buffer smaller than 4/3 of range_bytes is sized to
+ *                exactly 4/3 of it (128 GiB): a power of two, which the
+ *                device allocator places as one aligned block (a smaller
+ *                buffer may be pieced together from blocks placed anywhere,
+ *                and was measured in the slow placement).
  *   with_x       1: also place x, the stored Mix1 output of split execution
  *                ([M][ld] param_dtype, after theta_local); 0: no x
  *   range_bytes  span of one physical-memory range in bytes, a multiple of

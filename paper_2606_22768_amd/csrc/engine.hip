@@ -505,6 +505,16 @@ fgd_status fgd_state_layout(const fgd_engine *e, int32_t spread, int32_t with_x,
             range = (static_cast<int64_t>(total / 3) + kGiB / 2) / kGiB * kGiB;
         }
         if (range >= end) mom = range;
+        offsets[3] = mom;
+        *total_bytes = mom + vb;
+        // A buffer of up to 4/3 of a range is rounded up to exactly 4/3 of it
+        // (128 GiB for 96 GiB ranges), a power of two the device allocator
+        // hands out as one naturally aligned block that starts at 0 or at
+        // 128 GiB of physical memory: in both cases offset 0 and the
+        // momentum's offset lie in different ranges.
+        const int64_t block = (range / 3 * 4 + kPage - 1) / kPage * kPage;
+        if (mom == range && *total_bytes < block) *total_bytes = block;
+        return FGD_OK;
     }
     offsets[3] = mom;
     *total_bytes = mom + vb;

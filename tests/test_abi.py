@@ -281,13 +281,17 @@ def test_state_layout_arithmetic(M, P, ld, dtype, with_x):
             assert offs[:3] == packed[:3]
             end = want[3]
             assert offs[3] == (rng if rng >= end else end)
-            assert total == offs[3] + vb
+            block = -(-(rng // 3 * 4) // MiB2) * MiB2   # 4/3 of a range, whole 2 MiB pages
+            if offs[3] == rng and offs[3] + vb < block:
+                assert total == block                    # rounded up to one aligned block
+            else:
+                assert total == offs[3] + vb
             spans = [(o, o + n) for o, n in zip(offs, (tb, tb, tb, vb)) if o >= 0]
             for o, _ in spans:
                 assert o % MiB2 == 0
             spans.sort()
             assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
-            assert spans[-1][1] == total
+            assert spans[-1][1] <= total
         # spread = False ignores range_bytes
         assert eng.state_layout(spread=False, with_x=with_x, range_bytes=96 * GiB) == (packed, ptotal)
     finally:
