@@ -92,18 +92,21 @@ def test_fullsize_step(env, workload):
     w = configs.WORKLOADS[workload]
     M, P, dtype = w["M"], w["P"], w["dtype"]
     ld = pa.aligned_ld(P)
+    state = bool(w.get("mix1_state"))
+    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0, mix1_state=state)
+    # The arrays are placed as bench.py places them (one spread buffer).
+    st = eng.alloc_state(spread=True)
     print(f"[fullsize] {workload}: generating inputs", flush=True)
     tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
-                                     mom_std=w["mom_std"], seed=w["seed"], device="cuda")
+                                     mom_std=w["mom_std"], seed=w["seed"], device="cuda",
+                                     out=(st["theta_prev"], st["theta_local"], st["momentum"]))
     cols = _sample_columns(P, w["seed"])
     icol = torch.from_numpy(cols).cuda()
     s_tp, s_tl, s_v = (_host(t.index_select(1, icol), d) for t, d in ((tp, dtype), (tl, dtype), (v, "f32")))
 
     t1 = configs.topology(w["mix1"], M, w["k1"], w["seed"])
     t2 = configs.topology(w["mix2"], M, w["k2"], w["seed"], step=0)
-    state = bool(w.get("mix1_state"))
     segs = configs.subset_segments(w)
-    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0, mix1_state=state)
     eng.set_topology_dict("mix1", t1)
     eng.set_topology_dict("mix2", t2)
     if segs is not None:
@@ -164,6 +167,6 @@ def test_fullsize_step(env, workload):
             assert after <= s2 ** 2 * before * (1 + 1e-5), (workload, which, k, after / before, s2 ** 2)
     print(f"[fullsize] {workload}: ok, consensus rows {np.round(cd.mean(axis=1), 6).tolist()}", flush=True)
     eng.close()
-    del tp, tl, v, cd_x0, cd_g0, cd_out
+    del tp, tl, v, st, cd_x0, cd_g0, cd_out
     gc.collect()
     torch.cuda.empty_cache()
