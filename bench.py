@@ -296,7 +296,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the engine has no multi-GPU path "
               "(each parameter index is independent, so a P-sharded run needs no exchange); "
               "use --gpus 1", file=sys.stderr)
         sys.exit(2)

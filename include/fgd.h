@@ -62,7 +62,7 @@ typedef enum {
     FGD_OK = 0,
     FGD_ERR_INVALID_ARG = 1,   /* bad pointer, size, alignment, enum or alias */
     FGD_ERR_TOPOLOGY = 2,      /* malformed CSR or masks, or W not doubly stochastic */
-    FGD_ERR_UNSUPPORTED = 3,   /* valid request this build does not implement */
+    FGD_ERR_UNSUPPORTED = 3,   /* valid request the library does not implement */
     FGD_ERR_OUT_OF_MEMORY = 4, /* host or device allocation failed */
     FGD_ERR_HIP = 5,           /* a HIP runtime call or launch failed */
     FGD_ERR_STATE = 6          /* call not allowed in the engine's current state */
@@ -94,7 +94,7 @@ typedef enum {
                                     its row's diagonal (double, ascending j, rounded) */
 } fgd_reweight;
 
-#define FGD_MAX_WORKERS 64          /* largest M this build runs */
+#define FGD_MAX_WORKERS 64          /* largest M the library runs */
 #define FGD_MAX_ROUNDS 8            /* largest number of rounds per Mix slot */
 #define FGD_MAX_SUBSET_SEGMENTS 4096 /* largest number of Mix2 subset segments */
 
