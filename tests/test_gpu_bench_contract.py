@@ -52,3 +52,15 @@ def test_js_bench_line_is_one_json_object():
     assert d["mode"] == "js" and d["unit"] == "GB/s" and d["value"] > 0
     assert d["config"]["vocab"] == 128256 and d["config"]["top_k"] == 100
     assert 0.0 < d["cd_js"] < 1.0
+
+
+def test_packed_placement_and_split_mode_lines():
+    d = _bench("--workload", "tiny_m4_p1m_f32", "--steps", "3", "--warmup", "1", "--copy-gb", "0.05",
+               "--no-cpu-baseline", "--placement", "packed")
+    assert d["config"]["placement"] == "packed" and d["roofline"]["timed_launches"] == 3
+    s = _bench("--mode", "split", "--workload", "tiny_m4_p1m_f32", "--steps", "3", "--warmup", "1",
+               "--no-cpu-baseline")
+    assert s["mode"] == "split" and s["blocking_ms"] > 0 and s["mix1_ms"] > 0 and s["round_ms_median"] > 0
+    assert s["bytes"]["mix1"] == 4 * (1 << 20) * 2 * 4                # read theta_prev, write x
+    assert s["bytes"]["blocking"] == 4 * (1 << 20) * (4 * 4 + 8 + 4)  # with the write-back into theta_local
+    assert s["config"]["placement"].startswith("momentum one physical-memory range")
