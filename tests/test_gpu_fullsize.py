@@ -170,3 +170,72 @@ def test_fullsize_step(env, workload):
     del tp, tl, v, st, cd_x0, cd_g0, cd_out
     gc.collect()
     torch.cuda.empty_cache()
+
+
+def test_fullsize_split_round(env):
+    """Split execution at the size and launch configuration of `bench.py
+    --mode split` (8 x 1.1e9 bf16, one spread buffer with x, Mix1 half on 128
+    blocks, blocking half with the write-back into theta_local), element by
+    element on sampled columns.  The blocking half runs from the oracle's x at
+    the sampled columns (written into the engine's x there), so no engine
+    output feeds the oracle."""
+    fgd, torch = env
+    name = "m8_p1100m_bf16"
+    w = configs.WORKLOADS[name]
+    M, P, dtype = w["M"], w["P"], w["dtype"]
+    ld = pa.aligned_ld(P)
+    eng = fgd.Engine(M, P, ld, dtype, configs.OUTER_LR, configs.MOMENTUM, device=0)
+    st = eng.alloc_state(spread=True, with_x=True)
+    print(f"[fullsize] split {name}: generating inputs", flush=True)
+    tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
+                                     mom_std=w["mom_std"], seed=w["seed"], device="cuda",
+                                     out=(st["theta_prev"], st["theta_local"], st["momentum"]))
+    x = st["x"]
+    cols = _sample_columns(P, w["seed"] + 5)
+    icol = torch.from_numpy(cols).cuda()
+    s_tp, s_tl, s_v = (_host(t.index_select(1, icol), d) for t, d in ((tp, dtype), (tl, dtype), (v, "f32")))
+    t1 = configs.topology(w["mix1"], M, w["k1"], w["seed"])
+    t2 = configs.topology(w["mix2"], M, w["k2"], w["seed"], step=3)
+    eng.set_topology_dict("mix1", t1)
+    eng.set_topology_dict("mix2", t2)
+    n1, n2 = eng.num_cd_rows_split()
+    cd_x0 = torch.zeros(M, dtype=torch.float64, device="cuda")
+    eng.consensus_distance(tp, cd_x0)
+
+    print(f"[fullsize] split {name}: Mix1 half", flush=True)
+    cd1 = torch.full((n1, M), float("nan"), dtype=torch.float64, device="cuda")
+    eng.mix1(tp, x, None, cd1, num_blocks=128)
+    torch.cuda.synchronize()
+    got_x = _host(x.index_select(1, icol), dtype)
+    ref_x, _, _ = oracle.mix1_split(s_tp, oracle.Mix.from_topology(t1), dtype=dtype)
+    scale = float(np.abs(tensors.bf16_bits_to_f32(s_tp)).max())
+    d = np.abs(pa.ordered_bf16(got_x) - pa.ordered_bf16(ref_x))
+    assert d.max() <= 1, f"x differs by {d.max()} bf16 ulps"
+    cd1 = cd1.cpu().numpy()
+    np.testing.assert_allclose(cd1[0], cd_x0.cpu().numpy(), rtol=1e-9)   # x^0 row = theta_prev's consensus
+    assert np.all(cd1[1] == 0.0)                                         # a global mean leaves no disagreement
+
+    print(f"[fullsize] split {name}: blocking half", flush=True)
+    xs = torch.from_numpy(ref_x.view(np.int16)).cuda().view(torch.bfloat16)
+    x.index_copy_(1, icol, xs)
+    cd2 = torch.full((n2, M), float("nan"), dtype=torch.float64, device="cuda")
+    eng.outer_step_blocking(x, tp, tl, v, cd2, write_local=True)
+    cd_out = torch.zeros(M, dtype=torch.float64, device="cuda")
+    eng.consensus_distance(tp, cd_out)
+    torch.cuda.synchronize()
+    got_t, got_tl = _host(tp.index_select(1, icol), dtype), _host(tl.index_select(1, icol), dtype)
+    got_v = _host(v.index_select(1, icol), "f32")
+    ref_t, _, ref_v, _ = oracle.outer_blocking(ref_x, s_tp, s_tl, s_v, oracle.Mix.from_topology(t2),
+                                               lr=configs.OUTER_LR, mu=configs.MOMENTUM, dtype=dtype,
+                                               write_local=True)
+    pa.compare_outputs(dtype, got_t, ref_t, got_v, ref_v, len(cols), scale)
+    assert np.array_equal(got_tl, got_t)                                 # theta' written back as the next y_0
+    cd2 = cd2.cpu().numpy()
+    np.testing.assert_allclose(cd2[-1], cd_out.cpu().numpy(), rtol=1e-9)  # theta' row = standalone consensus
+    s2 = _sigma2(t2["row_ptr"], t2["col_idx"], eng.effective_weights("mix2", 0))
+    assert cd2[1].sum() <= s2 ** 2 * cd2[0].sum() * (1 + 1e-5)
+    print(f"[fullsize] split {name}: ok", flush=True)
+    eng.close()
+    del tp, tl, v, x, st, cd_x0, cd_out
+    gc.collect()
+    torch.cuda.empty_cache()
