@@ -394,8 +394,9 @@ class Engine:
 
     def alloc_state(self, spread=True, with_x=False, range_bytes=0):
         """One device buffer laid out by fgd_state_layout and [M][ld] views of
-        it: dict(pool, theta_prev, theta_local, x (or None), momentum).  The
-        views share the pool's memory; their contents are uninitialised."""
+        it: dict(pool, theta_prev, theta_local, x (or None), momentum, offsets),
+        offsets being the layout's byte offsets.  The views share the pool's
+        memory; their contents are uninitialised."""
         import torch
 
         offs, total = self.state_layout(spread, with_x, range_bytes)
