@@ -414,6 +414,19 @@ def main():
     achieved = bytes_step / (kernel_avg_ms * 1e-3) / 1e9
     cd_host = cd.cpu().numpy()
 
+    # The step's own access pattern without its arithmetic, on the same arrays
+    # (they keep their bits): the practical ceiling of this read/write mix.
+    pattern_ms = None
+    if M in (1, 2, 4, 8, 16, 32, 64):
+        eng.stream_step_pattern(tp, tl, v, stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(5):
+            eng.stream_step_pattern(tp, tl, v, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pattern_ms = e0.elapsed_time(e1) / 5
+
     # Plain copy reference (practical streaming ceiling), timed with torch events.
     copy_gbs = None
     if args.copy_gb > 0:
@@ -462,6 +475,10 @@ def main():
                      "traffic": read_traffic(args.workload, bytes_step),
                      "kernel": "fused outer-step kernel", "kernel_avg_ms": round(kernel_avg_ms, 4),
                      "timed_launches": n_kernels, "bytes_per_launch": bytes_step},
+        "pattern_reference": None if pattern_ms is None else {
+            "ms": round(pattern_ms, 4), "gbs": round(bytes_step / (pattern_ms * 1e-3) / 1e9, 1),
+            "kernel_rate_vs_pattern": round(pattern_ms / kernel_avg_ms, 4),
+            "what": "the step's loads and stores (same tiles, launch shape, cache hints) without its arithmetic"},
         "copy_reference_gbs": None if copy_gbs is None else round(copy_gbs, 1),
         "consensus_last_step": {"rows": int(cd_host.shape[0]),
                                 "cd_sq_mean_per_row": [float(x) for x in cd_host.mean(axis=1)]},

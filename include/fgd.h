@@ -333,6 +333,18 @@ fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, i
                            int64_t num_tokens, int64_t vocab, int64_t ldk, int32_t top_k, double *d_out,
                            double *mean_out, int32_t *topk_out, void *stream);
 
+/* Streaming reference with the fused step's memory traffic and none of its
+ * arithmetic: the tiles, lane vectors, cache hints and launch shape of
+ * fgd_outer_step; every theta_prev and theta_local row of a tile is loaded
+ * before use, then row by row the momentum is loaded and theta_prev and the
+ * momentum are stored back with their own bits (the arrays are left exactly
+ * as they were; a lane vector that straddles P is not stored).  Its rate is
+ * the practical ceiling of the step's read/write mix on the arrays' placement.
+ * Same arrays and rules as fgd_outer_step; M in {1, 2, 4, 8, 16, 32, 64}
+ * (else FGD_ERR_UNSUPPORTED).  Enqueued on `stream`. */
+fgd_status fgd_stream_step_pattern(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
+                                   void *stream);
+
 /* Plain device copy of `bytes` bytes (16-byte aligned pointers, bytes % 16 ==
  * 0) on `stream`: the streaming reference against which the step's
  * bandwidth and traffic counters are read. */

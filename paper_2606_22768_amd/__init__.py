@@ -77,6 +77,7 @@ def _load():
         "fgd_enable_timing": (I32, [P, I32]),
         "fgd_read_timing": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
         "fgd_stream_copy": (I32, [P, P, I64, P]),
+        "fgd_stream_step_pattern": (I32, [P, P, P, P, P]),
         "fgd_js_distance": (I32, [P, P, I32, I32, I64, I64, I64, I32, P, P, P, P]),
         "fgd_status_string": (ctypes.c_char_p, [I32]),
         "fgd_last_error": (ctypes.c_char_p, []),
@@ -277,6 +278,11 @@ def js_distance(logits_avg, logits_workers, top_k=100, vocab=None, d_out=None, m
     return d_out, mean_out
 
 
+def fgd_stream_step_pattern(h, theta_prev, theta_local, momentum, stream=None):
+    _check(lib.fgd_stream_step_pattern(h, _dev(theta_prev), _dev(theta_local), _dev(momentum), _stream(stream)),
+           "fgd_stream_step_pattern")
+
+
 def fgd_stream_copy(dst, src, nbytes, stream=None):
     _check(lib.fgd_stream_copy(_dev(dst), _dev(src), int(nbytes), _stream(stream)), "fgd_stream_copy")
 
@@ -410,6 +416,13 @@ class Engine:
         return {"pool": pool, "theta_prev": view(offs[0], pdt, es), "theta_local": view(offs[1], pdt, es),
                 "x": None if offs[2] < 0 else view(offs[2], pdt, es),
                 "momentum": view(offs[3], torch.float32, 4), "offsets": offs}
+
+    def stream_step_pattern(self, theta_prev, theta_local, momentum, stream=None):
+        """The step's memory traffic without its arithmetic (arrays unchanged)."""
+        self._check_rows(theta_prev, "theta_prev", self.dtype)
+        self._check_rows(theta_local, "theta_local", self.dtype)
+        self._check_rows(momentum, "momentum", "f32")
+        fgd_stream_step_pattern(self.handle, theta_prev, theta_local, momentum, self._stream(stream))
 
     def enable_timing(self, on=True):
         fgd_enable_timing(self.handle, on)

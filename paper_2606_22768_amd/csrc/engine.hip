@@ -829,6 +829,42 @@ fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, i
     return FGD_OK;
 }
 
+fgd_status fgd_stream_step_pattern(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
+                                   void *stream_handle) {
+    g_last_error.clear();
+    if (fgd_status st = check_engine(e)) return st;
+    if (e->host_only) return fail(FGD_ERR_STATE, "host-only engine cannot run a kernel");
+    const fgd_config &c = e->cfg;
+    if (!theta_prev || !theta_local || !momentum) return fail(FGD_ERR_INVALID_ARG, "NULL device array");
+    if (!aligned16(theta_prev) || !aligned16(theta_local) || !aligned16(momentum))
+        return fail(FGD_ERR_INVALID_ARG, "device arrays must be 16-byte aligned");
+    const int es = elem_size(c.param_dtype);
+    if (rows_overlap(e, theta_prev, es, theta_local, es) || rows_overlap(e, theta_prev, es, momentum, 4) ||
+        rows_overlap(e, theta_local, es, momentum, 4))
+        return fail(FGD_ERR_INVALID_ARG, "theta_prev, theta_local and momentum must not overlap");
+    const void *kernel = nullptr;
+    int v = 0, bpc = 0;
+    if (!fgd::pattern_kernel_for(c.num_workers, c.param_dtype == FGD_BF16, &kernel, &v, &bpc))
+        return fail(FGD_ERR_UNSUPPORTED, "the pattern reference runs for M in {1, 2, 4, 8, 16, 32, 64}");
+    if (c.num_params == 0) return FGD_OK;
+    DeviceGuard dg;
+    hipError_t herr = dg.enter(c.device);
+    if (herr != hipSuccess) return hip_fail(herr, "selecting the engine's device");
+    fgd::PatternParams p{};
+    p.theta_prev = theta_prev;
+    p.theta_out = theta_prev;
+    p.theta_local = theta_local;
+    p.mom = momentum;
+    p.mom_out = momentum;
+    p.P = c.num_params;
+    p.ld = c.ld;
+    p.ntiles = tiles_of(c.num_params, v);
+    p.mask = 0;
+    int grid = 0;
+    if (fgd_status st = grid_for(e, kernel, 0, p.ntiles, grid, bpc)) return st;
+    return launch(kernel, grid, 0, static_cast<hipStream_t>(stream_handle), &p);
+}
+
 fgd_status fgd_stream_copy(void *dst, const void *src, int64_t bytes, void *stream_handle) {
     g_last_error.clear();
     if (!dst || !src || bytes < 0 || bytes % 16 != 0 || !aligned16(dst) || !aligned16(src))

@@ -945,6 +945,101 @@ __global__ void finalize_kernel(const double *partials, int nblocks, int n, doub
 // Plain 16-byte streaming copy.
 __global__ void copy_kernel(const u32x4 *src, u32x4 *dst, int64_t n);
 
+// ----------------------------------------------- access-pattern reference
+
+// Raw 2-, 4-, 8- or 16-byte lane accesses with the step's cache policy (a
+// 2-byte value travels in the low half of its word).
+template <int N>
+struct RawIo {
+    static constexpr int kW = N >= 4 ? N / 4 : 1;  // words per lane
+    __device__ static void load(rsrc_t r, uint32_t off, uint32_t (&o)[kW]) {
+        if constexpr (N == 16) {
+            const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadPolicy);
+            o[0] = t[0]; o[1] = t[1]; o[2] = t[2]; o[3] = t[3];
+        } else if constexpr (N == 8) {
+            const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kLoadPolicy);
+            o[0] = t[0]; o[1] = t[1];
+        } else if constexpr (N == 4) {
+            o[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadPolicy);
+        } else {
+            o[0] = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kLoadPolicy);
+        }
+    }
+    __device__ static void store(rsrc_t r, uint32_t off, const uint32_t (&i)[kW]) {
+        if constexpr (N == 16) {
+            const u32x4 t = {i[0], i[1], i[2], i[3]};
+            __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, kStorePolicy);
+        } else if constexpr (N == 8) {
+            const u32x2 t = {i[0], i[1]};
+            __builtin_amdgcn_raw_buffer_store_b64(t, r, off, 0, kStorePolicy);
+        } else if constexpr (N == 4) {
+            __builtin_amdgcn_raw_buffer_store_b32(i[0], r, off, 0, kStorePolicy);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(i[0] & 0xFFFFu), r, off, 0, kStorePolicy);
+        }
+    }
+};
+
+// The fused step's memory traffic without its arithmetic: the tiles, lane
+// vectors, cache policy and launch shape of outer_step_kernel, every
+// theta_prev and theta_local row of a tile loaded before first use, then row
+// by row the momentum loaded and theta_prev and the momentum stored.  The
+// stored words are the loaded ones OR (theta_local word AND mask) with mask =
+// 0 passed at run time, so the arrays keep their exact bits while no load can
+// be dropped.  A lane whose vector straddles P loads it and stores nothing.
+// Its rate is the practical ceiling of the step's read/write mix.
+struct PatternParams {
+    const void *theta_prev;
+    void *theta_out;
+    const void *theta_local;
+    const float *mom;
+    float *mom_out;
+    int64_t P, ld, ntiles;
+    uint32_t mask;
+};
+
+template <int MMAX, int V, int kE>
+__global__ __launch_bounds__(kBlock) void pattern_kernel(PatternParams a) {
+    constexpr int NP = V * kE, NV = V * 4;  // bytes per lane vector: parameters, momentum
+    constexpr int64_t kTile = static_cast<int64_t>(kBlock) * V;
+    const uint32_t lo = static_cast<uint32_t>(threadIdx.x) * V;
+    for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+        const int64_t tb = tile * kTile;
+        const int64_t rem = a.P - tb - lo;
+        if (rem <= 0) continue;
+        const bool whole = rem >= V;
+        constexpr int WP = RawIo<NP>::kW, WV = RawIo<NV>::kW;
+        uint32_t u1[MMAX][WP], u2[MMAX][WP];
+#pragma unroll
+        for (int m = 0; m < MMAX; ++m) {
+            RawIo<NP>::load(row_rsrc(a.theta_prev, m * a.ld + tb, kE), lo * kE, u1[m]);
+            RawIo<NP>::load(row_rsrc(a.theta_local, m * a.ld + tb, kE), lo * kE, u2[m]);
+        }
+        // Momentum rows in the step's groups (all of a group's loads first).
+        constexpr int G = (MMAX * V <= 32) ? MMAX : (32 / V > 0 ? 32 / V : 1);
+#pragma unroll
+        for (int m0 = 0; m0 < MMAX; m0 += G) {
+            uint32_t vm[G][WV];
+#pragma unroll
+            for (int j = 0; j < G; ++j)
+                RawIo<NV>::load(row_rsrc(a.mom, (m0 + j) * a.ld + tb, 4), lo * 4, vm[j]);
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                const int m = m0 + j;
+                uint32_t t[WP];
+#pragma unroll
+                for (int k = 0; k < WP; ++k) t[k] = u1[m][k] | (u2[m][k] & a.mask);
+#pragma unroll
+                for (int k = 0; k < WV; ++k) vm[j][k] |= u2[m][k % WP] & a.mask;
+                if (whole) {
+                    RawIo<NV>::store(row_rsrc(a.mom_out, m * a.ld + tb, 4), lo * 4, vm[j]);
+                    RawIo<NP>::store(row_rsrc(a.theta_out, m * a.ld + tb, kE), lo * kE, t);
+                }
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------ dispatch
 
 // Launch description of one (M, dtype) instantiation.
@@ -1101,6 +1196,9 @@ bool kernels_bf16_ms(int M, int k1, int k2, bool subset, KernelSet *out);
 // Split-execution kernels.
 bool split_kernels_f32(int M, int k1, int k2, bool subset, bool mix_state, SplitSet *out);
 bool split_kernels_bf16(int M, int k1, int k2, bool subset, bool mix_state, SplitSet *out);
+// The access-pattern reference for exact M in {1, 2, 4, 8, 16, 32, 64}: the
+// pattern_kernel instance, its lane vector and the step's blocks per CU.
+bool pattern_kernel_for(int M, bool bf16, const void **kernel, int *v, int *blocks_per_cu);
 // Jensen--Shannon distance (js.hip): launches the per-token kernel and, when
 // mean_out is given, the per-worker mean; false if a launch failed.
 bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,

@@ -46,4 +46,33 @@ __global__ __launch_bounds__(256) void copy_kernel(const u32x4 *src, u32x4 *dst,
     }
 }
 
+namespace {
+template <int M>
+void pattern_pick(bool bf16, const void **kernel, int *v, int *bpc) {
+    if (bf16) {
+        constexpr int V = lanes_v_bf16(M);
+        *kernel = reinterpret_cast<const void *>(&pattern_kernel<M, V, 2>);
+        *v = V;
+    } else {
+        constexpr int V = lanes_v_f32(M);
+        *kernel = reinterpret_cast<const void *>(&pattern_kernel<M, V, 4>);
+        *v = V;
+    }
+    *bpc = step_blocks_per_cu(M);
+}
+}  // namespace
+
+bool pattern_kernel_for(int M, bool bf16, const void **kernel, int *v, int *blocks_per_cu) {
+    switch (M) {
+        case 1: pattern_pick<1>(bf16, kernel, v, blocks_per_cu); return true;
+        case 2: pattern_pick<2>(bf16, kernel, v, blocks_per_cu); return true;
+        case 4: pattern_pick<4>(bf16, kernel, v, blocks_per_cu); return true;
+        case 8: pattern_pick<8>(bf16, kernel, v, blocks_per_cu); return true;
+        case 16: pattern_pick<16>(bf16, kernel, v, blocks_per_cu); return true;
+        case 32: pattern_pick<32>(bf16, kernel, v, blocks_per_cu); return true;
+        case 64: pattern_pick<64>(bf16, kernel, v, blocks_per_cu); return true;
+        default: return false;
+    }
+}
+
 }  // namespace fgd

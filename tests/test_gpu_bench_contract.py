@@ -44,6 +44,8 @@ def test_fused_bench_line():
     assert r["bytes_per_launch"] == d["config"]["algorithmic_bytes_per_step"]
     c = d["cpu_baseline"]
     assert c["kind"] == "oracle" and c["cores"] == 1 and c["value"] > 0 and c["unit"] == "GB/s"
+    pr = d["pattern_reference"]                       # the step's access pattern without arithmetic
+    assert pr["ms"] > 0 and pr["gbs"] > 0 and pr["kernel_rate_vs_pattern"] > 0
 
 
 def test_js_bench_line_is_one_json_object():
