@@ -366,3 +366,22 @@ int main(void) {
     assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
     # Path graph 0-1-2, Metropolis: degrees 1, 2, 1 -> w01 = w12 = 1/3, w00 = w22 = 2/3, w11 = 1/3.
     assert r.stdout.split()[:4] == ["ok", f"{np.float32(2 / 3):g}", f"{np.float32(1 / 3):g}", f"{np.float32(1 / 3):g}"]
+
+
+def test_binding_refuses_to_import_without_the_library(tmp_path):
+    """No fallback: a copy of the package without libfgd.so fails to import,
+    naming the missing library, rather than running anything on the CPU."""
+    import shutil
+    pkg = os.path.join(ROOT, "paper_2606_22768_amd")
+    dst = tmp_path / "paper_2606_22768_amd"
+    dst.mkdir()
+    for name in os.listdir(pkg):
+        if name.endswith(".py"):
+            shutil.copy(os.path.join(pkg, name), dst / name)
+    assert not (dst / "libfgd.so").exists()
+    code = ("import sys; sys.path.insert(0, sys.argv[1])\n"
+            "try:\n    import paper_2606_22768_amd\nexcept ImportError as e:\n    print('refused:', e); sys.exit(3)\n"
+            "sys.exit(0)\n")
+    r = subprocess.run(["python", "-c", code, str(tmp_path)], capture_output=True, text=True, cwd=str(tmp_path))
+    assert r.returncode == 3, (r.returncode, r.stdout, r.stderr)
+    assert "libfgd.so is missing" in r.stdout
