@@ -280,7 +280,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="m8_p1100m_bf16")
-    ap.add_argument("--cpu-slice", type=int, default=1 << 25, help="parameters per worker in the CPU sample")
+    ap.add_argument("--cpu-slice", type=int, default=None,
+                    help="parameters per worker in the CPU sample (default: 3 * 2^27 parameter-workers in all, "
+                         "about 12 s of single-threaded oracle work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
     ap.add_argument("--mode", choices=["fused", "split", "js"], default="fused",
@@ -341,7 +343,7 @@ def main():
     tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
                                      mom_std=w["mom_std"], seed=w["seed"], device=dev,
                                      out=(st["theta_prev"], st["theta_local"], st["momentum"]))
-    sl = None if args.no_cpu_baseline else host_slice(tp, tl, v, dtype, min(args.cpu_slice, P))
+    sl = None if args.no_cpu_baseline else host_slice(tp, tl, v, dtype, min(args.cpu_slice or (3 << 27) // M, P))
     segs = configs.subset_segments(w)
     if segs is not None:
         eng.set_mix2_subset(segs)
@@ -443,6 +445,7 @@ def main():
         copy_gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
         del a, b
 
+    traffic = read_traffic(args.workload, bytes_step)  # HBM bytes per launch, counters of these sources
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -472,7 +475,8 @@ def main():
                    "parallelism": "single GPU, workers simulated as rows"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": read_traffic(args.workload, bytes_step),
+                     "traffic": None if traffic is None else traffic["total_bytes"],
+                     "traffic_detail": traffic,
                      "kernel": "fused outer-step kernel", "kernel_avg_ms": round(kernel_avg_ms, 4),
                      "timed_launches": n_kernels, "bytes_per_launch": bytes_step},
         "pattern_reference": None if pattern_ms is None else {

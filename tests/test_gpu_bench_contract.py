@@ -42,6 +42,8 @@ def test_fused_bench_line():
     assert r["timed_launches"] == 25                   # every timed step, across the restore chunks
     assert r["frac"] == pytest.approx(r["achieved"] / r["peak"], rel=1e-3)
     assert r["bytes_per_launch"] == d["config"]["algorithmic_bytes_per_step"]
+    # HBM bytes per launch from committed counters of these sources, or null
+    assert r["traffic"] is None or (isinstance(r["traffic"], int) and r["traffic"] == r["traffic_detail"]["total_bytes"])
     c = d["cpu_baseline"]
     assert c["kind"] == "oracle" and c["cores"] == 1 and c["value"] > 0 and c["unit"] == "GB/s"
     pr = d["pattern_reference"]                       # the step's access pattern without arithmetic
