@@ -34,6 +34,11 @@ RING, EXP = ("ring", "given"), ("exp", "given")
 RING_MH = ("ring", "metropolis", 0.1)
 REG4 = ("regular", "metropolis", 4)
 
+# As many Mix2 subset segments as the engine accepts (4096), one in each cell
+# of 3 parameters, lengths 1 to 3, some touching the next.
+_rng = np.random.default_rng(5)
+DENSE_SEGMENTS = [(3 * i + int(_rng.integers(0, 2)), 3 * i + 3 - int(_rng.integers(0, 2))) for i in range(4096)]
+
 # (M, P, dtype, mix1, K1, mix2, K2, state, subset)
 CASES = [
     (8, 3079, "bf16", G, 1, RING_MH, 1, False, None),                 # GlobalM1LocalM2
@@ -49,6 +54,7 @@ CASES = [
     # Most rounds at the largest worker count: the Mix1 half's per-chunk partials hold 9 rows, the blocking half 10.
     (64, 600, "f32", REG4, 8, REG4, 8, True, [(0, 128), (300, 600)]),
     (64, 520, "bf16", ("er_mh", 0.1, 0.2), 8, ("ring_self", 0.3), 8, False, None),
+    (8, 3 * 4096 + 123, "bf16", G, 1, RING_MH, 1, True, DENSE_SEGMENTS),
 ]
 
 
@@ -62,7 +68,8 @@ def _host_rows(torch, t, dtype):
 
 
 def _ids(c):
-    return f"M{c[0]}-{c[2]}-{c[3][0]}{c[4]}-{c[5][0]}{c[6]}-state{int(c[7])}" + ("-subset" if c[8] else "")
+    return (f"M{c[0]}-P{c[1]}-{c[2]}-{c[3][0]}{c[4]}-{c[5][0]}{c[6]}-state{int(c[7])}"
+            + (f"-subset{len(c[8])}" if c[8] else ""))
 
 
 @pytest.mark.parametrize("write_local", [False, True], ids=["keep-local", "write-local"])
@@ -70,7 +77,8 @@ def _ids(c):
 def test_split_halves(env, case, write_local):
     fgd, torch = env
     M, P, dtype, s1, k1, s2, k2, state, subset = case
-    print(f"[split] {case} write_local={write_local}", flush=True)
+    print(f"[split] {case[:8]} subset={None if subset is None else len(subset)} segments "
+          f"write_local={write_local}", flush=True)
     ld = pa.aligned_ld(P)
     tp, tl, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, mom_std=1e-3, seed=53)
     t1, t2 = pa.topo(s1, M, k1, 53), pa.topo(s2, M, k2, 60)

@@ -104,6 +104,29 @@ def test_subset(env, case, segs):
     pa.run_case(fgd, torch, M, P, dtype, s1, k1, s2, k2, seed=41, mom_std=1e-3, mix1_state=state, subset=segs)
 
 
+def _dense_segments(n, seed):
+    """n ascending, disjoint half-open segments, one in each cell of 3
+    parameters: lengths 1 to 3, some touching the next one."""
+    rng = np.random.default_rng(seed)
+    return [(3 * i + int(rng.integers(0, 2)), 3 * i + 3 - int(rng.integers(0, 2))) for i in range(n)]
+
+
+@pytest.mark.parametrize("case", [
+    (8, "bf16", G, 1, RING_MH, 1, False),   # about 340 segments in every 1024-parameter tile
+    (8, "f32", G, 1, RING, 1, True),
+    (64, "f32", REG4, 1, REG4, 3, False),   # about 85 segments in every 256-parameter tile
+], ids=lambda c: f"M{c[0]}-{c[1]}-state{int(c[6])}")
+def test_subset_at_the_segment_limit(env, case):
+    """As many segments as the engine accepts, each of 1 to 3 parameters."""
+    fgd, torch = env
+    M, dtype, s1, k1, s2, k2, state = case
+    n = fgd.FGD_MAX_SUBSET_SEGMENTS
+    P = 3 * n + 123
+    print(f"[variants] subset of {n} segments {case}", flush=True)
+    pa.run_case(fgd, torch, M, P, dtype, s1, k1, s2, k2, seed=47, mom_std=1e-3, mix1_state=state,
+                subset=_dense_segments(n, seed=5))
+
+
 def test_subset_cleared_equals_full(env):
     """Setting a subset and then clearing it gives the full-Mix2 step."""
     fgd, torch = env
