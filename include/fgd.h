@@ -30,8 +30,11 @@
  *
  * Conventions for every call:
  *  - Every call returns an fgd_status.  Nothing throws or aborts across the
- *    ABI.  On failure nothing is launched and fgd_last_error() (per thread)
- *    holds a readable reason.
+ *    ABI.  fgd_last_error() (per thread) then holds a readable reason.  An
+ *    argument, state or support error is found before any kernel is
+ *    launched (a topology upload may already be enqueued; it writes no
+ *    caller buffer).  FGD_ERR_HIP can come from a runtime call after part of
+ *    the work was enqueued (the outputs are then unspecified).
  *  - Device arrays are worker-major [M][ld] with ld >= P elements; element p
  *    of worker m is at index m * ld + p.  Each row must start on a 16-byte
  *    boundary (base pointer 16-byte aligned and ld * element size a multiple
@@ -42,6 +45,10 @@
  *  - `stream` is a hipStream_t (NULL = the device's null stream).  Compute
  *    calls are asynchronous with respect to the host.
  *  - An engine is not thread-safe; use one engine per host thread.
+ *  - The engine's compute calls are not meant to be recorded by HIP stream
+ *    capture: a topology upload copies from a pinned host staging slot that
+ *    later uploads reuse, after waiting on the slot's event from the host.
+ *    fgd_js_distance and fgd_stream_copy enqueue kernels only.
  *  - Engine calls run on the engine's device (fgd_config.device): they make
  *    it current for their duration and restore the caller's current device
  *    before returning.  The engine-free calls (fgd_js_distance,
