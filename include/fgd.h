@@ -303,7 +303,10 @@ fgd_status fgd_state_layout(const fgd_engine *e, int32_t spread, int32_t with_x,
 /* Kernel timing.  While enabled, every fgd_outer_step brackets its fused
  * kernel with HIP events on its stream.  fgd_read_timing waits for the
  * recorded events and returns the summed kernel milliseconds and the number
- * of timed kernels since the last reset (enabling resets). */
+ * of timed kernels since the last reset (enabling, or disabling, resets).
+ * At most 4096 kernels are timed between resets; later steps run untimed
+ * (count stays at 4096).  The events are created on first use and kept
+ * until fgd_destroy. */
 fgd_status fgd_enable_timing(fgd_engine *e, int32_t enable);
 fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count);
 
