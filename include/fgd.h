@@ -45,6 +45,12 @@
  *  - `stream` is a hipStream_t (NULL = the device's null stream).  Compute
  *    calls are asynchronous with respect to the host.
  *  - An engine is not thread-safe; use one engine per host thread.
+ *  - One engine's work on different streams: fgd_outer_step,
+ *    fgd_outer_step_blocking and fgd_consensus_distance share the engine's
+ *    consensus scratch, so no two of them may run at the same time; two
+ *    fgd_mix1 launches share the Mix1 half's own counter and scratch, so they
+ *    may not either; one fgd_mix1 may overlap one of the others.  Calls on
+ *    one stream are ordered by the stream.
  *  - The engine's compute calls are not meant to be recorded by HIP stream
  *    capture: a topology upload copies from a pinned host staging slot that
  *    later uploads reuse, after waiting on the slot's event from the host.
