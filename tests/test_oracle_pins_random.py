@@ -104,3 +104,42 @@ def test_step_equals_dense_products_on_random_graphs(M, P, k1, k2, p_edge, p_dro
     for r, u in enumerate(gs):
         want_cd = ((u - u.mean(axis=0)) ** 2).sum(axis=1)
         np.testing.assert_allclose(cd[r], want_cd, rtol=1e-9, atol=1e-18)
+
+
+@settings(max_examples=80, deadline=None)
+@given(K=st.integers(2, 40), k_frac=st.floats(0.0, 1.0), scale=st.sampled_from([0.1, 1.0, 8.0, 200.0]),
+       n_masked=st.integers(0, 5), tie_levels=st.integers(0, 3), seed=st.integers(0, 2 ** 31 - 1))
+def test_js_distance_equals_rel_entr_over_an_independently_sorted_top_k(K, k_frac, scale, n_masked, tie_levels, seed):
+    """d = sqrt(JS / ln 2) with JS = 1/2 sum_{i in T} p_i log(p_i / m_i)
+    + 1/2 sum_{i in T} q_i log(q_i / m_i), m = (p + q) / 2, p and q the
+    full-vocabulary softmax, T the k largest averaged-model logits with lower
+    index first on ties (Sec. 4.4; App. D.2).  Built here from scipy's
+    softmax and rel_entr (0 log 0 = 0) and a Python sort."""
+    import math
+
+    from scipy.special import rel_entr, softmax
+
+    from oracle import js as ojs
+
+    rng = np.random.default_rng(seed)
+    za = rng.standard_normal(K) * scale
+    zw = za + rng.standard_normal(K) * scale * 0.3
+    if tie_levels:  # snap some logits onto a few shared values
+        levels = rng.standard_normal(tie_levels) * scale
+        for arr in (za, zw):
+            pick = rng.random(K) < 0.4
+            arr[pick] = levels[rng.integers(0, tie_levels, pick.sum())]
+    for arr in (za, zw):  # masked tokens (logit -inf), keeping one finite logit
+        idx = rng.permutation(K)[:min(n_masked, K - 1)]
+        arr[idx] = -np.inf
+    k = max(1, int(round(k_frac * K)))
+    p, q = softmax(zw), softmax(za)
+    top = sorted(range(K), key=lambda i: (-za[i], i))[:k]
+    m = 0.5 * (p + q)
+    js = 0.0
+    for i in sorted(top):
+        js += 0.5 * float(rel_entr(p[i], m[i])) + 0.5 * float(rel_entr(q[i], m[i]))
+    want = math.sqrt(max(js, 0.0) / math.log(2.0))
+    got = ojs.js_distance_token(zw, za, k)
+    assert abs(got - want) <= 1e-12 + 1e-9 * want, (got, want)
+    assert list(ojs.top_k_indices(za, k)) == sorted(top)
