@@ -139,7 +139,119 @@ def test_js_distance_equals_rel_entr_over_an_independently_sorted_top_k(K, k_fra
     js = 0.0
     for i in sorted(top):
         js += 0.5 * float(rel_entr(p[i], m[i])) + 0.5 * float(rel_entr(q[i], m[i]))
-    want = math.sqrt(max(js, 0.0) / math.log(2.0))
     got = ojs.js_distance_token(zw, za, k)
-    assert abs(got - want) <= 1e-12 + 1e-9 * want, (got, want)
+    # Compared as JS = d^2 ln 2: the square root would amplify the rounding
+    # of a JS near 0 (d ~ 1e-6 turns an error of 1e-17 in JS into 3e-12 in
+    # d).  The two sums of at most K terms, each below 1 in magnitude, differ
+    # in rounding by at most about K * 2^-52 absolute.
+    got_js = got * got * math.log(2.0)
+    assert abs(got_js - max(js, 0.0)) <= K * 2.0 ** -52 + 1e-12 * js, (got_js, js)
     assert list(ojs.top_k_indices(za, k)) == sorted(top)
+
+
+def _random_segments(rng, P):
+    """Ascending, disjoint, non-empty half-open segments inside [0, P)."""
+    cuts = np.sort(rng.choice(np.arange(P + 1), size=min(P + 1, 2 * int(rng.integers(1, 4))), replace=False))
+    segs = [(int(cuts[i]), int(cuts[i + 1])) for i in range(0, len(cuts) - 1, 2) if cuts[i + 1] > cuts[i]]
+    return segs or [(0, P)]
+
+
+def _dense_rounds(row_ptr, col_idx, masks, kind, M, rounds):
+    """Per-round dense matrices of a Mix slot (identity: none; global: one J)."""
+    if kind == "identity":
+        return []
+    if kind == "global":
+        return [np.full((M, M), 1.0 / M)]
+    return [_metropolis_dense(row_ptr, col_idx, masks[k]) for k in range(rounds)]
+
+
+def _apply(Ws, u, cols=None):
+    """Rounds applied in order; with cols, only on those columns (identity
+    elsewhere).  Returns every intermediate, input first."""
+    out = [u]
+    for W in Ws:
+        nxt = out[-1].copy()
+        if cols is None:
+            nxt = W @ out[-1]
+        else:
+            nxt[:, cols] = W @ out[-1][:, cols]
+        out.append(nxt)
+    return out
+
+
+def _S(u):
+    return ((u - u.mean(axis=0)) ** 2).sum(axis=1)
+
+
+@settings(max_examples=60, deadline=None)
+@given(M=st.integers(2, 8), P=st.integers(1, 20), k1=st.integers(1, 2), k2=st.integers(1, 3),
+       kind1=st.sampled_from(["csr", "global", "identity"]), kind2=st.sampled_from(["csr", "identity"]),
+       nesterov=st.booleans(), state=st.booleans(), use_subset=st.booleans(), write_local=st.booleans(),
+       seed=st.integers(0, 2 ** 31 - 1))
+def test_variants_and_split_halves_equal_dense_products(M, P, k1, k2, kind1, kind2, nesterov, state, use_subset,
+                                                         write_local, seed):
+    """Plain momentum (App. B without the Nesterov term), Mix1 on the state
+    (App. B, GlobalM1S), a Mix2 subset (Sec. 4.1, App. C: Mix2 on the listed
+    columns, identity elsewhere, consensus over every column) and the two
+    halves of split execution (App. A, Alg. 1) against dense float64 products
+    on random graphs with link drops."""
+    rng = np.random.default_rng(seed)
+    row_ptr, col_idx = _random_graph(rng, M, 0.6)
+    m1 = _random_masks(rng, row_ptr, col_idx, k1, 0.3)
+    m2 = _random_masks(rng, row_ptr, col_idx, k2, 0.3)
+    if kind2 != "csr":
+        use_subset = False  # a subset needs a table Mix2
+    segs = _random_segments(rng, P) if use_subset else None
+    cols = None if segs is None else np.concatenate([np.arange(b, e) for b, e in segs])
+    tp = (rng.standard_normal((M, P)) * 0.02).astype(np.float32)
+    tl = (tp + rng.standard_normal((M, P)) * 1e-3).astype(np.float32)
+    v = (rng.standard_normal((M, P)) * 1e-4).astype(np.float32)
+    lr, mu = float(np.float32(rng.uniform(0.1, 1.0))), float(np.float32(rng.uniform(0.0, 0.95)))
+
+    def mix(kind, masks, rounds):
+        if kind == "csr":
+            return oracle.Mix("csr", row_ptr, col_idx, None, rounds=rounds, masks=masks, reweight="metropolis")
+        return oracle.Mix(kind)
+
+    mix1, mix2 = mix(kind1, m1, k1), mix(kind2, m2, k2)
+    W1 = _dense_rounds(row_ptr, col_idx, m1, kind1, M, k1)
+    W2 = _dense_rounds(row_ptr, col_idx, m2, kind2, M, k2)
+
+    def check(got, want, what):
+        tol = max(np.abs(want).max(), 1e-30) * 2.4e-7
+        np.testing.assert_allclose(got, want, rtol=0, atol=tol, err_msg=what)
+
+    def check_cd(got, rows, what):
+        for r, u in enumerate(rows):
+            np.testing.assert_allclose(got[r], _S(u), rtol=1e-9, atol=1e-18, err_msg=f"{what} row {r}")
+
+    def optimizer(x, g, vin):
+        vn = mu * vin + g
+        return x - lr * (g + mu * vn if nesterov else vn), vn
+
+    g_rows = _apply(W2, tp.astype(np.float64) - tl.astype(np.float64), cols)
+    v_in = _apply(W1, v.astype(np.float64))[-1] if state else v.astype(np.float64)
+
+    # Fused step.
+    x_rows = _apply(W1, tp.astype(np.float64))
+    want_t, want_v = optimizer(x_rows[-1], g_rows[-1], v_in)
+    got_t, got_v, got_cd = oracle.outer_step(tp, tl, v, mix1, mix2, lr=lr, mu=mu, nesterov=nesterov,
+                                             mix1_state=state, subset=segs)
+    check(got_t, want_t, "theta'")
+    check(got_v, want_v, "v'")
+    check_cd(got_cd, g_rows + x_rows + [got_t.astype(np.float64)], "fused consensus")
+
+    # Split halves: the Mix1 half stores x in float32; the blocking half reads it.
+    x_st, v_st, cd1 = oracle.mix1_split(tp, mix1, mom=v, mix1_state=state)
+    check(x_st, x_rows[-1], "stored x")
+    check_cd(cd1, x_rows, "Mix1-half consensus")
+    if state:
+        check(v_st, v_in, "mixed state")
+    vb = v_st if state else v
+    want_t2, want_v2 = optimizer(x_st.astype(np.float64), g_rows[-1], vb.astype(np.float64))
+    got_t2, got_tl2, got_v2, cd2 = oracle.outer_blocking(x_st, tp, tl, vb, mix2, lr=lr, mu=mu, nesterov=nesterov,
+                                                         subset=segs, write_local=write_local)
+    check(got_t2, want_t2, "blocking theta'")
+    check(got_v2, want_v2, "blocking v'")
+    assert np.array_equal(got_tl2, got_t2 if write_local else tl)
+    check_cd(cd2, g_rows + [got_t2.astype(np.float64)], "blocking consensus")
