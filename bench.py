@@ -260,6 +260,7 @@ def split_round_bench(args, eng, torch, tp, tl, v, x, w, step_topos, placement):
     out = {
         "metric": "split outer step: Mix1 half hidden under the inner loop; blocking-half HBM GB/s",
         "mode": "split", "workload": args.workload, "steps": args.steps, "warmup": args.warmup,
+        "value": round(b2 / (t_block * 1e-3) / 1e9, 2), "unit": "GB/s",
         "mix1_ms": round(t_mix1, 4), "mix1_gbs": round(b1 / (t_mix1 * 1e-3) / 1e9, 1),
         "blocking_ms": round(t_block, 4), "blocking_gbs": round(b2 / (t_block * 1e-3) / 1e9, 1),
         "blocking_frac_of_peak": round(b2 / (t_block * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -269,6 +270,10 @@ def split_round_bench(args, eng, torch, tp, tl, v, x, w, step_topos, placement):
         "mix1_hidden_fraction": round(1.0 - min(exposed, t_mix1) / t_mix1, 4),
         "config": {"workers": M, "params_per_worker": P, "dtype": w["dtype"], "write_back_theta_local": True,
                    "mix1_also_on_momentum": bool(w.get("mix1_state")), "placement": placement},
+        "roofline": {"bound": "hbm", "achieved": round(b2 / (t_block * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(b2 / (t_block * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "blocking half (stream time of the call: kernel and consensus finalize)",
+                     "bytes_per_launch": b2},
         "kernel_source_hash": kernel_source_hash(),
     }
     print(json.dumps(out))

@@ -68,3 +68,5 @@ def test_packed_placement_and_split_mode_lines():
     assert s["bytes"]["mix1"] == 4 * (1 << 20) * 2 * 4                # read theta_prev, write x
     assert s["bytes"]["blocking"] == 4 * (1 << 20) * (4 * 4 + 8 + 4)  # with the write-back into theta_local
     assert s["config"]["placement"].startswith("momentum one physical-memory range")
+    assert s["unit"] == "GB/s" and s["value"] == s["roofline"]["achieved"] > 0
+    assert s["roofline"]["bound"] == "hbm" and s["roofline"]["bytes_per_launch"] == s["bytes"]["blocking"]
