@@ -333,17 +333,24 @@ __device__ inline float wave_reduce_scatter(float (&part)[C], int lane) {
     return part[0];
 }
 
-// Mean over the M rows of u, per element (float32, ascending rows).
+// Sum of element v of rows [LO, LO + N) of u, rows at or past M counting as
+// 0, as a balanced tree: each rounding chain has about log2(N) additions
+// instead of N - 1 (64 workers of zero-mean values otherwise lose a few
+// parts in 1e7 of their mean to float32 rounding).
+template <int MMAX, bool EXACT, int V, int LO, int N>
+__device__ __forceinline__ float tree_sum(const float (&u)[MMAX][V], int M, int v) {
+    if constexpr (N == 1) {
+        return (EXACT || LO < M) ? u[LO][v] : 0.0f;
+    } else {
+        return tree_sum<MMAX, EXACT, V, LO, N / 2>(u, M, v) + tree_sum<MMAX, EXACT, V, LO + N / 2, N - N / 2>(u, M, v);
+    }
+}
+
+// Mean over the M rows of u, per element (float32, fixed pairwise order).
 template <int MMAX, bool EXACT, int V>
 __device__ inline void row_mean(const float (&u)[MMAX][V], int M, float (&mean)[V]) {
 #pragma unroll
-    for (int v = 0; v < V; ++v) {
-        float s = 0.0f;
-#pragma unroll
-        for (int m = 0; m < MMAX; ++m)
-            if (EXACT || m < M) s += u[m][v];
-        mean[v] = s / static_cast<float>(EXACT ? MMAX : M);
-    }
+    for (int v = 0; v < V; ++v) mean[v] = tree_sum<MMAX, EXACT, V, 0, MMAX>(u, M, v) / static_cast<float>(EXACT ? MMAX : M);
 }
 
 // Adds this lane-column's contribution to S_m(u) = sum_p (u_m - mean)^2 into
@@ -398,6 +405,30 @@ constexpr int kStored = 4;
 // scalar registers, shared by the wave.
 typedef const __attribute__((address_space(4))) int32_t *const_table_ptr;
 
+// The lane's V values of row `col` in its LDS column.
+template <int V>
+__device__ __forceinline__ void lds_row(const float *rows, int col, int tid, float (&r)[V]) {
+    const float *src = rows + (static_cast<int64_t>(col) * kBlock + tid) * V;
+    if constexpr (V == 4) {
+        const f32x4 t = *reinterpret_cast<const f32x4 *>(src);
+        r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
+    } else if constexpr (V == 2) {
+        const f32x2 t = *reinterpret_cast<const f32x2 *>(src);
+        r[0] = t.x; r[1] = t.y;
+    } else {
+#pragma unroll
+        for (int v = 0; v < V; ++v) r[v] = src[v];
+    }
+}
+
+// Tables at least this wide (in kernels for more than 16 workers) are summed
+// four entries at a time, each four as a small tree added to the running
+// sum: one float32 chain over a dense row of W (up to 64 entries) would
+// otherwise lose up to a part in 1e6 of a mixed value that is much smaller
+// than its terms.  Narrower tables (the sparse graphs: rings, exponential
+// and regular graphs) take one fused multiply-add per entry.
+constexpr int kWideTable = 16;
+
 // One table round applied in place, u_m <- sum_d w[d][m] * u_{col[d][m]},
 // gathering through the lane's LDS column.
 template <int MMAX, bool EXACT, int V>
@@ -420,7 +451,35 @@ __device__ inline void table_round_lds(const_table_ptr tab, int width, int M, fl
 #pragma unroll
         for (int v = 0; v < V; ++v) u[m][v] = 0.0f;
     }
-    for (int d = 0; d < width; ++d) {
+    int d = 0;
+    // Kernels for up to 16 workers leave this path out: their tables are at
+    // most 16 wide, short enough for one chain, and the path's presence alone
+    // made the compiler schedule their narrow path 8-14% slower.
+    if constexpr (MMAX > kWideTable) {
+        for (; width >= kWideTable && d + 4 <= width; d += 4) {
+            const_table_ptr td = tab + 2 * d * Mr;
+#pragma unroll
+            for (int m = 0; m < MMAX; ++m) {
+                if (m % 8 == 0 && m > 0) __builtin_amdgcn_sched_barrier(0);
+                if (EXACT || m < M) {
+                    float r0[V], r1[V], r2[V], r3[V];
+                    lds_row<V>(rows, td[2 * m], tid, r0);
+                    lds_row<V>(rows, td[2 * Mr + 2 * m], tid, r1);
+                    lds_row<V>(rows, td[4 * Mr + 2 * m], tid, r2);
+                    lds_row<V>(rows, td[6 * Mr + 2 * m], tid, r3);
+                    const float w0 = __int_as_float(td[2 * m + 1]), w1 = __int_as_float(td[2 * Mr + 2 * m + 1]);
+                    const float w2 = __int_as_float(td[4 * Mr + 2 * m + 1]), w3 = __int_as_float(td[6 * Mr + 2 * m + 1]);
+#pragma unroll
+                    for (int v = 0; v < V; ++v) {
+                        const float a = fmaf(w0, r0[v], w1 * r1[v]);
+                        const float b = fmaf(w2, r2[v], w3 * r3[v]);
+                        u[m][v] += a + b;
+                    }
+                }
+            }
+        }
+    }
+    for (; d < width; ++d) {
         const_table_ptr td = tab + 2 * d * Mr;
 #pragma unroll
         for (int m = 0; m < MMAX; ++m) {
@@ -428,20 +487,9 @@ __device__ inline void table_round_lds(const_table_ptr tab, int width, int M, fl
             // scalar registers at once.
             if (m % 16 == 0 && m > 0) __builtin_amdgcn_sched_barrier(0);
             if (EXACT || m < M) {
-                const int col = td[2 * m];
                 const float w = __int_as_float(td[2 * m + 1]);
-                const float *src = rows + (static_cast<int64_t>(col) * kBlock + tid) * V;
                 float r[V];
-                if constexpr (V == 4) {
-                    const f32x4 t = *reinterpret_cast<const f32x4 *>(src);
-                    r[0] = t.x; r[1] = t.y; r[2] = t.z; r[3] = t.w;
-                } else if constexpr (V == 2) {
-                    const f32x2 t = *reinterpret_cast<const f32x2 *>(src);
-                    r[0] = t.x; r[1] = t.y;
-                } else {
-#pragma unroll
-                    for (int v = 0; v < V; ++v) r[v] = src[v];
-                }
+                lds_row<V>(rows, td[2 * m], tid, r);
 #pragma unroll
                 for (int v = 0; v < V; ++v) u[m][v] = fmaf(w, r[v], u[m][v]);
             }

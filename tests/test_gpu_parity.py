@@ -81,6 +81,11 @@ LARGE_M_CASES = [
     (32, 2049, "f32", G, 1, ("er_mh", 0.3, 0.2), 2, None),
     (32, 130, "bf16", G, 1, ID, 0, None),                          # GlobalM1
     (32, 4100, "bf16", ("ring_self", 0.2), 2, ("er_mh", 0.4, 0.1), 1, 4104),
+    # Dense W (64 and about 40 entries per row): sums long enough that one
+    # float32 chain per row would approach the 1e-6 bar on their small means.
+    (64, 2661, "f32", ("complete",), 2, G, 1, None),
+    (48, 1777, "f32", ("er_mh", 0.9, 0.1), 3, ("complete",), 2, None),
+    (64, 901, "bf16", ("complete",), 1, ("er_mh", 0.7, 0.0), 2, None),
 ]
 
 
