@@ -75,6 +75,22 @@ def _ids(c):
 @pytest.mark.parametrize("write_local", [False, True], ids=["keep-local", "write-local"])
 @pytest.mark.parametrize("case", CASES, ids=_ids)
 def test_split_halves(env, case, write_local):
+    _split_case(env, case, write_local)
+
+
+@pytest.mark.parametrize("i", range(200))
+def test_split_halves_random_configurations(env, i):
+    """The seeded random configurations of the fused-step variants tests
+    (worker count, size, storage, Mix kinds and rounds, masks, reweighting,
+    optimizer form, state mix, subset) through both halves."""
+    from tests.test_gpu_variants import _random_case
+
+    c = _random_case(5000 + i)
+    _split_case(env, (c["M"], c["P"], c["dtype"], c["s1"], c["k1"], c["s2"], c["k2"], c["state"], c["subset"]),
+                bool(i % 2))
+
+
+def _split_case(env, case, write_local):
     fgd, torch = env
     M, P, dtype, s1, k1, s2, k2, state, subset = case
     print(f"[split] {case[:8]} subset={None if subset is None else len(subset)} segments "

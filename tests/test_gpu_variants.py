@@ -197,7 +197,7 @@ def _random_case(i):
                 state=bool(rng.random() < 0.3), subset=subset)
 
 
-@pytest.mark.parametrize("i", range(24))
+@pytest.mark.parametrize("i", range(200))
 def test_random_configurations(env, i):
     fgd, torch = env
     c = _random_case(i)
