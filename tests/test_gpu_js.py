@@ -218,3 +218,49 @@ def test_js_wide_logit_range(env, dtype):
         A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
         W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
     _check(fgd, torch, A, W, dtype, K, k)
+
+
+def _random_js_case(i):
+    """Seeded random JS configuration: workers, tokens, vocabulary (tiny,
+    mid, large), row stride, storage, k up to 1024, and a logit kind: plain,
+    heavy ties (integers), wide range (the rescale path), masked tokens, or
+    rows of equal logits (the radix-select fallback)."""
+    rng = np.random.default_rng(777 + i)
+    M = int(rng.integers(1, 7))
+    U = int(rng.integers(1, 5))
+    K = int(rng.choice([int(rng.integers(1, 64)), int(rng.integers(64, 3000)), int(rng.integers(3000, 9000))]))
+    dtype = str(rng.choice(["f32", "bf16"]))
+    per = 4 if dtype == "f32" else 8
+    ldk = (K + int(rng.integers(0, 3)) * per + per - 1) // per * per
+    k = int(min(K, rng.choice([1, int(rng.integers(1, 100)), 100, int(rng.integers(100, 1025))])))
+    kind = int(rng.integers(0, 5))
+    za = rng.standard_normal((U, ldk)) * float(rng.choice([0.5, 2.0, 8.0]))
+    if kind == 1:
+        za = np.round(za)
+    if kind == 2:
+        za = za * 50
+    zw = za[None] + rng.standard_normal((M, U, ldk)) * float(rng.choice([1e-3, 0.1, 1.0]))
+    if kind == 3:  # masked tokens; every distribution keeps a finite logit
+        ma = rng.random(ldk) < 0.2
+        mw = rng.random(ldk) < 0.2
+        ma[0] = mw[0] = False
+        za[:, ma] = -np.inf
+        zw[:, :, mw] = -np.inf
+    if kind == 4:
+        za[:] = za[:, :1]
+        zw[:] = zw[:, :, :1]
+    za, zw = za.astype(np.float32), zw.astype(np.float32)
+    if dtype == "bf16":
+        import torch
+
+        za = torch.from_numpy(za).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        zw = torch.from_numpy(zw).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    return M, U, K, ldk, dtype, k, za, zw
+
+
+@pytest.mark.parametrize("i", range(300))
+def test_js_random_configurations(env, i):
+    fgd, torch = env
+    M, U, K, ldk, dtype, k, A, W = _random_js_case(i)
+    print(f"[js] random case {i}: M={M} U={U} K={K} ldk={ldk} {dtype} k={k}", flush=True)
+    _check(fgd, torch, A, W, dtype, K, k)
