@@ -202,6 +202,44 @@ def test_standalone_consensus(env, M, P, dtype, ld):
     eng.close()
 
 
+@pytest.mark.parametrize("i", range(100))
+def test_standalone_consensus_random(env, i):
+    """fgd_consensus_distance on seeded random shapes and storages: plain
+    rows, identical workers (S = 0 in double; float32 means of equal values
+    sit at the rounding floor) and one worker offset from the rest."""
+    fgd, torch = env
+    rng = np.random.default_rng(4000 + i)
+    M = int(rng.choice([1, 2, 3, 5, 8, 9, 16, 17, 31, 32, 47, 64]))
+    P = int(rng.integers(1, 20000))
+    dtype = str(rng.choice(["f32", "bf16"]))
+    per = 4 if dtype == "f32" else 8
+    ld = (P + int(rng.integers(0, 3)) * per + per - 1) // per * per
+    tp, _, _ = tensors.numpy_inputs(M, ld, dtype=dtype, seed=4000 + i)
+    kind = int(rng.integers(0, 3))
+    if kind == 1:
+        tp[:] = tp[:1]
+    elif kind == 2 and M > 1:  # all rows equal but one, offset by 0.01
+        tp[:] = tp[:1]
+        j = int(rng.integers(0, M))
+        if dtype == "f32":
+            tp[j] = tp[j] + np.float32(0.01)
+        else:
+            tp[j] = tensors.f32_to_bf16_bits(tensors.bf16_bits_to_f32(tp[j]) + np.float32(0.01))
+    print(f"[parity] standalone consensus {i}: M={M} P={P} ld={ld} {dtype} kind={kind}", flush=True)
+    ref = oracle.consensus(tp, P=P)
+    eng = fgd.Engine(M, P, ld, dtype, device=0)
+    x = torch.from_numpy(tp if dtype == "f32" else tp.view(np.int16)).cuda()
+    if dtype == "bf16":
+        x = x.view(torch.bfloat16)
+    out = torch.full((M,), float("nan"), dtype=torch.float64, device="cuda")
+    eng.consensus_distance(x, out)
+    torch.cuda.synchronize()
+    vals = tensors.bf16_bits_to_f32(tp) if dtype == "bf16" else tp
+    scale = float(np.abs(vals[:, :P]).max())
+    pa.compare_cd(out.cpu().numpy()[None, :], ref[None, :], pa.cd_floor(P, scale))
+    eng.close()
+
+
 def test_fused_theta_row_matches_standalone(env):
     """The fused consensus row of theta' equals the standalone kernel run on
     the stored theta' (two different kernels, same definition)."""
