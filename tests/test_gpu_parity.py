@@ -202,6 +202,26 @@ def test_standalone_consensus(env, M, P, dtype, ld):
     eng.close()
 
 
+# Sizes large enough that the persistent grid (one block per CU at 16 or
+# fewer workers, two at 32 and 64) strides over several tiles per block, so
+# the consensus accumulators carry across tiles; every output is compared.
+MULTI_TILE_CASES = [
+    (8, 600_003, "f32", G, 1, RING_MH, 1),           # ~2.3 tiles per block
+    (8, 1_200_001, "bf16", G, 1, RING_MH, 1),        # ~4.6
+    (16, 700_001, "f32", G, 1, EXP, 2),              # ~2.7
+    (64, 200_003, "f32", REG4, 1, REG4, 3),          # ~1.5 (V = 1, 512 blocks)
+    (32, 600_001, "bf16", G, 1, ("er_mh", 0.3, 0.2), 2),  # ~2.3 (V = 2, 512 blocks)
+]
+
+
+@pytest.mark.parametrize("case", MULTI_TILE_CASES, ids=lambda c: f"M{c[0]}-P{c[1]}-{c[2]}")
+def test_multi_tile_per_block_parity(env, case):
+    fgd, torch = env
+    M, P, dtype, s1, k1, s2, k2 = case
+    print(f"[parity] multi-tile {case}", flush=True)
+    pa.run_case(fgd, torch, M, P, dtype, s1, k1, s2, k2, seed=61)
+
+
 @pytest.mark.parametrize("i", range(100))
 def test_standalone_consensus_random(env, i):
     """fgd_consensus_distance on seeded random shapes and storages: plain

@@ -55,6 +55,9 @@ CASES = [
     (64, 600, "f32", REG4, 8, REG4, 8, True, [(0, 128), (300, 600)]),
     (64, 520, "bf16", ("er_mh", 0.1, 0.2), 8, ("ring_self", 0.3), 8, False, None),
     (8, 3 * 4096 + 123, "bf16", G, 1, RING_MH, 1, True, DENSE_SEGMENTS),
+    # Enough tiles that the Mix1 half's chunks hold several tiles each and the
+    # blocking half's blocks stride over several tiles.
+    (8, 4_300_003, "f32", G, 1, RING_MH, 1, False, [(0, 1_420_000), (3_870_000, 4_300_003)]),
 ]
 
 
