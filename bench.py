@@ -22,7 +22,6 @@ them back to back instead.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import platform
@@ -38,39 +37,21 @@ RESTORE_EVERY = 20      # timed steps between restores of the pristine inputs
 METRIC = "outer-step HBM GB/s and % of MI355X HBM peak; params·workers/sec"
 
 
-def kernel_source_hash(component="step"):
-    """Hash of the HIP sources of one component: "step" (the fused step, the
-    split halves, consensus, finalize and copy kernels and their launches:
-    every source but the JS distance's) or "js" (the JS distance kernels and
-    the header they include).  Traffic counters are valid only for the hash
-    they were taken with."""
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2606_22768_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if not name.endswith((".hip", ".hpp")):
-            continue
-        if component == "js" and name not in ("js.hip", "kernels.hpp"):
-            continue
-        if component == "step" and name == "js.hip":
-            continue
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
-    return h.hexdigest()[:16]
-
-
-def read_traffic(workload, bytes_per_launch):
-    """HBM traffic per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_fused_step_{workload}.json")
+def read_traffic(workload, bytes_per_launch, step_hash, kernel="fused_step"):
+    """HBM traffic per launch from the committed rocprofv3 counter summary,
+    if it was taken with a library built from the same step sources as the
+    loaded one (`step_hash`, the library's own fgd_source_hash); else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("kernel_source_hash") != kernel_source_hash():
+    if t.get("kernel_source_hash") != step_hash:
         return None
     return {"fetch_bytes": t["fetch_bytes_per_launch"], "write_bytes": t["write_bytes_per_launch"],
             "total_bytes": t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"],
-            "ratio_to_algorithmic": (t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"]) / bytes_per_launch}
+            "ratio_to_algorithmic": (t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"]) / bytes_per_launch,
+            "kernel_source_hash": step_hash}
 
 
 def host_cpu():
@@ -171,7 +152,7 @@ def js_bench(args, fgd, torch):
            "cd_js": float(mean.mean().item()),
            "config": {"workload": f"js_m{M}_u{U}_v{K}_{w['dtype']}", "workers": M, "tokens": U, "vocab": K,
                       "top_k": k, "dtype": w["dtype"], "bytes_per_step": nbytes},
-           "kernel_source_hash": kernel_source_hash("js")}
+           "kernel_source_hash": fgd.library_source_hash()["js"], "library_source_hash": fgd.library_source_hash()}
     if not args.no_cpu_baseline:
         from oracle import js as ojs
 
@@ -187,7 +168,7 @@ def js_bench(args, fgd, torch):
     print(json.dumps(out))
 
 
-def split_round_bench(args, eng, torch, tp, tl, v, x, w, step_topos, placement):
+def split_round_bench(args, fgd, eng, torch, tp, tl, v, x, w, step_topos, placement):
     """Split execution of a round (Appendix A, Algorithm 1): the Mix1 half is
     launched on a side stream at the start of the round and overlaps a
     stand-in inner loop (bf16 matrix products on the main stream); the
@@ -274,7 +255,7 @@ def split_round_bench(args, eng, torch, tp, tl, v, x, w, step_topos, placement):
                      "unit": "GB/s", "frac": round(b2 / (t_block * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
                      "kernel": "blocking half (stream time of the call: kernel and consensus finalize)",
                      "bytes_per_launch": b2},
-        "kernel_source_hash": kernel_source_hash(),
+        "kernel_source_hash": fgd.library_source_hash()["step"], "library_source_hash": fgd.library_source_hash(),
     }
     print(json.dumps(out))
 
@@ -373,7 +354,7 @@ def main():
         eng.outer_step(tp, tl, v, cd, stream)
 
     if split:
-        split_round_bench(args, eng, torch, tp, tl, v, st["x"], w, step_topos, placement)
+        split_round_bench(args, fgd, eng, torch, tp, tl, v, st["x"], w, step_topos, placement)
         eng.close()
         return
 
@@ -450,7 +431,8 @@ def main():
         copy_gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
         del a, b
 
-    traffic = read_traffic(args.workload, bytes_step)  # HBM bytes per launch, counters of these sources
+    lib_hash = fgd.library_source_hash()
+    traffic = read_traffic(args.workload, bytes_step, lib_hash["step"])  # counters of this library's sources
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -464,7 +446,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32",  # the arithmetic type; storage_dtype gives the parameters' storage
+        "storage_dtype": dtype,
         "data": "synthetic",
         "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
         "params_workers_per_s": round(M * P * args.steps / elapsed, 1),
@@ -491,7 +474,8 @@ def main():
         "copy_reference_gbs": None if copy_gbs is None else round(copy_gbs, 1),
         "consensus_last_step": {"rows": int(cd_host.shape[0]),
                                 "cd_sq_mean_per_row": [float(x) for x in cd_host.mean(axis=1)]},
-        "kernel_source_hash": kernel_source_hash(),
+        "kernel_source_hash": lib_hash["step"],
+        "library_source_hash": lib_hash,
     }
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)

@@ -372,6 +372,15 @@ const char *fgd_status_string(int32_t status);
 /* Detail of the last failure on the calling thread ("" if none). */
 const char *fgd_last_error(void);
 
+/* Hash of the sources this library was built from, 16 hex digits, fixed at
+ * build time: component 0 = every library source and this header, 1 = the
+ * outer-step sources (every kernel source but the JS distance's), 2 = the JS
+ * distance sources; "unstamped" for a build that did not supply them, "" for
+ * another component.  A static string, never NULL.  Tools compare it with
+ * the source tree to refuse a library built from other sources, and accept
+ * recorded counters or timings only for the hash they were taken with. */
+const char *fgd_source_hash(int32_t component);
+
 #ifdef __cplusplus
 }
 #endif

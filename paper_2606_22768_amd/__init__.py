@@ -55,7 +55,7 @@ def _load():
     import torch  # noqa: F401
 
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_22768_amd.build`")
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2606_22768_amd/build.py`")
     L = ctypes.CDLL(LIB_PATH)
     P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     sig = {
@@ -81,14 +81,39 @@ def _load():
         "fgd_js_distance": (I32, [P, P, I32, I32, I64, I64, I64, I32, P, P, P, P]),
         "fgd_status_string": (ctypes.c_char_p, [I32]),
         "fgd_last_error": (ctypes.c_char_p, []),
+        "fgd_source_hash": (ctypes.c_char_p, [I32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
         f.restype, f.argtypes = res, args
+    _check_sources(L)
     return L
 
 
+def _library_hashes(L):
+    return {c: L.fgd_source_hash(i).decode() for i, c in enumerate(("all", "step", "js"))}
+
+
+def _check_sources(L, root=None):
+    """Refuses a library built from other sources than the tree beside it:
+    its tests and timings would describe other code."""
+    from . import build as _build
+
+    root = root or _build.ROOT
+    if not os.path.isdir(os.path.join(root, "paper_2606_22768_amd", "csrc")):
+        return  # an installed copy without sources: nothing to compare with
+    have, want = _library_hashes(L), _build.source_hashes(root)
+    if have["all"] != want["all"]:
+        raise ImportError(f"{LIB_PATH} was built from other sources (library {have['all']}, sources "
+                          f"{want['all']}): rebuild it with `python paper_2606_22768_amd/build.py`")
+
+
 lib = _load()
+
+
+def library_source_hash() -> dict:
+    """The source hashes compiled into the loaded library (all, step, js)."""
+    return _library_hashes(lib)
 
 
 def fgd_status_string(status: int) -> str:
@@ -346,6 +371,27 @@ class Engine:
         if not t.is_cuda or t.device.index != self.device:
             raise ValueError(f"{name}: expected a tensor on cuda:{self.device}, got {t.device}")
 
+    def _check_out(self, t, name, rows):
+        """A consensus output: float64, rows x M doubles or more, contiguous, on
+        the engine's device.  The kernels write rows * M doubles through the
+        raw pointer, so a smaller or differently typed buffer is refused here,
+        before anything is enqueued."""
+        import torch
+
+        if t is None:
+            return
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+        if t.dtype != torch.float64:
+            raise TypeError(f"{name}: expected torch.float64, got {t.dtype}")
+        need = int(rows) * self.M
+        if t.numel() < need:
+            raise ValueError(f"{name}: needs at least {rows} x {self.M} = {need} doubles, got {t.numel()}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name}: must be contiguous")
+        if not t.is_cuda or t.device.index != self.device:
+            raise ValueError(f"{name}: expected a tensor on cuda:{self.device}, got {t.device}")
+
     def _stream(self, stream):
         """The given stream, or torch's current stream on the engine's device."""
         if stream is not None:
@@ -355,6 +401,8 @@ class Engine:
         return torch.cuda.current_stream(self.device)
 
     def outer_step(self, theta_prev, theta_local, momentum, cd_out=None, stream=None):
+        if cd_out is not None:
+            self._check_out(cd_out, "cd_out", self.num_cd_rows())
         self._check_rows(theta_prev, "theta_prev", self.dtype)
         self._check_rows(theta_local, "theta_local", self.dtype)
         self._check_rows(momentum, "momentum", "f32")
@@ -363,6 +411,8 @@ class Engine:
     def mix1(self, theta_prev, x_out, momentum=None, cd_out=None, stream=None, num_blocks=0):
         """Mix1 half of split execution: x_out = Mix1(theta_prev) (and the
         momentum mixed in place when the engine mixes the state)."""
+        if cd_out is not None:
+            self._check_out(cd_out, "cd_out", self.num_cd_rows_split()[0])
         self._check_rows(theta_prev, "theta_prev", self.dtype)
         self._check_rows(x_out, "x_out", self.dtype)
         if momentum is not None:
@@ -371,6 +421,8 @@ class Engine:
 
     def outer_step_blocking(self, x, theta_prev, theta_local, momentum, cd_out=None, write_local=False, stream=None):
         """Blocking half of split execution, from the stored Mix1 output x."""
+        if cd_out is not None:
+            self._check_out(cd_out, "cd_out", self.num_cd_rows_split()[1])
         self._check_rows(x, "x", self.dtype)
         self._check_rows(theta_prev, "theta_prev", self.dtype)
         self._check_rows(theta_local, "theta_local", self.dtype)
@@ -386,6 +438,7 @@ class Engine:
 
     def consensus_distance(self, x, out, stream=None, dtype=None):
         dtype = dtype or self.dtype
+        self._check_out(out, "out", 1)
         self._check_rows(x, "x", dtype)
         fgd_consensus_distance(self.handle, x, dtype, out, self._stream(stream))
 

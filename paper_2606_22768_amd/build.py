@@ -1,11 +1,22 @@
 """Builds libfgd.so in-tree: hipcc for the gfx950 kernels and the engine,
 g++ for the host-only topology code.
 
-    python -m paper_2606_22768_amd.build
+    python paper_2606_22768_amd/build.py
+
+(run as a script: importing the package loads the library, which a stale
+or missing build would refuse).
+
+The library carries the hashes of the sources it was built from: they are
+compiled into it (fgd_source_hash) and written beside it in libfgd.so.json,
+so a library and a source tree that disagree can be told apart without
+running anything (needs_build) and once loaded (the binding refuses such a
+library).
 """
 
 from __future__ import annotations
 
+import hashlib
+import json
 import os
 import shutil
 import subprocess
@@ -28,6 +39,55 @@ ARCH = "gfx950"
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-function",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-ffp-contract=fast"]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
+
+HASH_COMPONENTS = ("all", "step", "js")
+
+
+def source_hashes(root: str = ROOT) -> dict:
+    """Hashes (16 hex digits) of the sources under `root`:
+    all   every file under paper_2606_22768_amd/csrc and include/fgd.h;
+    step  the HIP sources of the outer step, its split halves, consensus,
+          finalize and copy kernels and their launches (every .hip/.hpp but
+          the JS distance's);
+    js    the JS distance kernels and the header they include.
+    Traffic counters and timings are valid only for the hash they were
+    taken with."""
+    csrc = os.path.join(root, "paper_2606_22768_amd", "csrc")
+    names = sorted(os.listdir(csrc))
+    hs = {c: hashlib.sha256() for c in HASH_COMPONENTS}
+    for name in names:
+        with open(os.path.join(csrc, name), "rb") as f:
+            data = name.encode() + b"\0" + f.read()
+        hs["all"].update(data)
+        if name.endswith((".hip", ".hpp")):
+            if name != "js.hip":
+                hs["step"].update(data)
+            if name in ("js.hip", "kernels.hpp"):
+                hs["js"].update(data)
+    with open(os.path.join(root, "include", "fgd.h"), "rb") as f:
+        hs["all"].update(b"fgd.h\0" + f.read())
+    return {c: h.hexdigest()[:16] for c, h in hs.items()}
+
+
+def sidecar_path(lib_path: str = LIB) -> str:
+    return lib_path + ".json"
+
+
+def read_sidecar(lib_path: str = LIB):
+    """The source hashes recorded beside a built library, or None."""
+    try:
+        with open(sidecar_path(lib_path)) as f:
+            return json.load(f).get("source_hash")
+    except (OSError, ValueError):
+        return None
+
+
+def needs_build(lib_path: str = LIB, root: str = ROOT) -> bool:
+    """True when the library is missing or was built from other sources than
+    those now under `root` (judged from its sidecar, without loading it)."""
+    if not os.path.exists(lib_path):
+        return True
+    return read_sidecar(lib_path) != source_hashes(root)
 
 
 def _hipcc():
@@ -52,14 +112,17 @@ def build(verbose: bool = False, jobs: int = 8, defines=(), out=None, build_dir=
     lib_path = out or LIB
     bdir = build_dir or BUILD
     os.makedirs(bdir, exist_ok=True)
+    hashes = source_hashes()
     extra = [f"-D{d}" for d in defines]
+    stamp = [f'-DFGD_HASH_{c.upper()}="{hashes[c]}"' for c in HASH_COMPONENTS]
     hipcc = _hipcc()
     inc = ["-I", os.path.join(ROOT, "include")]
     cmds = []
     objs = []
     for s in HIP_SOURCES:
         o = os.path.join(bdir, s.replace(".", "_") + ".o")
-        cmds.append([hipcc, *HIP_FLAGS, *extra, *inc, "-c", os.path.join(CSRC, s), "-o", o])
+        cmds.append([hipcc, *HIP_FLAGS, *extra, *(stamp if s == "engine.hip" else []), *inc, "-c",
+                     os.path.join(CSRC, s), "-o", o])
         objs.append(o)
     for s in CXX_SOURCES:
         o = os.path.join(bdir, s.replace(".", "_") + ".o")
@@ -71,7 +134,14 @@ def build(verbose: bool = False, jobs: int = 8, defines=(), out=None, build_dir=
                 print(r.stderr, file=sys.stderr)
     tmp = lib_path + ".tmp"
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs])
+    # The sidecar is written only with the library it describes: a build
+    # with tuning macros is not the shipped configuration, so its sidecar
+    # records them and never matches needs_build's plain source hashes.
+    side = {"source_hash": hashes if not defines else {**hashes, "defines": list(defines)}}
+    with open(sidecar_path(lib_path) + ".tmp", "w") as f:
+        json.dump(side, f)
     os.replace(tmp, lib_path)
+    os.replace(sidecar_path(lib_path) + ".tmp", sidecar_path(lib_path))
     return lib_path
 
 

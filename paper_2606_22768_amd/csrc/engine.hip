@@ -312,6 +312,26 @@ const char *fgd_status_string(int32_t s) {
 
 const char *fgd_last_error(void) { return g_last_error.c_str(); }
 
+// Source hashes stamped in by the build (paper_2606_22768_amd/build.py).
+#ifndef FGD_HASH_ALL
+#define FGD_HASH_ALL "unstamped"
+#endif
+#ifndef FGD_HASH_STEP
+#define FGD_HASH_STEP "unstamped"
+#endif
+#ifndef FGD_HASH_JS
+#define FGD_HASH_JS "unstamped"
+#endif
+
+const char *fgd_source_hash(int32_t component) {
+    switch (component) {
+        case 0: return FGD_HASH_ALL;
+        case 1: return FGD_HASH_STEP;
+        case 2: return FGD_HASH_JS;
+        default: return "";
+    }
+}
+
 fgd_status fgd_create(const fgd_config *cfg, fgd_engine **out) {
     g_last_error.clear();
     if (!cfg || !out) return fail(FGD_ERR_INVALID_ARG, "cfg and out must not be NULL");

@@ -385,3 +385,91 @@ def test_binding_refuses_to_import_without_the_library(tmp_path):
     r = subprocess.run(["python", "-c", code, str(tmp_path)], capture_output=True, text=True, cwd=str(tmp_path))
     assert r.returncode == 3, (r.returncode, r.stdout, r.stderr)
     assert "libfgd.so is missing" in r.stdout
+
+
+def _tree_copy(tmp_path, with_lib):
+    """A copy of the package (sources, binding, optionally the built library and
+    its sidecar) and the header under tmp_path."""
+    import shutil
+    pkg = os.path.join(ROOT, "paper_2606_22768_amd")
+    dst = tmp_path / "paper_2606_22768_amd"
+    shutil.copytree(os.path.join(pkg, "csrc"), dst / "csrc")
+    for name in os.listdir(pkg):
+        if name.endswith(".py") or (with_lib and name in ("libfgd.so", "libfgd.so.json")):
+            shutil.copy(os.path.join(pkg, name), dst / name)
+    (tmp_path / "include").mkdir()
+    shutil.copy(os.path.join(ROOT, "include", "fgd.h"), tmp_path / "include" / "fgd.h")
+    return dst
+
+
+def test_library_carries_the_hashes_of_its_sources():
+    from paper_2606_22768_amd import build
+    want = build.source_hashes()
+    assert fgd.library_source_hash() == want
+    assert build.read_sidecar() == want
+    assert not build.needs_build()
+
+
+def test_stale_library_is_rebuilt_or_refused(tmp_path):
+    """Editing a kernel source in a copy of the tree marks the copied library
+    stale for ensure_built (which then rebuilds) and makes the binding refuse
+    to load it; the unedited copy is accepted."""
+    from paper_2606_22768_amd import build
+    dst = _tree_copy(tmp_path, with_lib=True)
+    lib = str(dst / "libfgd.so")
+    assert not build.needs_build(lib, str(tmp_path))
+    code = ("import sys; sys.path.insert(0, sys.argv[1])\n"
+            "try:\n    import paper_2606_22768_amd\nexcept ImportError as e:\n    print('refused:', e); sys.exit(3)\n"
+            "print('loaded'); sys.exit(0)\n")
+    r = subprocess.run(["python", "-c", code, str(tmp_path)], capture_output=True, text=True, cwd=str(tmp_path))
+    assert r.returncode == 0 and "loaded" in r.stdout, (r.stdout, r.stderr)
+    with open(dst / "csrc" / "kernels.hpp", "a") as f:
+        f.write("\n// edited\n")
+    assert build.needs_build(lib, str(tmp_path))
+    assert build.source_hashes(str(tmp_path))["step"] != build.source_hashes()["step"]
+    r = subprocess.run(["python", "-c", code, str(tmp_path)], capture_output=True, text=True, cwd=str(tmp_path))
+    assert r.returncode == 3, (r.returncode, r.stdout, r.stderr)
+    assert "built from other sources" in r.stdout
+    os.remove(dst / "libfgd.so.json")
+    with open(dst / "csrc" / "kernels.hpp", "rb") as f:
+        text = f.read()
+    with open(dst / "csrc" / "kernels.hpp", "wb") as f:
+        f.write(text.replace(b"\n// edited\n", b""))
+    assert build.needs_build(lib, str(tmp_path))  # no record of what it was built from
+
+
+@pytest.mark.parametrize("call", ["outer_step", "mix1", "outer_step_blocking", "consensus_distance"])
+def test_consensus_outputs_are_checked_before_any_launch(call):
+    """The kernels write rows x M doubles through the raw cd_out / out pointer,
+    so the wrapper refuses a buffer of another dtype, a smaller one, a
+    non-contiguous one or one off the engine's device before calling the C
+    ABI (a host-only engine: any call that got through would fail there)."""
+    import torch
+    M, P = 8, 64
+    eng = fgd.Engine(M, P, P, "f32", device=-1)
+    eng.set_topology("mix1", "global")
+    rp, ci, w = graphs.ring_weights(M)
+    eng.set_topology("mix2", "csr", rp, ci, w, rounds=2)
+    rows = {"outer_step": eng.num_cd_rows(), "mix1": eng.num_cd_rows_split()[0],
+            "outer_step_blocking": eng.num_cd_rows_split()[1], "consensus_distance": 1}[call]
+    a = torch.zeros((M, P))
+
+    def run(out):
+        if call == "outer_step":
+            eng.outer_step(a, a, a, out)
+        elif call == "mix1":
+            eng.mix1(a, a, None, out)
+        elif call == "outer_step_blocking":
+            eng.outer_step_blocking(a, a, a, a, out)
+        else:
+            eng.consensus_distance(a, out)
+
+    with pytest.raises(TypeError, match="float64"):
+        run(torch.zeros(rows * M, dtype=torch.float32))
+    with pytest.raises(ValueError, match="needs at least"):
+        run(torch.zeros(rows * M - 1, dtype=torch.float64))
+    with pytest.raises(ValueError, match="contiguous"):
+        run(torch.zeros((M, 2 * rows), dtype=torch.float64)[:, ::2])
+    with pytest.raises(ValueError, match="cuda"):
+        run(torch.zeros((rows, M), dtype=torch.float64))
+    eng.close()

@@ -26,10 +26,11 @@ def test_more_than_one_gpu_is_refused(argv, env):
 
 @pytest.fixture()
 def tree(tmp_path, monkeypatch):
-    """A copy of the HIP sources under a temporary root that bench.py reads."""
-    src = os.path.join(ROOT, "paper_2606_22768_amd", "csrc")
-    dst = tmp_path / "paper_2606_22768_amd" / "csrc"
-    shutil.copytree(src, dst)
+    """A copy of the library sources and header under a temporary root that
+    bench.py and the build's hash read."""
+    shutil.copytree(os.path.join(ROOT, "paper_2606_22768_amd", "csrc"), tmp_path / "paper_2606_22768_amd" / "csrc")
+    (tmp_path / "include").mkdir()
+    shutil.copy(os.path.join(ROOT, "include", "fgd.h"), tmp_path / "include" / "fgd.h")
     (tmp_path / "profiles").mkdir()
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     return tmp_path
@@ -40,29 +41,39 @@ def _touch(tree, name):
     p.write_text(p.read_text() + "\n// edited\n")
 
 
+def _hashes(tree):
+    from paper_2606_22768_amd import build
+    return build.source_hashes(str(tree))
+
+
 def test_component_hashes_cover_their_sources(tree):
-    step0, js0 = bench.kernel_source_hash("step"), bench.kernel_source_hash("js")
-    assert step0 != js0
+    h0 = _hashes(tree)
+    assert h0["step"] != h0["js"]
     _touch(tree, "js.hip")
-    step1, js1 = bench.kernel_source_hash("step"), bench.kernel_source_hash("js")
-    assert step1 == step0 and js1 != js0           # the JS kernels are not part of the step
+    h1 = _hashes(tree)
+    assert h1["step"] == h0["step"] and h1["js"] != h0["js"] and h1["all"] != h0["all"]  # JS is not the step
     _touch(tree, "engine.hip")
-    step2, js2 = bench.kernel_source_hash("step"), bench.kernel_source_hash("js")
-    assert step2 != step1 and js2 == js1           # launch code belongs to the step only
+    h2 = _hashes(tree)
+    assert h2["step"] != h1["step"] and h2["js"] == h1["js"]  # launch code belongs to the step only
     _touch(tree, "kernels.hpp")
-    assert bench.kernel_source_hash("step") != step2 and bench.kernel_source_hash("js") != js2
+    h3 = _hashes(tree)
+    assert h3["step"] != h2["step"] and h3["js"] != h2["js"]
+    _touch(tree, "topology.cpp")
+    h4 = _hashes(tree)
+    assert h4["step"] == h3["step"] and h4["all"] != h3["all"]  # host code: only the whole library
 
 
-def test_traffic_applies_only_to_the_sources_it_was_taken_on(tree):
+def test_traffic_applies_only_to_the_library_it_was_taken_with(tree):
     wl, algo = "m8_p1100m_bf16", 123_200_000_000
-    assert bench.read_traffic(wl, algo) is None    # no summary
-    summary = {"kernel_source_hash": bench.kernel_source_hash("step"), "fetch_bytes_per_launch": 70_400_000_000,
+    step = _hashes(tree)["step"]
+    assert bench.read_traffic(wl, algo, step) is None    # no summary
+    summary = {"kernel_source_hash": step, "fetch_bytes_per_launch": 70_400_000_000,
                "write_bytes_per_launch": 52_800_000_000}
     path = tree / "profiles" / f"traffic_fused_step_{wl}.json"
     path.write_text(json.dumps(summary))
-    t = bench.read_traffic(wl, algo)
+    t = bench.read_traffic(wl, algo, step)
     assert t["total_bytes"] == algo and t["ratio_to_algorithmic"] == pytest.approx(1.0)
-    _touch(tree, "js.hip")                         # a JS edit leaves the step's counters valid
-    assert bench.read_traffic(wl, algo) is not None
-    _touch(tree, "kernels_bf16.hip")               # a step edit voids them
-    assert bench.read_traffic(wl, algo) is None
+    _touch(tree, "js.hip")                               # a JS edit leaves the step's counters valid
+    assert bench.read_traffic(wl, algo, _hashes(tree)["step"]) is not None
+    _touch(tree, "kernels_bf16.hip")                     # a library of edited step sources voids them
+    assert bench.read_traffic(wl, algo, _hashes(tree)["step"]) is None
