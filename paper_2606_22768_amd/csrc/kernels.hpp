@@ -526,12 +526,30 @@ __device__ inline void keep_own(float (&u)[MMAX][V], const float *rows, int tid,
     }
 }
 
+// Consensus row of a global-mean output: every worker holds the mean, so
+// S_m = sum_p (mean_p - mean_p)^2 is 0 where the mean is finite and NaN
+// where it is not (IEEE: inf - inf and NaN - NaN are NaN).  Only that case
+// needs work: when some lane's mean is non-finite the wave's accumulators
+// of the row become NaN for every worker.
+template <int V>
+__device__ inline void cd_global_row(const float (&mean)[V], int M, double *acc, int lane) {
+    bool bad = false;
+#pragma unroll
+    for (int v = 0; v < V; ++v) bad |= !__builtin_isfinite(mean[v]);
+    if (__builtin_amdgcn_ballot_w64(bad)) {
+        for (int m = lane; m < M; m += kWave) acc[m] = __builtin_nan("");
+    }
+}
+
 // keep: bit v set = element v of this lane is outside the Mix's subset and
 // passes through unchanged (0 for a Mix over every element).
 template <int MMAX, bool EXACT, int V, int KIND>
 __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], const float (&mean)[V], float *rows,
                                  int tid, double *cd_acc, int cd_stride, int lane, uint32_t keep) {
-    if constexpr (KIND == kIdentity || KIND == kGlobal) {
+    if constexpr (KIND == kIdentity) {
+        return;
+    } else if constexpr (KIND == kGlobal) {
+        if (cd_acc) cd_global_row<V>(mean, M, cd_acc, lane);
         return;
     } else {
         if (KIND == kAny && mx.kind == kGlobal) {
@@ -539,7 +557,9 @@ __device__ inline void mix_apply(const MixDev &mx, int M, float (&u)[MMAX][V], c
             for (int m = 0; m < MMAX; ++m)
 #pragma unroll
                 for (int v = 0; v < V; ++v) u[m][v] = mean[v];
-            return;  // every row equal: the consensus row stays 0 (subsets need a table Mix)
+            // Every row equal (subsets need a table Mix).
+            if (cd_acc) cd_global_row<V>(mean, M, cd_acc, lane);
+            return;
         }
         if (KIND == kAny && mx.kind != kTable) return;
         const int Mr = EXACT ? MMAX : M;
