@@ -256,6 +256,27 @@ fgd_status fgd_min_bytes_split(const fgd_engine *e, int32_t write_local, int64_t
  * (Sec. 4.4; Appendix D.1). */
 fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, double *out, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP stream
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * S_m as fgd_consensus_distance, with no engine and no allocation.  Its
+ * block partials live in a static device array of the library, 2048 blocks
+ * x FGD_MAX_WORKERS doubles (1 MiB), held on every device it runs on until
+ * the process ends; the first call on a device resolves that array's
+ * address (hipGetSymbolAddress) and no call allocates or frees anything.
+ *   num_workers  M in [1, FGD_MAX_WORKERS]; larger M is rejected
+ *                (FGD_ERR_INVALID_ARG): the array holds 64 workers per block
+ *   num_params   P >= 0; ld >= P, ld * elem_size a multiple of 16
+ *   x            device [M][ld] dtype, 16-byte aligned, read
+ *   out          device double[M], 8-byte aligned: S_m
+ * Runs on the caller's current device, enqueued on `stream`.  The grid and
+ * summation order are those of fgd_consensus_distance on the same device,
+ * so the two give the same bits.  Every call on one device shares the one
+ * array: calls that may overlap on that device (different streams, or
+ * threads) race and must be ordered by the caller.  Each call writes every
+ * partial it reads, so nothing needs clearing between calls. */
+fgd_status fgd_consensus_distance_noalloc(int32_t num_workers, int64_t num_params, int64_t ld, int32_t dtype,
+                                          const void *x, double *out, void *stream);
+
 /* Effective float weights of one round of one slot, in the slot's CSR entry
  * order (dropped entries read 0).  out: host float[nnz]. */
 fgd_status fgd_get_effective_weights(const fgd_engine *e, int32_t which, int32_t round, float *out);

@@ -70,6 +70,7 @@ def _load():
         "fgd_num_cd_rows_split": (I32, [P, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
         "fgd_min_bytes_split": (I32, [P, I32, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
         "fgd_consensus_distance": (I32, [P, P, I32, P, P]),
+        "fgd_consensus_distance_noalloc": (I32, [I32, I64, I64, I32, P, P, P]),
         "fgd_get_effective_weights": (I32, [P, I32, I32, P]),
         "fgd_effective_weights": (I32, [I32, P, P, P, P, I32, P]),
         "fgd_min_bytes_per_step": (I32, [P, ctypes.POINTER(I64)]),
@@ -230,6 +231,11 @@ def fgd_min_bytes_split(h, write_local=False):
 def fgd_consensus_distance(h, x, dtype, out, stream=None):
     _check(lib.fgd_consensus_distance(h, _dev(x), DTYPES.get(dtype, dtype), _dev(out), _stream(stream)),
            "fgd_consensus_distance")
+
+
+def fgd_consensus_distance_noalloc(num_workers, num_params, ld, dtype, x, out, stream=None):
+    _check(lib.fgd_consensus_distance_noalloc(int(num_workers), int(num_params), int(ld), DTYPES.get(dtype, dtype),
+                                              _dev(x), _dev(out), _stream(stream)), "fgd_consensus_distance_noalloc")
 
 
 def fgd_get_effective_weights(h, which, rnd, nnz):

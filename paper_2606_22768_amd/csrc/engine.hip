@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -208,7 +209,8 @@ int64_t tiles_of(int64_t P, int v) {
     return (P + per - 1) / per;
 }
 
-fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntiles, int &grid, int cap = kMaxBlocksPerCu) {
+fgd_status grid_for_cus(int num_cus, const void *kernel, size_t lds, int64_t ntiles, int &grid,
+                        int cap = kMaxBlocksPerCu) {
     int per_cu = 0;
     if (lds > 65536) {
         hipError_t err = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
@@ -218,9 +220,13 @@ fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntile
     if (err != hipSuccess) return hip_fail(err, "occupancy query");
     if (per_cu < 1) return fail(FGD_ERR_UNSUPPORTED, "kernel does not fit on a compute unit (LDS %zu bytes)", lds);
     per_cu = std::min(per_cu, std::min(cap, kMaxBlocksPerCu));
-    const int64_t g = std::min<int64_t>(static_cast<int64_t>(per_cu) * e->num_cus, std::max<int64_t>(ntiles, 1));
+    const int64_t g = std::min<int64_t>(static_cast<int64_t>(per_cu) * num_cus, std::max<int64_t>(ntiles, 1));
     grid = static_cast<int>(g);
     return FGD_OK;
+}
+
+fgd_status grid_for(fgd_engine *e, const void *kernel, size_t lds, int64_t ntiles, int &grid, int cap = kMaxBlocksPerCu) {
+    return grid_for_cus(e->num_cus, kernel, lds, ntiles, grid, cap);
 }
 
 fgd_status launch(const void *kernel, int grid, size_t lds, hipStream_t stream, void *arg) {
@@ -291,6 +297,56 @@ bool rows_overlap(const fgd_engine *e, const void *a, int ea, const void *b, int
     span(a, c.num_workers, c.ld, c.num_params, ea, a0, a1);
     span(b, c.num_workers, c.ld, c.num_params, eb, b0, b1);
     return overlap(a0, a1, b0, b1);
+}
+
+}  // namespace
+
+// ------------------------------------------- consensus without allocation
+//
+// fgd_consensus_distance_noalloc keeps its per-block partials in this array
+// instead of engine memory: 2048 blocks (256 compute units x 8 resident
+// blocks) x FGD_MAX_WORKERS doubles, 1 MiB on every device the library runs
+// on, held until the process ends.  Host code never uses the name itself
+// (on the host it is only a stand-in for the symbol): its device address is
+// taken once per device with hipGetSymbolAddress and kept below.
+namespace {
+constexpr int kNoAllocBlocks = 2048;
+constexpr int kNoAllocDoubles = kNoAllocBlocks * FGD_MAX_WORKERS;
+constexpr int kNoAllocDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) double scratch[kNoAllocDoubles];
+
+namespace {
+
+struct NoAllocDevice {
+    bool ready = false;
+    double *ptr = nullptr;  // device address of `scratch` on this device
+    int num_cus = 0;
+};
+std::mutex g_noalloc_mutex;
+NoAllocDevice g_noalloc[kNoAllocDevices];
+
+// The scratch address and compute-unit count of the current device `dev`,
+// resolved on the first call for that device (with it current).
+fgd_status noalloc_device(int dev, double *&ptr, int &num_cus) {
+    if (dev < 0 || dev >= kNoAllocDevices) return fail(FGD_ERR_UNSUPPORTED, "device %d is beyond %d", dev, kNoAllocDevices);
+    std::lock_guard<std::mutex> lock(g_noalloc_mutex);
+    NoAllocDevice &d = g_noalloc[dev];
+    if (!d.ready) {
+        void *p = nullptr;
+        hipError_t err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return hip_fail(err, "resolving the static consensus scratch");
+        int cus = 0;
+        err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (err != hipSuccess) return hip_fail(err, "querying the compute-unit count");
+        d.ptr = static_cast<double *>(p);
+        d.num_cus = cus;
+        d.ready = true;
+    }
+    ptr = d.ptr;
+    num_cus = d.num_cus;
+    return FGD_OK;
 }
 
 }  // namespace
@@ -796,6 +852,43 @@ fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, d
         return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
     if (fgd_status st = launch(ks.consensus, grid, 0, stream, &p)) return st;
     return launch_finalize(e->d_partials, grid, c.num_workers, out, stream);
+}
+
+fgd_status fgd_consensus_distance_noalloc(int32_t num_workers, int64_t num_params, int64_t ld, int32_t dtype,
+                                          const void *x, double *out, void *stream_handle) {
+    g_last_error.clear();
+    if (num_workers < 1 || num_workers > FGD_MAX_WORKERS)
+        return fail(FGD_ERR_INVALID_ARG, "num_workers %d is outside [1, %d] (the static scratch holds %d blocks of %d)",
+                    num_workers, FGD_MAX_WORKERS, kNoAllocBlocks, FGD_MAX_WORKERS);
+    if (num_params < 0 || ld < num_params) return fail(FGD_ERR_INVALID_ARG, "need 0 <= num_params <= ld");
+    if (dtype != FGD_F32 && dtype != FGD_BF16) return fail(FGD_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+    if (!x || !out) return fail(FGD_ERR_INVALID_ARG, "NULL device array");
+    if (!aligned16(x)) return fail(FGD_ERR_INVALID_ARG, "x must be 16-byte aligned");
+    if ((ld * elem_size(dtype)) % 16 != 0) return fail(FGD_ERR_INVALID_ARG, "ld * elem_size must be a multiple of 16");
+    if (reinterpret_cast<uintptr_t>(out) & 7u) return fail(FGD_ERR_INVALID_ARG, "out must be 8-byte aligned");
+    fgd::KernelSet ks;
+    if (!lookup(num_workers, dtype, 0, 0, false, false, ks)) return fail(FGD_ERR_UNSUPPORTED, "no kernel for M=%d", num_workers);
+    int dev = 0;
+    hipError_t herr = hipGetDevice(&dev);
+    if (herr != hipSuccess) return hip_fail(herr, "querying the current device");
+    double *partials = nullptr;
+    int num_cus = 0;
+    if (fgd_status st = noalloc_device(dev, partials, num_cus)) return st;
+    fgd::ConsensusParams p{};
+    p.x = x;
+    p.P = num_params;
+    p.ld = ld;
+    p.ntiles = tiles_of(num_params, ks.v);
+    p.M = num_workers;
+    p.partials = partials;
+    int grid = 0;
+    if (fgd_status st = grid_for_cus(num_cus, ks.consensus, 0, p.ntiles, grid)) return st;
+    // The grid of fgd_consensus_distance (so the same sums in the same
+    // order), capped to the blocks the scratch holds on a larger device.
+    grid = std::min(grid, kNoAllocDoubles / num_workers);
+    hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    if (fgd_status st = launch(ks.consensus, grid, 0, stream, &p)) return st;
+    return launch_finalize(partials, grid, num_workers, out, stream);
 }
 
 fgd_status fgd_enable_timing(fgd_engine *e, int32_t enable) {

@@ -473,3 +473,17 @@ def test_consensus_outputs_are_checked_before_any_launch(call):
     with pytest.raises(ValueError, match="cuda"):
         run(torch.zeros((rows, M), dtype=torch.float64))
     eng.close()
+
+
+def test_noalloc_consensus_rejects_arguments_before_any_device_call():
+    """The scratch-free consensus call checks its arguments first: more workers
+    than its static scratch holds, bad sizes, dtype or alignment."""
+    L = fgd.lib
+    assert L.fgd_consensus_distance_noalloc(65, 16, 16, 0, 256, 256, None) == fgd.FGD_ERR_INVALID_ARG
+    assert "num_workers 65" in fgd.fgd_last_error()
+    assert L.fgd_consensus_distance_noalloc(0, 16, 16, 0, 256, 256, None) == fgd.FGD_ERR_INVALID_ARG
+    assert L.fgd_consensus_distance_noalloc(4, 17, 16, 0, 256, 256, None) == fgd.FGD_ERR_INVALID_ARG
+    assert L.fgd_consensus_distance_noalloc(4, 16, 16, 7, 256, 256, None) == fgd.FGD_ERR_INVALID_ARG
+    assert L.fgd_consensus_distance_noalloc(4, 16, 16, 0, 264, 256, None) == fgd.FGD_ERR_INVALID_ARG
+    assert L.fgd_consensus_distance_noalloc(4, 16, 16, 0, 256, 260, None) == fgd.FGD_ERR_INVALID_ARG
+    assert L.fgd_consensus_distance_noalloc(4, 6, 6, 0, 256, 256, None) == fgd.FGD_ERR_INVALID_ARG  # 24-byte rows
