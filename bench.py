@@ -168,6 +168,103 @@ def js_bench(args, fgd, torch):
     print(json.dumps(out))
 
 
+def copy_reference(fgd, torch, dev, gb):
+    """GB/s of a plain 16-byte streaming copy of `gb` GB (read and written),
+    the practical streaming ceiling and the size reference against which the
+    HBM traffic counters are calibrated; None for gb <= 0."""
+    if gb <= 0:
+        return None
+    n = int(gb * 1e9) // 16 * 16
+    a = torch.empty(n, dtype=torch.uint8, device=dev)
+    b = torch.empty(n, dtype=torch.uint8, device=dev)
+    fgd.fgd_stream_copy(b, a, n)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        fgd.fgd_stream_copy(b, a, n)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    return round(gbs, 1)
+
+
+def consensus_bench(args, fgd, torch, w):
+    """Standalone consensus distance (Sec. 4.4; Appendix D.1): S_m of the
+    workload's theta_prev, resident in HBM; a step is one
+    fgd_consensus_distance call (the streaming kernel and its finalize).  The
+    scratch-free variant is timed beside it on the same array."""
+    from synth import tensors
+
+    M, P, dtype = w["M"], w["P"], w["dtype"]
+    ld = -(-P // 8) * 8
+    es = 2 if dtype == "bf16" else 4
+    dev = torch.device("cuda:0")
+    print(f"[bench] consensus: generating {args.workload} theta_prev", file=sys.stderr, flush=True)
+    tp, tl, v = tensors.torch_inputs(M, P, ld=ld, dtype=dtype, prev_std=w["prev_std"], drift_std=w["drift_std"],
+                                     mom_std=0.0, seed=w["seed"], device=dev)
+    del tl, v
+    eng = fgd.Engine(M, P, ld, dtype, device=0)
+    out = torch.zeros(M, dtype=torch.float64, device=dev)
+    out2 = torch.zeros(M, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        t0 = time.perf_counter()
+        ev[0].record(stream)
+        for i in range(args.steps):
+            fn()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return wall, sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+
+    wall, ms = timed(lambda: eng.consensus_distance(tp, out, stream))
+    _, ms2 = timed(lambda: fgd.fgd_consensus_distance_noalloc(M, P, ld, dtype, tp, out2, stream))
+    nbytes = M * P * es
+    avg = sum(ms) / len(ms)
+    achieved = nbytes / (avg * 1e-3) / 1e9
+    res = {"metric": "standalone consensus distance: HBM GB/s and % of MI355X HBM peak", "mode": "consensus",
+           "value": round(nbytes * args.steps / wall / 1e9, 2), "unit": "GB/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
+           "step_ms_median": round(ms[len(ms) // 2], 4), "step_ms_min": round(ms[0], 4),
+           "higher_is_better": True, "dtype": "f32", "storage_dtype": dtype, "data": "synthetic",
+           "config": {"workload": args.workload, "workers": M, "params_per_worker": P,
+                      "what": "S_m = sum_p (x_m,p - mean_n x_n,p)^2 of theta_prev", "bytes_per_call": nbytes},
+           "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(achieved / HBM_PEAK_GBS, 4),
+                        "traffic": None, "kernel": "consensus_kernel + finalize_kernel (one call)",
+                        "kernel_avg_ms": round(avg, 4), "bytes_per_launch": nbytes},
+           "noalloc_ms_median": round(ms2[len(ms2) // 2], 4),
+           "copy_reference_gbs": copy_reference(fgd, torch, dev, args.copy_gb),
+           "noalloc_same_bits": bool(torch.equal(out, out2)),
+           "kernel_source_hash": fgd.library_source_hash()["step"], "library_source_hash": fgd.library_source_hash()}
+    t = read_traffic(args.workload, nbytes, fgd.library_source_hash()["step"], kernel="consensus")
+    if t is not None:
+        res["roofline"]["traffic"] = t["total_bytes"]
+        res["roofline"]["traffic_detail"] = t
+    if not args.no_cpu_baseline:
+        import oracle
+
+        p_slice = min(P, (1 << 27) // M)
+        h = tp[:, :p_slice].contiguous()
+        h = h.view(torch.int16).cpu().numpy().view("uint16") if dtype == "bf16" else h.cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.consensus(h, P=p_slice, dtype=dtype)
+        dt = time.perf_counter() - t0
+        model, ncpu = host_cpu()
+        res["cpu_baseline"] = {"value": round(M * p_slice * es / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+                               "kind": "oracle", "sample": f"first {p_slice} of {P} parameters x {M} workers, "
+                                                           f"{dt:.2f} s single-threaded",
+                               "host_cpu": model, "host_nproc": ncpu}
+    eng.close()
+    print(json.dumps(res))
+
+
 def split_round_bench(args, fgd, eng, torch, tp, tl, v, x, w, step_topos, placement):
     """Split execution of a round (Appendix A, Algorithm 1): the Mix1 half is
     launched on a side stream at the start of the round and overlaps a
@@ -218,6 +315,7 @@ def split_round_bench(args, fgd, eng, torch, tp, tl, v, x, w, step_topos, placem
     n_gemm = max(1, int(2.0 * t_mix1 / t_gemm + 0.999))
     t_inner = timed(lambda i: [torch.matmul(A, B, out=C) for _ in range(n_gemm)], main_s, 5)
 
+    copy_gbs = copy_reference(fgd, torch, tp.device, args.copy_gb)
     print("[bench] split: overlapped rounds", file=sys.stderr, flush=True)
     rounds = []
     for r in range(args.steps):
@@ -238,6 +336,9 @@ def split_round_bench(args, fgd, eng, torch, tp, tl, v, x, w, step_topos, placem
     torch.cuda.synchronize()
     t_round = sorted(a.elapsed_time(b) for a, b in rounds)[len(rounds) // 2]
     exposed = max(0.0, t_round - t_inner - t_block)
+    lib_hash = fgd.library_source_hash()
+    tr1 = read_traffic(args.workload, b1, lib_hash["step"], kernel="split_mix1")
+    tr2 = read_traffic(args.workload, b2, lib_hash["step"], kernel="split_blocking")
     out = {
         "metric": "split outer step: Mix1 half hidden under the inner loop; blocking-half HBM GB/s",
         "mode": "split", "workload": args.workload, "steps": args.steps, "warmup": args.warmup,
@@ -252,10 +353,17 @@ def split_round_bench(args, fgd, eng, torch, tp, tl, v, x, w, step_topos, placem
         "config": {"workers": M, "params_per_worker": P, "dtype": w["dtype"], "write_back_theta_local": True,
                    "mix1_also_on_momentum": bool(w.get("mix1_state")), "placement": placement},
         "roofline": {"bound": "hbm", "achieved": round(b2 / (t_block * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(b2 / (t_block * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(b2 / (t_block * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None if tr2 is None else tr2["total_bytes"], "traffic_detail": tr2,
                      "kernel": "blocking half (stream time of the call: kernel and consensus finalize)",
                      "bytes_per_launch": b2},
-        "kernel_source_hash": fgd.library_source_hash()["step"], "library_source_hash": fgd.library_source_hash(),
+        "mix1_roofline": {"bound": "hbm", "achieved": round(b1 / (t_mix1 * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                          "unit": "GB/s", "frac": round(b1 / (t_mix1 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "traffic": None if tr1 is None else tr1["total_bytes"], "traffic_detail": tr1,
+                          "kernel": f"Mix1 half on {nb or 'one block per CU'} blocks (counter reset, kernel, "
+                                    f"finalize)", "bytes_per_launch": b1},
+        "copy_reference_gbs": copy_gbs,
+        "kernel_source_hash": lib_hash["step"], "library_source_hash": lib_hash,
     }
     print(json.dumps(out))
 
@@ -271,10 +379,11 @@ def main():
                          "about 12 s of single-threaded oracle work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
-    ap.add_argument("--mode", choices=["fused", "split", "js"], default="fused",
+    ap.add_argument("--mode", choices=["fused", "split", "js", "consensus"], default="fused",
                     help="fused: one-pass outer step (the benchmark); split: Mix1 half on a side stream "
                          "overlapping a stand-in inner loop, then the blocking half; js: Jensen-Shannon "
-                         "distance of 8 workers over 2048 tokens of a 128256-token vocabulary (bf16 logits)")
+                         "distance of 8 workers over 2048 tokens of a 128256-token vocabulary (bf16 logits); "
+                         "consensus: the standalone consensus distance of the workload's theta_prev")
     ap.add_argument("--placement", choices=["spread", "packed"], default="spread",
                     help="spread: the momentum one physical-memory range past the parameter arrays "
                          "(fgd_state_layout; packed when memory is short); packed: the arrays back to back")
@@ -304,6 +413,9 @@ def main():
         js_bench(args, fgd, torch)
         return
     w = configs.WORKLOADS[args.workload]
+    if args.mode == "consensus":
+        consensus_bench(args, fgd, torch, w)
+        return
     M, P, dtype = w["M"], w["P"], w["dtype"]
     ld = -(-P // 8) * 8
     dev = torch.device("cuda:0")
@@ -415,21 +527,7 @@ def main():
         torch.cuda.synchronize()
         pattern_ms = e0.elapsed_time(e1) / 5
 
-    # Plain copy reference (practical streaming ceiling), timed with torch events.
-    copy_gbs = None
-    if args.copy_gb > 0:
-        n = int(args.copy_gb * 1e9) // 16 * 16
-        a = torch.empty(n, dtype=torch.uint8, device=dev)
-        b = torch.empty(n, dtype=torch.uint8, device=dev)
-        fgd.fgd_stream_copy(b, a, n)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(5):
-            fgd.fgd_stream_copy(b, a, n)
-        e1.record()
-        torch.cuda.synchronize()
-        copy_gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-        del a, b
+    copy_gbs = copy_reference(fgd, torch, dev, args.copy_gb)
 
     lib_hash = fgd.library_source_hash()
     traffic = read_traffic(args.workload, bytes_step, lib_hash["step"])  # counters of this library's sources
