@@ -241,6 +241,20 @@ fgd_status fgd_mix1(fgd_engine *e, const void *theta_prev, void *x_out, float *m
 fgd_status fgd_outer_step_blocking(fgd_engine *e, const void *x, void *theta_prev, void *theta_local, float *momentum,
                                    double *cd_out, int32_t write_local, void *stream);
 
+/* Which kernel fgd_outer_step launches for the engine's current topology.
+ *   FGD_STEP_LANE_PER_PARAM  a lane holds V consecutive parameters of every
+ *                            worker (any M, every Mix kind and variant)
+ *   FGD_STEP_WORKER_GROUPS   64 workers: a lane holds 16 workers x 4
+ *                            parameters; chosen for a CSR Mix2 of at most 4
+ *                            rounds with a CSR (at most 2 rounds) or global
+ *                            Mix1, rows of at most 15 live entries, tables
+ *                            that fit in 80 KiB of LDS with the rows, no
+ *                            subset and no state mixing
+ * Both compute the same step to the same bars.  Needs both slots set. */
+#define FGD_STEP_LANE_PER_PARAM 0
+#define FGD_STEP_WORKER_GROUPS 1
+fgd_status fgd_step_variant(const fgd_engine *e, int32_t *variant);
+
 /* Consensus rows of the two halves: K1 + 1 and K2 + 2 (GLOBAL_MEAN counts as
  * one round, IDENTITY as zero).  Needs both slots set. */
 fgd_status fgd_num_cd_rows_split(const fgd_engine *e, int32_t *mix1_rows, int32_t *blocking_rows);

@@ -64,6 +64,7 @@ def _load():
         "fgd_set_topology": (I32, [P, I32, I32, P, P, P, I32, P, I32]),
         "fgd_set_mix2_subset": (I32, [P, P, I32]),
         "fgd_num_cd_rows": (I32, [P, ctypes.POINTER(I32)]),
+        "fgd_step_variant": (I32, [P, ctypes.POINTER(I32)]),
         "fgd_outer_step": (I32, [P, P, P, P, P, P]),
         "fgd_mix1": (I32, [P, P, P, P, P, I32, P]),
         "fgd_outer_step_blocking": (I32, [P, P, P, P, P, P, I32, P]),
@@ -196,6 +197,15 @@ def fgd_set_mix2_subset(h, segments=None):
 def fgd_num_cd_rows(h) -> int:
     n = ctypes.c_int32()
     _check(lib.fgd_num_cd_rows(h, ctypes.byref(n)), "fgd_num_cd_rows")
+    return n.value
+
+
+FGD_STEP_LANE_PER_PARAM, FGD_STEP_WORKER_GROUPS = 0, 1
+
+
+def fgd_step_variant(h) -> int:
+    n = ctypes.c_int32()
+    _check(lib.fgd_step_variant(h, ctypes.byref(n)), "fgd_step_variant")
     return n.value
 
 
@@ -363,6 +373,10 @@ class Engine:
 
     def num_cd_rows(self):
         return fgd_num_cd_rows(self.handle)
+
+    def step_variant(self):
+        """"worker-groups" or "lane-per-param": the kernel fgd_outer_step launches."""
+        return "worker-groups" if fgd_step_variant(self.handle) == FGD_STEP_WORKER_GROUPS else "lane-per-param"
 
     def _check_rows(self, t, name, dtype):
         import torch

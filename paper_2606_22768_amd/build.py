@@ -30,7 +30,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libfgd.so")
 
 HIP_SOURCES = ["engine.hip", "kernels_f32.hip", "kernels_bf16.hip", "kernels_f32_ms.hip", "kernels_bf16_ms.hip",
-               "kernels_f32_split.hip", "kernels_bf16_split.hip", "kernels_common.hip", "js.hip"]
+               "kernels_f32_split.hip", "kernels_bf16_split.hip", "kernels_wg.hip", "kernels_common.hip",
+               "js.hip"]
 CXX_SOURCES = ["topology.cpp"]
 
 ARCH = "gfx950"

@@ -14,6 +14,7 @@
 
 #include "../../include/fgd.h"
 #include "kernels.hpp"
+#include "kernels_wg.hpp"
 #include "topology.hpp"
 
 namespace {
@@ -75,6 +76,8 @@ constexpr int kTopoRing = 8;
 constexpr int kMaxBlocksPerCu = FGD_MAX_BLOCKS_PER_CU;
 constexpr int kTimingPool = 4096;
 constexpr int64_t kMix1Chunks = 4096;  // chunks the Mix1 half's tiles are cut into (at most)
+// LDS of a worker-group step block: two blocks share a compute unit's 160 KiB.
+constexpr size_t kWgMaxLds = 80 * 1024;
 
 }  // namespace
 
@@ -284,6 +287,27 @@ int32_t lds_rows_for(const fgd_engine *e, bool use1, bool use2) {
     const bool t1 = use1 && e->slot[0].kind == 2, t2 = use2 && e->slot[1].kind == 2;
     const bool padded = (t1 && e->slot[0].padded) || (t2 && e->slot[1].padded);
     return (t1 || t2) ? e->cfg.num_workers + (padded ? 1 : 0) : 0;
+}
+
+// Whether the 64-worker worker-group kernel serves this engine's step (a
+// CSR Mix2, a CSR or global Mix1, sparse tables that fit in LDS beside the
+// rows, no subset, no state mixing, per-lane row offsets below 2^32 bytes);
+// if so its LDS bytes and rows per wave.
+bool wg_step_fits(const fgd_engine *e, fgd::WgKernel &k, size_t &lds, int &wave_rows) {
+    const fgd_config &c = e->cfg;
+    const fgd::MixTopology &s1 = e->slot[0], &s2 = e->slot[1];
+    if (c.num_workers != fgd::kWgWorkers || !e->subset.empty() || c.mix1_state) return false;
+    if (s2.kind != 2 || s2.rounds > fgd::kWgR2 || s2.width > fgd::kWgMaxWidth) return false;
+    if (s1.kind == 2 && (s1.rounds > fgd::kWgR1 || s1.width > fgd::kWgMaxWidth)) return false;
+    if (!fgd::wg_kernel(c.param_dtype == FGD_BF16, s1.kind, s2.kind, &k)) return false;
+    const int64_t es = elem_size(c.param_dtype);
+    if ((3 * c.ld + fgd::kWgTile) * std::max<int64_t>(es, 4) + 64 > int64_t{0xFFFFFFFF}) return false;
+    const bool padded = (s1.kind == 2 && s1.padded) || s2.padded;
+    wave_rows = fgd::kWgWorkers + (padded ? 1 : 0);
+    const size_t entries = static_cast<size_t>(s1.kind == 2 ? s1.rounds * s1.width : 0) * fgd::kWgWorkers +
+                           static_cast<size_t>(s2.rounds) * s2.width * fgd::kWgWorkers;
+    lds = static_cast<size_t>(fgd::kWavesPerBlock) * wave_rows * fgd::kWgRowBytes + entries * sizeof(int2);
+    return lds <= kWgMaxLds;
 }
 
 // Checks a device [M][ld] array: non-NULL and 16-byte aligned.
@@ -658,12 +682,45 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     size_t lds = static_cast<size_t>(p.lds_rows) * fgd::kBlock * ks.v * sizeof(float);
     if (cd_out) lds += static_cast<size_t>(p.n_cd) * fgd::kWavesPerBlock * ks.mmax * sizeof(double);
 
+    // 64 workers on sparse tables: the worker-group kernel.
+    fgd::WgKernel wk{};
+    size_t wg_lds = 0;
+    int wave_rows = 0;
+    const bool wg = wg_step_fits(e, wk, wg_lds, wave_rows);
+    fgd::WgParams wp{};
+    const void *kernel = ks.step;
+    void *args = &p;
+    if (wg) {
+        wp.theta_prev = theta_prev;
+        wp.theta_out = theta_prev;
+        wp.theta_local = theta_local;
+        wp.mom = momentum;
+        wp.mom_out = momentum;
+        wp.P = c.num_params;
+        wp.ld = c.ld;
+        wp.ntiles = (c.num_params + fgd::kWgTile - 1) / fgd::kWgTile;
+        wp.n_cd = p.n_cd;
+        wp.wave_rows = wave_rows;
+        wp.nesterov = c.nesterov;
+        wp.lr = c.outer_lr;
+        wp.mu = c.momentum;
+        wp.rows_bytes = fgd::kWavesPerBlock * wave_rows * fgd::kWgRowBytes;
+        const fgd::MixTopology &s1 = e->slot[0], &s2 = e->slot[1];
+        wp.mix1 = fgd::WgMix{s1.kind, s1.rounds, s1.width, 0, static_cast<const int2 *>(t1)};
+        wp.mix2 = fgd::WgMix{s2.kind, s2.rounds, s2.width, s1.kind == 2 ? s1.rounds * s1.width * fgd::kWgWorkers : 0,
+                             static_cast<const int2 *>(t2)};
+        kernel = wk.step;
+        lds = wg_lds;
+        args = &wp;
+    }
     int grid = 0;
-    if (fgd_status st = grid_for(e, ks.step, lds, p.ntiles, grid, ks.step_blocks_per_cu)) return st;
+    if (fgd_status st = grid_for(e, kernel, lds, wg ? wp.ntiles : p.ntiles, grid, wg ? kMaxBlocksPerCu : ks.step_blocks_per_cu))
+        return st;
     if (cd_out) {
         if (static_cast<size_t>(grid) * p.n_cd * c.num_workers > e->partials_capacity)
             return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
         p.cd_partials = e->d_partials;
+        wp.cd_partials = e->d_partials;
     }
 
     const bool timed = e->timing && e->timed < kTimingPool;
@@ -679,7 +736,7 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
         herr = hipEventRecord(e->ev_start[e->timed], stream);
         if (herr != hipSuccess) return hip_fail(herr, "recording a timing event");
     }
-    if (fgd_status st = launch(ks.step, grid, lds, stream, &p)) return st;
+    if (fgd_status st = launch(kernel, grid, lds, stream, args)) return st;
     if (timed) {
         herr = hipEventRecord(e->ev_stop[e->timed], stream);
         if (herr != hipSuccess) return hip_fail(herr, "recording a timing event");
@@ -689,6 +746,17 @@ fgd_status fgd_outer_step(fgd_engine *e, void *theta_prev, const void *theta_loc
     if (herr != hipSuccess) return hip_fail(herr, "recording the topology event");
     e->topo_pending[ring] = true;
     if (cd_out) return launch_finalize(e->d_partials, grid, p.n_cd * c.num_workers, cd_out, stream);
+    return FGD_OK;
+}
+
+fgd_status fgd_step_variant(const fgd_engine *e, int32_t *variant) {
+    if (fgd_status st = check_engine(e)) return st;
+    if (!variant) return fail(FGD_ERR_INVALID_ARG, "variant is NULL");
+    if (!e->slot_set[0] || !e->slot_set[1]) return fail(FGD_ERR_STATE, "both Mix slots must be set");
+    fgd::WgKernel k{};
+    size_t lds = 0;
+    int rows = 0;
+    *variant = wg_step_fits(e, k, lds, rows) ? FGD_STEP_WORKER_GROUPS : FGD_STEP_LANE_PER_PARAM;
     return FGD_OK;
 }
 

@@ -174,6 +174,9 @@ def topo(spec, M, rounds, seed=0, step=0):
     return configs.topology(spec, M, rounds, seed, step)
 
 
+last_variant = None  # the step kernel the last run_engine call launched (Engine.step_variant)
+
+
 def run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd=True, lr=0.7, mu=0.9, nesterov=True,
                mix1_state=False, subset=None):
     """One step on the GPU.  Inputs are numpy arrays; returns numpy copies of
@@ -196,6 +199,8 @@ def run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp, tl, v, with_cd=True, lr=
         cd = None
         if with_cd:
             cd = torch.full((eng.num_cd_rows(), M), float("nan"), dtype=torch.float64, device=dev)
+        global last_variant
+        last_variant = eng.step_variant()
         eng.outer_step(g_tp, g_tl, g_v, cd)
         torch.cuda.synchronize()
     finally:

@@ -487,3 +487,48 @@ def test_noalloc_consensus_rejects_arguments_before_any_device_call():
     assert L.fgd_consensus_distance_noalloc(4, 16, 16, 0, 264, 256, None) == fgd.FGD_ERR_INVALID_ARG
     assert L.fgd_consensus_distance_noalloc(4, 16, 16, 0, 256, 260, None) == fgd.FGD_ERR_INVALID_ARG
     assert L.fgd_consensus_distance_noalloc(4, 6, 6, 0, 256, 256, None) == fgd.FGD_ERR_INVALID_ARG  # 24-byte rows
+
+
+def _variant(M, t1, t2, dtype="f32", subset=None, mix1_state=False, P=4096):
+    from tests import _parity as pa
+    eng = fgd.Engine(M, P, P, dtype, device=-1, mix1_state=mix1_state)
+    eng.set_topology_dict("mix1", t1)
+    eng.set_topology_dict("mix2", t2)
+    if subset:
+        eng.set_mix2_subset(subset)
+    v = eng.step_variant()
+    eng.close()
+    return v
+
+
+def test_step_variant_choice():
+    """The worker-group kernel serves 64 workers on sparse CSR tables within
+    its round and LDS limits; everything else runs on the lane-per-parameter
+    kernel."""
+    from tests import _parity as pa
+    reg4, ring = ("regular", "metropolis", 4), ("ring", "metropolis", 0.1)
+    G = ("global",)
+    wg, lpp = "worker-groups", "lane-per-param"
+    assert _variant(64, pa.topo(reg4, 64, 1), pa.topo(reg4, 64, 3)) == wg            # LocalM1M2, 64 x 124M shape
+    assert _variant(64, pa.topo(reg4, 64, 1), pa.topo(reg4, 64, 3), "bf16") == wg
+    assert _variant(64, pa.topo(G, 64, 1), pa.topo(ring, 64, 4)) == wg               # GlobalM1LocalM2
+    assert _variant(64, pa.topo(reg4, 64, 2), pa.topo(reg4, 64, 4)) == wg            # the unrolled maxima
+    assert _variant(64, pa.topo(reg4, 64, 3), pa.topo(reg4, 64, 1)) == lpp           # Mix1 rounds beyond 2
+    assert _variant(64, pa.topo(reg4, 64, 1), pa.topo(reg4, 64, 5)) == lpp           # Mix2 rounds beyond 4
+    assert _variant(64, pa.topo(G, 64, 1), pa.topo(("complete",), 64, 1)) == lpp     # 64-entry rows
+    assert _variant(64, pa.topo(("identity",), 64, 0), pa.topo(reg4, 64, 1)) == lpp  # identity Mix1
+    assert _variant(64, pa.topo(G, 64, 1), pa.topo(G, 64, 1)) == lpp                 # no CSR Mix2
+    assert _variant(64, pa.topo(G, 64, 1), pa.topo(reg4, 64, 1), subset=[(0, 100)]) == lpp
+    assert _variant(64, pa.topo(G, 64, 1), pa.topo(reg4, 64, 1), mix1_state=True) == lpp
+    assert _variant(32, pa.topo(reg4, 32, 1), pa.topo(reg4, 32, 3)) == lpp
+    assert _variant(63, pa.topo(G, 63, 1), pa.topo(ring, 63, 1)) == lpp
+    # Rows of up to 15 entries are accepted: two rounds of such tables
+    # (15 KiB) beside 65 KiB of rows (a padded table adds a zero row per
+    # wave) fill the 80 KiB LDS budget of a block exactly; three exceed it.
+    dense = ("er_mh", 0.1, 0.0)
+    t = pa.topo(dense, 64, 1, seed=3)
+    assert np.diff(t["row_ptr"]).max() == 15
+    assert _variant(64, pa.topo(dense, 64, 1, seed=3), pa.topo(dense, 64, 1, seed=3)) == wg
+    assert _variant(64, pa.topo(dense, 64, 1, seed=3), pa.topo(dense, 64, 2, seed=3)) == lpp
+    assert _variant(64, pa.topo(G, 64, 1), pa.topo(dense, 64, 1, seed=3)) == wg
+    assert _variant(64, pa.topo(ring, 64, 2), pa.topo(ring, 64, 4)) == wg
