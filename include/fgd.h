@@ -391,8 +391,10 @@ fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, i
  * momentum are stored back with their own bits (the arrays are left exactly
  * as they were; a lane vector that straddles P is not stored).  Its rate is
  * the practical ceiling of the step's read/write mix on the arrays' placement.
- * Same arrays and rules as fgd_outer_step; M in {1, 2, 4, 8, 16, 32, 64}
- * (else FGD_ERR_UNSUPPORTED).  Enqueued on `stream`. */
+ * It follows the kernel fgd_outer_step would launch for the current
+ * topology (fgd_step_variant; the lane-per-parameter layout when the slots
+ * are not set).  Same arrays and rules as fgd_outer_step; M in {1, 2, 4, 8,
+ * 16, 32, 64} (else FGD_ERR_UNSUPPORTED).  Enqueued on `stream`. */
 fgd_status fgd_stream_step_pattern(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
                                    void *stream);
 

@@ -1025,7 +1025,12 @@ fgd_status fgd_stream_step_pattern(fgd_engine *e, void *theta_prev, const void *
         return fail(FGD_ERR_INVALID_ARG, "theta_prev, theta_local and momentum must not overlap");
     const void *kernel = nullptr;
     int v = 0, bpc = 0;
-    if (!fgd::pattern_kernel_for(c.num_workers, c.param_dtype == FGD_BF16, &kernel, &v, &bpc))
+    // The worker-group step's own layout when the current topology selects it.
+    fgd::WgKernel wk{};
+    size_t wg_lds = 0;
+    int wave_rows = 0;
+    const bool wg = e->slot_set[0] && e->slot_set[1] && wg_step_fits(e, wk, wg_lds, wave_rows);
+    if (!wg && !fgd::pattern_kernel_for(c.num_workers, c.param_dtype == FGD_BF16, &kernel, &v, &bpc))
         return fail(FGD_ERR_UNSUPPORTED, "the pattern reference runs for M in {1, 2, 4, 8, 16, 32, 64}");
     if (c.num_params == 0) return FGD_OK;
     DeviceGuard dg;
@@ -1039,9 +1044,14 @@ fgd_status fgd_stream_step_pattern(fgd_engine *e, void *theta_prev, const void *
     p.mom_out = momentum;
     p.P = c.num_params;
     p.ld = c.ld;
-    p.ntiles = tiles_of(c.num_params, v);
     p.mask = 0;
     int grid = 0;
+    if (wg) {  // the step's grid: its occupancy with its LDS
+        p.ntiles = (c.num_params + fgd::kWgTile - 1) / fgd::kWgTile;
+        if (fgd_status st = grid_for(e, wk.step, wg_lds, p.ntiles, grid)) return st;
+        return launch(wk.pattern, grid, 0, static_cast<hipStream_t>(stream_handle), &p);
+    }
+    p.ntiles = tiles_of(c.num_params, v);
     if (fgd_status st = grid_for(e, kernel, 0, p.ntiles, grid, bpc)) return st;
     return launch(kernel, grid, 0, static_cast<hipStream_t>(stream_handle), &p);
 }

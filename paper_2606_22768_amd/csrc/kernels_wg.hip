@@ -16,6 +16,8 @@ const void *pick(int k1, int k2) {
 
 bool wg_kernel(bool bf16, int k1, int k2, WgKernel *out) {
     out->step = bf16 ? pick<ParamBF16>(k1, k2) : pick<ParamF32>(k1, k2);
+    out->pattern = bf16 ? reinterpret_cast<const void *>(&wg_pattern_kernel<2>)
+                        : reinterpret_cast<const void *>(&wg_pattern_kernel<4>);
     return out->step != nullptr;
 }
 

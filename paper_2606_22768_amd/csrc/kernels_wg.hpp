@@ -52,6 +52,9 @@ constexpr int kWgR1 = 2;                              // Mix1 rounds the kernel 
 constexpr int kWgR2 = 4;                              // Mix2 rounds the kernel unrolls
 constexpr int kWgSlots = (kWgR2 + 1) + (kWgR1 + 1) + 1;  // consensus accumulators per lane
 constexpr int kWgMaxWidth = 15;                       // widest table row (entries)
+#ifndef FGD_WG_BATCH
+#define FGD_WG_BATCH 4  // table entries whose gathers are in flight together
+#endif
 
 struct WgMix {
     int32_t kind;        // MixKind
@@ -155,25 +158,34 @@ __device__ __forceinline__ void wg_round(float (&u)[kWgJ][kWgV], unsigned char *
     // reads above the writes.
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // Entries are taken in batches of B rows: the B table reads, then the B
+    // gathers they address, then the multiply-adds, so that B pairs of
+    // dependent LDS reads are in flight together.
+    constexpr int B = FGD_WG_BATCH;
     const int2 *t = tab + wg;
-#pragma unroll
-    for (int j = 0; j < kWgJ; ++j) {
-        const int2 e = t[j * kWgGroups];
-        const f32x4 r = *reinterpret_cast<const f32x4 *>(rows + e.x + lane_col);
-        const float w = __int_as_float(e.y);
-        u[j][0] = w * r.x; u[j][1] = w * r.y; u[j][2] = w * r.z; u[j][3] = w * r.w;
-    }
-    for (int d = 1; d < width; ++d) {
+    for (int d = 0; d < width; ++d) {
         const int2 *td = t + d * kWgJ * kWgGroups;
 #pragma unroll
-        for (int j = 0; j < kWgJ; ++j) {
-            const int2 e = td[j * kWgGroups];
-            const f32x4 r = *reinterpret_cast<const f32x4 *>(rows + e.x + lane_col);
-            const float w = __int_as_float(e.y);
-            u[j][0] = fmaf(w, r.x, u[j][0]);
-            u[j][1] = fmaf(w, r.y, u[j][1]);
-            u[j][2] = fmaf(w, r.z, u[j][2]);
-            u[j][3] = fmaf(w, r.w, u[j][3]);
+        for (int j0 = 0; j0 < kWgJ; j0 += B) {
+            int2 e[B];
+            f32x4 r[B];
+#pragma unroll
+            for (int q = 0; q < B; ++q) e[q] = td[(j0 + q) * kWgGroups];
+#pragma unroll
+            for (int q = 0; q < B; ++q) r[q] = *reinterpret_cast<const f32x4 *>(rows + e[q].x + lane_col);
+#pragma unroll
+            for (int q = 0; q < B; ++q) {
+                const int j = j0 + q;
+                const float w = __int_as_float(e[q].y);
+                if (d == 0) {
+                    u[j][0] = w * r[q].x; u[j][1] = w * r[q].y; u[j][2] = w * r[q].z; u[j][3] = w * r[q].w;
+                } else {
+                    u[j][0] = fmaf(w, r[q].x, u[j][0]);
+                    u[j][1] = fmaf(w, r[q].y, u[j][1]);
+                    u[j][2] = fmaf(w, r[q].z, u[j][2]);
+                    u[j][3] = fmaf(w, r[q].w, u[j][3]);
+                }
+            }
         }
     }
     // The next round's writes must not pass this round's reads.
@@ -390,6 +402,59 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) voi
     }
 }
 
+// The worker-group step's memory traffic without its arithmetic (the
+// access-pattern reference of fgd_stream_step_pattern for this layout):
+// same tiles, per-lane rows and vectors, cache policy and launch shape;
+// every theta_prev and theta_local row of a tile loaded before first use,
+// then four momentum rows at a time loaded and theta_prev and the momentum
+// stored back with their own bits (OR of theta_local AND mask, mask = 0 at
+// run time, keeps every load live).  Lanes of a ragged vector store nothing.
+template <int kE>
+__global__ __launch_bounds__(kBlock) void wg_pattern_kernel(PatternParams a) {
+    constexpr int NP = kWgV * kE, WP = RawIo<NP>::kW, WV = RawIo<kWgV * 4>::kW;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int wg = lane >> 4, pg = lane & (kWgPg - 1);
+    const int lane_param = wave * kWgWaveParams + pg * kWgV;
+    const uint32_t off_p = static_cast<uint32_t>((wg * a.ld + lane_param) * kE);
+    const uint32_t off_v = static_cast<uint32_t>((wg * a.ld + lane_param) * 4);
+    for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+        const int64_t tb = tile * kWgTile;
+        const int64_t rem = a.P - tb - lane_param;
+        if (rem <= 0) continue;
+        const bool whole = rem >= kWgV;
+        uint32_t u1[kWgJ][WP], u2[kWgJ][WP];
+#pragma unroll
+        for (int j = 0; j < kWgJ; ++j) {
+            const int64_t e = static_cast<int64_t>(kWgGroups * j) * a.ld + tb;
+            RawIo<NP>::load(row_rsrc_wide(a.theta_prev, e, kE), off_p, u1[j]);
+            RawIo<NP>::load(row_rsrc_wide(a.theta_local, e, kE), off_p, u2[j]);
+        }
+        constexpr int G = 4;
+#pragma unroll
+        for (int j0 = 0; j0 < kWgJ; j0 += G) {
+            uint32_t vm[G][WV];
+#pragma unroll
+            for (int i = 0; i < G; ++i)
+                RawIo<kWgV * 4>::load(row_rsrc_wide(a.mom, static_cast<int64_t>(kWgGroups * (j0 + i)) * a.ld + tb, 4),
+                                      off_v, vm[i]);
+#pragma unroll
+            for (int i = 0; i < G; ++i) {
+                const int j = j0 + i;
+                uint32_t t[WP];
+#pragma unroll
+                for (int k = 0; k < WP; ++k) t[k] = u1[j][k] | (u2[j][k] & a.mask);
+#pragma unroll
+                for (int k = 0; k < WV; ++k) vm[i][k] |= u2[j][k % WP] & a.mask;
+                if (whole) {
+                    const int64_t e = static_cast<int64_t>(kWgGroups * j) * a.ld + tb;
+                    RawIo<kWgV * 4>::store(row_rsrc_wide(a.mom_out, e, 4), off_v, vm[i]);
+                    RawIo<NP>::store(row_rsrc_wide(a.theta_out, e, kE), off_p, t);
+                }
+            }
+        }
+    }
+}
+
 // Worker-group kernel for the (Mix1, Mix2) kinds of the paper's sparse
 // configurations at 64 workers: LocalM1M2 (CSR, CSR) and GlobalM1LocalM2
 // (global mean, CSR).  False for other kinds (their run-time-kind form
@@ -397,6 +462,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) voi
 // outer_step_kernel).
 struct WgKernel {
     const void *step;
+    const void *pattern;  // wg_pattern_kernel of the storage
 };
 bool wg_kernel(bool bf16, int k1, int k2, WgKernel *out);
 

@@ -58,3 +58,34 @@ def test_pattern_refuses_other_worker_counts(env):
         assert e.value.status == fgd.FGD_ERR_UNSUPPORTED
     finally:
         eng.close()
+
+
+@pytest.mark.parametrize("P,dtype", [(777, "f32"), (300, "bf16"), (300_001, "f32")])
+def test_worker_group_pattern_leaves_arrays_unchanged(env, P, dtype):
+    """With a topology that selects the 64-worker worker-group step, the
+    reference follows that layout; it too leaves every array bit-identical."""
+    fgd, torch = env
+    M = 64
+    print(f"[pattern wg] P={P} {dtype}", flush=True)
+    ld = pa.aligned_ld(P) + 8
+    tp, tl, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, seed=P)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    dev = lambda a, t: (torch.from_numpy(a).cuda() if a.dtype == np.float32 and t == torch.float32
+                        else torch.from_numpy(a.view(np.int16)).cuda().view(t))
+    g_tp, g_tl, g_v = dev(tp, tdt), dev(tl, tdt), torch.from_numpy(v).cuda()
+    g_v[M - 1, P - 1] = float("nan")
+    before = [t.clone() for t in (g_tp, g_tl, g_v)]
+    eng = fgd.Engine(M, P, ld, dtype, device=0)
+    try:
+        reg4 = ("regular", "metropolis", 4)
+        eng.set_topology_dict("mix1", pa.topo(reg4, M, 1))
+        eng.set_topology_dict("mix2", pa.topo(reg4, M, 3))
+        assert eng.step_variant() == "worker-groups"
+        for _ in range(2):
+            eng.stream_step_pattern(g_tp, g_tl, g_v)
+        torch.cuda.synchronize()
+    finally:
+        eng.close()
+    for a, b in zip((g_tp, g_tl, g_v), before):
+        w = torch.int16 if a.dtype == torch.bfloat16 else torch.int32
+        assert torch.equal(a.view(w), b.view(w))
