@@ -49,8 +49,9 @@ def source_hashes(root: str = ROOT) -> dict:
     all   every file under paper_2606_22768_amd/csrc and include/fgd.h;
     step  the HIP sources of the outer step, its split halves, consensus,
           finalize and copy kernels and their launches (every .hip/.hpp but
-          the JS distance's);
-    js    the JS distance kernels and the header they include.
+          the JS distance's js.hip and js.hpp);
+    js    the JS distance kernels, their launcher header and the kernel
+          header they include.
     Traffic counters and timings are valid only for the hash they were
     taken with."""
     csrc = os.path.join(root, "paper_2606_22768_amd", "csrc")
@@ -61,9 +62,9 @@ def source_hashes(root: str = ROOT) -> dict:
             data = name.encode() + b"\0" + f.read()
         hs["all"].update(data)
         if name.endswith((".hip", ".hpp")):
-            if name != "js.hip":
+            if name not in ("js.hip", "js.hpp"):
                 hs["step"].update(data)
-            if name in ("js.hip", "kernels.hpp"):
+            if name in ("js.hip", "js.hpp", "kernels.hpp"):
                 hs["js"].update(data)
     with open(os.path.join(root, "include", "fgd.h"), "rb") as f:
         hs["all"].update(b"fgd.h\0" + f.read())

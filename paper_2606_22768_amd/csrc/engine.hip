@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "../../include/fgd.h"
+#include "js.hpp"
 #include "kernels.hpp"
 #include "kernels_wg.hpp"
 #include "topology.hpp"
@@ -370,6 +371,27 @@ fgd_status noalloc_device(int dev, double *&ptr, int &num_cus) {
     }
     ptr = d.ptr;
     num_cus = d.num_cus;
+    return FGD_OK;
+}
+
+// Compute units of the current device (sizes persistent grids of the
+// engine-free calls), queried once per device.
+constexpr int kCuCacheDevices = 64;
+std::mutex g_cu_mutex;
+int g_cu_count[kCuCacheDevices] = {};
+fgd_status current_device_cus(int &num_cus) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return hip_fail(err, "querying the current device");
+    if (dev < 0 || dev >= kCuCacheDevices) return fail(FGD_ERR_UNSUPPORTED, "device %d is beyond %d", dev, kCuCacheDevices);
+    std::lock_guard<std::mutex> lock(g_cu_mutex);
+    if (g_cu_count[dev] == 0) {
+        int cus = 0;
+        err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (err != hipSuccess) return hip_fail(err, "querying the compute-unit count");
+        g_cu_count[dev] = cus > 0 ? cus : 1;
+    }
+    num_cus = g_cu_count[dev];
     return FGD_OK;
 }
 
@@ -1004,8 +1026,10 @@ fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, i
     if (top_k < 1 || top_k > FGD_MAX_JS_TOPK || top_k > vocab)
         return fail(FGD_ERR_INVALID_ARG, "top_k %d is outside [1, min(vocab, %d)]", top_k, FGD_MAX_JS_TOPK);
     hipStream_t stream = static_cast<hipStream_t>(stream_handle);
+    int num_cus = 0;
+    if (fgd_status st = current_device_cus(num_cus)) return st;
     if (!fgd::js_launch(logits_avg, logits_workers, dtype == FGD_BF16, num_workers, num_tokens, vocab, ldk, top_k,
-                        d_out, mean_out, topk_out, stream))
+                        d_out, mean_out, topk_out, num_cus, stream))
         return fail(FGD_ERR_HIP, "JS distance launch failed");
     return FGD_OK;
 }

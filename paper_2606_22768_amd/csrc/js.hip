@@ -13,24 +13,44 @@
 //                lq = zbar_i - lse_a, lmix = log((p + q) / 2)
 //   d_m(u)     = sqrt(max(JS_m, 0) / log 2)
 // Probabilities are those of the full softmax; only the sum is restricted to
-// T.  Two kernels: js_lse_kernel takes one (token, worker) row per block, so
-// the bulk of the work (M of the M + 1 rows) spreads over M * U blocks, and
-// parks lse_m in d_out; js_kernel takes one token per block: the averaged
-// row, the selection and the JS terms, and overwrites d_out with d_m(u).
+// T.  Two kernels: the worker-row kernel computes every lse_m (M of the
+// M + 1 rows per token, the bulk of the work) and parks it in d_out;
+// js_kernel takes one token per block: the averaged row, the selection and
+// the JS terms, and overwrites d_out with d_m(u).
 //
-// The log-sum-exp of a row is a (shift, scaled sum) reduction: the shift is
-// a lane's first finite value and moves only when a later value exceeds it
-// by more than kLseSlack, so every exponent is at most kLseSlack and the
-// sums cannot overflow.  exp is a table-driven float64 exp (Tang's method:
-// ACM TOMS 15(2), 1989): x = (256 n + j) ln2/256 + r with |r| <= ln2/512,
-// exp(x) = 2^n 2^(j/256) (1 + q(r)), q the degree-4 Taylor polynomial of
-// e^r - 1 (truncation below 0.4 ulp), 2^(j/256) from a table in LDS; within
-// 2 ulp of the correctly rounded value.  Every reduction has a fixed order,
-// so results are deterministic.  The selected indices are rank-sorted so
-// that the JS sum runs in index order.
+// Worker rows.  bf16 logits take only 65536 bit patterns, and the exp of
+// every bf16 value v with 2^-16 <= |v| < 64 (22 binades, both signs: 5632
+// values) is a table of 44 KB in LDS, filled once per block with the
+// library's float64 exp.  Such terms need no shift: each is below e^64, so
+// their plain sum cannot overflow; a term costs an index from the bit
+// pattern, one LDS read and one add.  A 16-byte vector of logits in which
+// any lane of the wave holds another value (0, |v| < 2^-16, |v| >= 64,
+// -inf, or the ragged end of the row) goes through the general path below,
+// whose shifted sum is merged with the table sum at the end of the row.
+// float32 logits always take the general path.
+//
+// General path.  The log-sum-exp of a row is a (shift, scaled sum)
+// reduction: the shift is a lane's first finite value and moves only when a
+// later value exceeds it by more than kLseSlack, so every exponent is at
+// most kLseSlack and the sums cannot overflow.  exp is a table-driven
+// float64 exp (Tang's method: ACM TOMS 15(2), 1989): x = (256 n + j) ln2/256
+// + r with |r| <= ln2/512, exp(x) = 2^n 2^(j/256) (1 + q(r)), q the degree-4
+// Taylor polynomial of e^r - 1 (truncation below 0.4 ulp), 2^(j/256) from a
+// table in LDS; within 2 ulp of the correctly rounded value.  The factor 2^n
+// is applied by an integer add to the table entry's exponent field (the
+// entry is stored with j << 12 already subtracted from its high word, so
+// adding n << 12 leaves the mantissa alone and adds n >> 8 to the
+// exponent); x is clamped at -708 so that the scaled entry stays a normal
+// double.  Lanes are combined through the block's largest shift (one exp
+// per lane, no pairwise rescaling).  Every reduction has a fixed order, so
+// results are deterministic.  The selected indices are rank-sorted so that
+// the JS sum runs in index order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
+#include "js.hpp"
 #include "kernels.hpp"
 
 namespace fgd {
@@ -50,6 +70,7 @@ struct JsParams {
 // = ascending value; -0 and +0 share the key of +0).
 struct JsF32 {
     static constexpr int kPer = 4, kElem = 4, kKeyBits = 32;
+    static constexpr bool kBf16 = false;
     __device__ static void unpack(u32x4 t, float (&v)[kPer], uint32_t (&key)[kPer]) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -66,10 +87,20 @@ struct JsF32 {
     __device__ static float at(rsrc_t r, int64_t i) {
         return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, static_cast<uint32_t>(i * 4), 0, 0));
     }
+    // The key of a value, and the value of a key that some value has.
+    __device__ static uint32_t key_of(float v) {
+        uint32_t b = __float_as_uint(v);
+        if ((b & 0x7FFFFFFFu) == 0) b = 0;
+        return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+    }
+    __device__ static float value_of(uint32_t key) {
+        return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+    }
 };
 
 struct JsBF16 {
     static constexpr int kPer = 8, kElem = 2, kKeyBits = 16;
+    static constexpr bool kBf16 = true;
     __device__ static void unpack(u32x4 t, float (&v)[kPer], uint32_t (&key)[kPer]) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -90,6 +121,16 @@ struct JsBF16 {
         const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(r, static_cast<uint32_t>(i * 2), 0, 0);
         return __uint_as_float(h << 16);
     }
+    // The key of a value (a bf16 widened to float), and the value of a key
+    // that some value has.
+    __device__ static uint32_t key_of(float v) {
+        uint32_t h = __float_as_uint(v) >> 16;
+        if ((h & 0x7FFFu) == 0) h = 0;
+        return (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u);
+    }
+    __device__ static float value_of(uint32_t key) {
+        return __uint_as_float(((key & 0x8000u) ? (key & 0x7FFFu) : (~key & 0xFFFFu)) << 16);
+    }
 };
 
 __device__ inline rsrc_t js_row(const void *base, int64_t row, int64_t ldk, int es) {
@@ -97,37 +138,11 @@ __device__ inline rsrc_t js_row(const void *base, int64_t row, int64_t ldk, int 
                                              static_cast<short>(0), 0x7fffffff, kRawBufferFlags);
 }
 
-// (max, sum of exp(x - max)) pairs: the combination is symmetric, so every
-// lane of a butterfly ends with the same value.
-__device__ inline void lse_combine(double &m, double &s, double m2, double s2) {
-    const double mm = m > m2 ? m : m2;
-    if (mm == -INFINITY) return;  // both empty
-    const double a = m == -INFINITY ? 0.0 : s * exp(m - mm);
-    const double b = m2 == -INFINITY ? 0.0 : s2 * exp(m2 - mm);
-    m = mm;
-    s = a + b;
-}
-
 __device__ inline double shfl_xor_d(double x, int mask) {
     const int64_t b = __double_as_longlong(x);
     const int lo = __shfl_xor(static_cast<int>(b & 0xFFFFFFFF), mask);
     const int hi = __shfl_xor(static_cast<int>(b >> 32), mask);
     return __longlong_as_double((static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo));
-}
-
-// Block-wide log-sum-exp of per-thread (m, s); every thread gets the result.
-__device__ inline double block_lse(double m, double s, double *red) {
-    for (int o = kWave / 2; o > 0; o >>= 1) lse_combine(m, s, shfl_xor_d(m, o), shfl_xor_d(s, o));
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    __syncthreads();
-    if (lane == 0) {
-        red[2 * wave] = m;
-        red[2 * wave + 1] = s;
-    }
-    __syncthreads();
-    double M = red[0], S = red[1];
-    for (int w = 1; w < kWavesPerBlock; ++w) lse_combine(M, S, red[2 * w], red[2 * w + 1]);
-    return M == -INFINITY ? -INFINITY : M + log(S);
 }
 
 // Block-wide sum in a fixed order; every thread gets the result.
@@ -237,9 +252,23 @@ constexpr double kExpRound = 0x1.8p52;                   // adding it rounds to 
 constexpr double kExpInvL = 0x1.71547652b82fep+8;        // 256 / ln 2
 constexpr double kExpL1 = 0x1.62e42fee00000p-9;          // ln2 / 256, high part (n * kExpL1 is exact)
 constexpr double kExpL2 = 0x1.a39ef35793c76p-41;         // ln2 / 256 - kExpL1
-constexpr double kExpFloor = -746.0;                     // exp(-746) rounds to 0
+constexpr double kExpFloor = -708.0;                     // 2^(n >> 8) 2^(j/256) stays normal above it
 
-// exp(x) for x <= 700 (and x = -inf); `tab` is kExp2Frac in LDS.
+// The LDS copy of kExp2Frac with j << 12 subtracted from entry j's high
+// word (see exp_table).  Block-wide; ends with a barrier.
+__device__ inline void load_exp_table(double *tab) {
+    const int tid = threadIdx.x;
+    if (tid < kTab) {
+        const double t = kExp2Frac[tid];
+        tab[tid] = __hiloint2double(__double2hiint(t) - (tid << 12), __double2loint(t));
+    }
+    __syncthreads();
+}
+
+// exp(x) for x <= 700; x below -708 (and -inf) gives exp(-708) ~ 3.3e-308,
+// which no sum it joins can notice (every sum it is added to holds a term
+// of at least 1, or is discarded; see lse_add and the row kernels).  `tab`
+// comes from load_exp_table.
 __device__ __forceinline__ double exp_table(double x, const double *tab) {
     x = fmax(x, kExpFloor);
     const double y = fma_vsv(x, kExpInvL, kExpRound);
@@ -250,19 +279,20 @@ __device__ __forceinline__ double exp_table(double x, const double *tab) {
     p = fma_vvs(p, r, 0.5);
     p = fma_vvs(p, r, 1.0);
     const double q = p * r;                              // e^r - 1
-    const double t = tab[n & (kTab - 1)];
-    return ldexp(fma(t, q, t), n >> kTabBits);
+    const double tb = tab[n & (kTab - 1)];
+    // 2^(j/256) * 2^(n >> 8): the entry's high word already lacks j << 12.
+    const double t = __hiloint2double(__double2hiint(tb) + (n << 12), __double2loint(tb));
+    return fma(t, q, t);
 }
 
 // ------------------------------------------------------------ log-sum-exp
 constexpr double kLseSlack = 64.0;     // largest exponent a sum may take
 constexpr double kLseEmpty = -1e300;   // shift of a lane that has seen no finite value
 
-// Values of one 16-byte vector of a row; those at or past K read as -inf,
-// which the log-sum-exp ignores exactly.
+// Values of one loaded 16-byte vector of a row that starts at element i0;
+// those at or past K read as -inf, which the log-sum-exp ignores exactly.
 template <class E>
-__device__ inline void load_values(rsrc_t r, int64_t i0, int64_t K, float (&v)[E::kPer]) {
-    const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy);
+__device__ inline void vec_values(u32x4 t, int64_t i0, int64_t K, float (&v)[E::kPer]) {
     E::values(t, v);
     if (i0 + E::kPer > K) {
 #pragma unroll
@@ -287,17 +317,35 @@ __device__ inline int load_vec(rsrc_t r, int64_t i0, int64_t K, float (&v)[E::kP
     return n;
 }
 
-// Adds one vector to a lane's (shift m, sum s = sum exp(x - m)).  The terms
-// are summed pairwise before they join the running sum.
+// Largest of four or eight values (three-operand maxima; logits are never
+// NaN).
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+    float d;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
+    return d;
+}
 template <int N>
-__device__ inline void lse_add(double &m, double &s, const float (&v)[N], const double *tab) {
-    float vm = v[0];
-#pragma unroll
-    for (int j = 1; j < N; ++j) vm = fmaxf(vm, v[j]);
-    const double dm = vm;
-    if (dm > m + kLseSlack) {
-        s *= exp(m - dm);
+__device__ __forceinline__ float vec_max(const float (&v)[N]) {
+    static_assert(N == 4 || N == 8, "a 16-byte vector holds 4 or 8 logits");
+    if constexpr (N == 8) return max3f(max3f(max3f(v[0], v[1], v[2]), v[3], v[4]), max3f(v[5], v[6], v[7]), v[0]);
+    return max3f(max3f(v[0], v[1], v[2]), v[3], v[0]);
+}
+
+// Adds one vector to a lane's (shift m, sum s = sum exp(x - m)); thr is
+// m + kLseSlack rounded to float (-inf while the lane is empty), the value
+// above which the shift moves.  The terms are summed pairwise before they
+// join the running sum.  Once a lane has seen a finite value, s holds a
+// term of at least 1 (the one at the shift), so clamped terms (exp_table)
+// vanish in it; the terms a still-empty lane gathers are scaled to 0 when
+// its shift first moves, or dropped by lane_state.
+template <int N>
+__device__ inline void lse_add(double &m, float &thr, double &s, const float (&v)[N], const double *tab) {
+    const float vm = vec_max<N>(v);
+    if (vm > thr) {
+        const double dm = vm;
+        s *= exp_table(m - dm, tab);
         m = dm;
+        thr = static_cast<float>(dm + kLseSlack);
     }
     double e[N];
 #pragma unroll
@@ -309,27 +357,192 @@ __device__ inline void lse_add(double &m, double &s, const float (&v)[N], const 
     s += e[0];
 }
 
-// lse of one worker row (token blockIdx.x, worker blockIdx.y) into
-// d_out[w][u].
+// log-sum-exp over the threads [g * G, (g + 1) * G) of the block (G a
+// multiple of the wave, g the caller's group) from per-thread (m, s): the
+// group's largest shift M, then sum s exp(m - M) in a fixed order; every
+// thread of the group gets the result.  Block-wide barriers: every thread
+// of the block calls it.  `red` holds 2 doubles per wave of the block.
+template <int G>
+__device__ inline double group_lse(double m, double s, double *red, const double *tab) {
+    constexpr int kW = G / kWave;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave, g0 = (threadIdx.x / G) * kW;
+    double M = m;
+    for (int o = kWave / 2; o > 0; o >>= 1) M = fmax(M, shfl_xor_d(M, o));
+    __syncthreads();
+    if (lane == 0) red[2 * wave] = M;
+    __syncthreads();
+    M = red[2 * g0];
+    for (int w = 1; w < kW; ++w) M = fmax(M, red[2 * (g0 + w)]);
+    double t = s == 0.0 ? 0.0 : s * exp_table(m - M, tab);
+    for (int o = kWave / 2; o > 0; o >>= 1) t += shfl_xor_d(t, o);
+    if (lane == 0) red[2 * wave + 1] = t;
+    __syncthreads();
+    double S = red[2 * g0 + 1];
+    for (int w = 1; w < kW; ++w) S += red[2 * (g0 + w) + 1];
+    return S == 0.0 ? -INFINITY : M + log(S);
+}
+
+// A lane's (shift, sum) at the end of a row: an empty lane reports no terms.
+__device__ inline void lane_state(double &m, double &s) {
+    if (m == kLseEmpty) s = 0.0;
+}
+
+// lse of worker rows, general path (float32 logits): one row per block
+// (token blockIdx.x, worker blockIdx.y) into d_out[w][u]; the next vector of
+// the row is loaded while the current one is summed.
 template <class E>
 __global__ __launch_bounds__(kBlock) void js_lse_kernel(JsParams a) {
     constexpr int P = E::kPer;
     constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;
     __shared__ double tab[kTab];
     __shared__ double red[2 * kWavesPerBlock];
-    const int tid = threadIdx.x;
-    if (tid < kTab) tab[tid] = kExp2Frac[tid];
-    __syncthreads();
+    load_exp_table(tab);
     const int64_t row = static_cast<int64_t>(blockIdx.y) * a.U + blockIdx.x;
     const rsrc_t r = js_row(a.workers, row, a.ldk, E::kElem);
     double m = kLseEmpty, s = 0.0;
-    for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
+    float thr = -INFINITY;
+    int64_t i0 = static_cast<int64_t>(threadIdx.x) * P;
+    u32x4 nxt = {0, 0, 0, 0};
+    if (i0 < a.K) nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy);
+    for (; i0 < a.K; i0 += kStride) {
+        const u32x4 cur = nxt;
+        if (i0 + kStride < a.K)
+            nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * E::kElem), 0,
+                                                        kLoadPolicy);
         float v[P];
-        load_values<E>(r, i0, a.K, v);
-        lse_add<P>(m, s, v, tab);
+        vec_values<E>(cur, i0, a.K, v);
+        lse_add<P>(m, thr, s, v, tab);
     }
-    const double lse = block_lse(m, s, red);
-    if (tid == 0) a.d_out[row] = lse;
+    lane_state(m, s);
+    const double lse = group_lse<kBlock>(m, s, red, tab);
+    if (threadIdx.x == 0) a.d_out[row] = lse;
+}
+
+// ------------------------------------------------ bf16 rows: exp table
+constexpr int kBfTabE0 = 111;                              // exponent field of 2^-16
+constexpr int kBfTabE1 = 132;                              // exponent field of [32, 64)
+constexpr uint32_t kBfTabLo = kBfTabE0 << 7;               // first magnitude pattern in the table
+constexpr uint32_t kBfTabN = (kBfTabE1 - kBfTabE0 + 1) << 7;  // magnitudes per sign (2816)
+constexpr int kBfTabEntries = 2 * kBfTabN;
+constexpr int kBfRowThreads = kBlock;                      // threads per row (js_kernel's block)
+constexpr int kBfRowsPerBlock = 2;                         // rows a worker-row block sums at once
+constexpr int kBfBlock = kBfRowThreads * kBfRowsPerBlock;
+constexpr int kBfBlocksPerCu = 3;                          // LDS: 3 x 47 KB of the CU's 160 KB
+
+// Entry 2 (a - kBfTabLo) + s = exp of the bf16 value with magnitude
+// pattern a and sign s, from the library's float64 exp.  Block-wide, no
+// barrier of its own.
+__device__ inline void fill_bf16_exp_table(double *etab) {
+    for (int i = threadIdx.x; i < kBfTabEntries; i += blockDim.x) {
+        const uint32_t h = (kBfTabLo + static_cast<uint32_t>(i >> 1)) | (static_cast<uint32_t>(i & 1) << 15);
+        etab[i] = exp(static_cast<double>(__uint_as_float(h << 16)));
+    }
+}
+
+// A lane's partial log-sum-exp of a row: table terms summed unshifted (s0)
+// and general-path terms shifted by m (s1, thr as in lse_add).
+struct RowLse {
+    double s0 = 0.0, m = kLseEmpty, s1 = 0.0;
+    float thr = -INFINITY;
+};
+
+// Adds the 16-byte vector `t` of bf16 logits (elements i0 .. i0 + 7 of a
+// row of K).  When every active lane of the wave holds eight values inside
+// the table, their terms are read from it; otherwise the vector takes the
+// general path, one term at a time (which keeps the kernels' registers
+// within their occupancy).  The choice depends only on the data and the
+// lane-to-element map, so two rows with equal logits summed under the same
+// map give bit-identical results.
+__device__ inline void bf16_lse_add(RowLse &st, u32x4 t, int64_t i0, int64_t K, const double *etab,
+                                    const double *tab) {
+    constexpr int P = JsBF16::kPer;
+    uint32_t idx[P];
+    bool in_table = i0 + P <= K;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t w = t[j];
+        const uint32_t d0 = (w & 0x7FFFu) - kBfTabLo, d1 = ((w >> 16) & 0x7FFFu) - kBfTabLo;
+        in_table = in_table && d0 < kBfTabN && d1 < kBfTabN;
+        idx[2 * j] = (d0 << 1) | ((w >> 15) & 1u);
+        idx[2 * j + 1] = (d1 << 1) | (w >> 31);
+    }
+    if (__all(in_table)) {
+        double e[P];
+#pragma unroll
+        for (int j = 0; j < P; ++j) e[j] = etab[idx[j]];
+#pragma unroll
+        for (int w = 1; w < P; w *= 2)
+#pragma unroll
+            for (int j = 0; j + w < P; j += 2 * w) e[j] += e[j + w];
+        st.s0 += e[0];
+    } else {
+        float v[P];
+        vec_values<JsBF16>(t, i0, K, v);
+        const float vm = vec_max<P>(v);
+        if (vm > st.thr) {
+            const double dm = vm;
+            st.s1 *= exp_table(st.m - dm, tab);
+            st.m = dm;
+            st.thr = static_cast<float>(dm + kLseSlack);
+        }
+#pragma unroll 1
+        for (int j = 0; j < P; ++j) st.s1 += exp_table(static_cast<double>(v[j]) - st.m, tab);
+    }
+}
+
+// The lane's (shift, sum) at the end of a row: the table sum has shift 0,
+// the general one shift m; an empty lane reports no terms.
+__device__ inline void row_lse_lane(RowLse st, double &ml, double &sl, const double *tab) {
+    lane_state(st.m, st.s1);
+    if (st.s1 == 0.0) {
+        ml = st.s0 == 0.0 ? kLseEmpty : 0.0;
+        sl = st.s0;
+    } else if (st.s0 == 0.0) {
+        ml = st.m;
+        sl = st.s1;
+    } else {
+        ml = st.m > 0.0 ? st.m : 0.0;
+        sl = st.s0 * exp_table(-ml, tab) + st.s1 * exp_table(st.m - ml, tab);
+    }
+}
+
+// Worker rows of bf16 logits, persistent: block b sums rows 2p and 2p + 1
+// for p = b, b + gridDim.x, ...; thread lt of a row takes the same elements
+// as thread lt of js_kernel does on the averaged row.
+__global__ __launch_bounds__(kBfBlock) __attribute__((amdgpu_waves_per_eu(6, 8)))
+void js_lse_bf16_table_kernel(JsParams a) {
+    constexpr int P = JsBF16::kPer;
+    constexpr int64_t kStride = static_cast<int64_t>(kBfRowThreads) * P;
+    __shared__ double etab[kBfTabEntries];
+    __shared__ double tab[kTab];
+    __shared__ double red[2 * kBfBlock / kWave];
+    fill_bf16_exp_table(etab);
+    load_exp_table(tab);  // its barrier also covers etab
+    const int g = threadIdx.x / kBfRowThreads, lt = threadIdx.x % kBfRowThreads;
+    const int64_t rows = static_cast<int64_t>(a.M) * a.U;
+    const int64_t groups = (rows + kBfRowsPerBlock - 1) / kBfRowsPerBlock;
+    for (int64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
+        const int64_t row = grp * kBfRowsPerBlock + g;
+        const bool valid = row < rows;
+        RowLse st;
+        if (valid) {
+            const rsrc_t r = js_row(a.workers, row, a.ldk, JsBF16::kElem);
+            int64_t i0 = static_cast<int64_t>(lt) * P;
+            u32x4 nxt = {0, 0, 0, 0};
+            if (i0 < a.K) nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * 2), 0, kLoadPolicy);
+            for (; i0 < a.K; i0 += kStride) {
+                const u32x4 cur = nxt;
+                if (i0 + kStride < a.K)
+                    nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * 2), 0,
+                                                                kLoadPolicy);
+                bf16_lse_add(st, cur, i0, a.K, etab, tab);
+            }
+        }
+        double ml, sl;
+        row_lse_lane(st, ml, sl, tab);
+        const double lse = group_lse<kBfRowThreads>(ml, sl, red, tab);
+        if (valid && lt == 0) a.d_out[row] = lse;
+    }
 }
 
 // One token's term of the JS sum from the two log-probabilities; a side of
@@ -367,9 +580,34 @@ __device__ inline double block_sum_n(double (&x)[N], double *red) {
 }
 
 constexpr int kJsGroup = 8;  // workers whose logits are gathered together
+constexpr int kJsHalf = kJsGroup / 2;  // of them, per half of the block
+#ifndef FGD_JS_BATCH
+#define FGD_JS_BATCH 8
+#endif
+constexpr int kJsBatch = FGD_JS_BATCH;  // vectors of the averaged row a thread loads before using them
+constexpr int kJsMaxBatches = 16;       // batches per thread whose largest keys js_kernel records
 
-// One token per block: the averaged row's log-sum-exp and top-k set, then
-// JS_m for every worker from the lse_m that js_lse_kernel left in d_out.
+// Loads the vectors of a row at i0, i0 + stride, ... (kJsBatch of them) so
+// that their latencies overlap; those at or past K read as zero and are
+// never used.
+template <class E>
+__device__ inline void load_batch(rsrc_t r, int64_t i0, int64_t K, int64_t stride, u32x4 (&t)[kJsBatch]) {
+#pragma unroll
+    for (int d = 0; d < kJsBatch; ++d) {
+        const int64_t i = i0 + d * stride;
+        t[d] = u32x4{0, 0, 0, 0};
+        if (i < K) t[d] = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i * E::kElem), 0, kLoadPolicy);
+    }
+}
+// Resident blocks of js_kernel per CU (its persistent grid): LDS bounds the
+// bf16 kernel (79 KB with the exp table), registers the float32 one.
+constexpr int kJsBlocksPerCuBf16 = 2;
+constexpr int kJsBlocksPerCuF32 = 2;
+
+// One token at a time per block (persistent: tokens blockIdx.x,
+// blockIdx.x + gridDim.x, ...): the averaged row's log-sum-exp and top-k
+// set, then JS_m for every worker from the lse_m that the worker-row kernel
+// left in d_out.
 //
 // Selection.  Fast path (k <= kBlock): the k-th largest of the threads'
 // largest keys, T0, is at most the k-th largest key of the row, so the
@@ -385,9 +623,9 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
     constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;  // elements per block sweep
     constexpr int kCand = kJsMaxTopK;                              // candidate capacity
     __shared__ uint32_t hist[256];
-    __shared__ int32_t sel_idx[kJsMaxTopK];
+    __shared__ __align__(16) int32_t sel_idx[kJsMaxTopK];
     __shared__ float sel_val[kJsMaxTopK];
-    __shared__ union {
+    __shared__ __align__(16) union {
         struct {
             int32_t idx[kCand];
             uint32_t key[kCand];
@@ -400,231 +638,317 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
     } sm;
     __shared__ double red[2 * kWavesPerBlock];
     __shared__ double red_n[kJsGroup * kWavesPerBlock];
-    __shared__ uint32_t s_tkey[kBlock];
+    __shared__ __align__(16) uint32_t s_tkey[kBlock];
+    __shared__ uint16_t s_bmax[kJsMaxBatches][kBlock];  // per thread: largest key of each batch, top 16 bits
     __shared__ uint32_t s_prefix, s_thr;
     __shared__ int s_need, s_count_eq, s_nsel;
     __shared__ int s_scan[kBlock];
     __shared__ double tab[kTab];
+    __shared__ double etab[E::kBf16 ? kBfTabEntries : 1];
 
     const int tid = threadIdx.x;
-    const int64_t u = blockIdx.x;
     const int k = a.k;
-    const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
-    if (tid < kTab) tab[tid] = kExp2Frac[tid];
-    __syncthreads();
+    if constexpr (E::kBf16) fill_bf16_exp_table(etab);
+    load_exp_table(tab);  // its barrier also covers etab
 
-    // Pass 1 over the averaged row: log-sum-exp and this thread's largest key
-    // (key 0 lies below the key of every value).
-    double m = kLseEmpty, s = 0.0;
-    uint32_t kmax = 0;
-    for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
-        float v[P];
-        uint32_t key[P];
-        const int n = load_vec<E>(ra, i0, a.K, v, key);
-        lse_add<P>(m, s, v, tab);
+    for (int64_t u = blockIdx.x; u < a.U; u += gridDim.x) {
+        const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
+
+        // Pass 1 over the averaged row: log-sum-exp (the same sums, in the same
+        // lane order, as the worker rows get) and this thread's largest key
+        // (key 0 lies below the key of every value).
+        RowLse st;
+        uint32_t kmax = 0;
+        int nb = 0;  // batches this thread reads
+        for (int64_t b0 = static_cast<int64_t>(tid) * P; b0 < a.K; b0 += kJsBatch * kStride, ++nb) {
+            u32x4 tb[kJsBatch];
+            load_batch<E>(ra, b0, a.K, kStride, tb);
+            uint32_t bmax = 0;
 #pragma unroll
-        for (int j = 0; j < P; ++j) kmax = max(kmax, j < n ? key[j] : 0u);
-    }
-    const double lse_a = block_lse(m, s, red);
-
-    bool fast = k <= kBlock;
-    if (fast) {
-        // T0: the thread maxima ranked with ties by thread index form a
-        // permutation, so exactly one thread holds rank k - 1.
-        s_tkey[tid] = kmax;
-        if (tid == 0) s_nsel = 0;
-        __syncthreads();
-        int r = 0;
-        for (int j = 0; j < kBlock; ++j) {
-            const uint32_t o = s_tkey[j];
-            r += (o > kmax || (o == kmax && j < tid)) ? 1 : 0;
+            for (int d = 0; d < kJsBatch; ++d) {
+                const int64_t i0 = b0 + d * kStride;
+                if (i0 < a.K) {
+                    float v[P];
+                    vec_values<E>(tb[d], i0, a.K, v);  // past K: -inf, below every value in the vector
+                    bmax = max(bmax, E::key_of(vec_max<P>(v)));
+                    if constexpr (E::kBf16)
+                        bf16_lse_add(st, tb[d], i0, a.K, etab, tab);
+                    else
+                        lse_add<P>(st.m, st.thr, st.s1, v, tab);
+                }
+            }
+            kmax = max(kmax, bmax);
+            if (nb < kJsMaxBatches) s_bmax[nb][tid] = static_cast<uint16_t>(bmax >> (E::kKeyBits - 16));
         }
-        if (r == k - 1) s_thr = kmax;
-        __syncthreads();
-        const uint32_t T0 = s_thr;
-        for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
-            float v[P];
-            uint32_t key[P];
-            const int n = load_vec<E>(ra, i0, a.K, v, key);
+        double ml, sl;
+        row_lse_lane(st, ml, sl, tab);
+        const double lse_a = group_lse<kBlock>(ml, sl, red, tab);
+
+        bool fast = k <= kBlock;
+        if (fast) {
+            // T0: the thread maxima ranked with ties by thread index form a
+            // permutation, so exactly one thread holds rank k - 1.
+            s_tkey[tid] = kmax;
+            if (tid == 0) s_nsel = 0;
+            __syncthreads();
+            int r = 0;
+#pragma unroll 4
+            for (int j = 0; j < kBlock; j += 4) {
+                const u32x4 o = *reinterpret_cast<const u32x4 *>(&s_tkey[j]);
 #pragma unroll
-            for (int j = 0; j < P; ++j) {
-                if (j < n && key[j] >= T0) {
-                    const int slot = atomicAdd(&s_nsel, 1);
-                    if (slot < kCand) {
-                        sm.cand.idx[slot] = static_cast<int32_t>(i0 + j);
-                        sm.cand.key[slot] = key[j];
-                        sm.cand.val[slot] = v[j];
+                for (int q = 0; q < 4; ++q) r += (o[q] > kmax || (o[q] == kmax && j + q < tid)) ? 1 : 0;
+            }
+            if (r == k - 1) s_thr = kmax;
+            __syncthreads();
+            const uint32_t T0 = s_thr;
+            // The candidates are the row's elements with key >= T0, that is
+            // with value >= the value of T0 (-0 and +0 share a key and
+            // compare equal; T0 = 0 takes every element).  A thread reads
+            // again only the batches whose recorded largest key (its top 16
+            // bits, a monotone coarsening) reaches T0's, and a thread whose
+            // largest key is below T0 reads nothing.
+            const float f0 = T0 == 0 ? -INFINITY : E::value_of(T0);
+            const uint16_t t16 = static_cast<uint16_t>(T0 >> (E::kKeyBits - 16));
+            // Batches to read again: a bit per recorded batch whose largest
+            // key may reach T0, and every batch past the recorded ones.  A
+            // lane walks its own set bits, so a wave takes as many trips as
+            // its busiest lane rather than one per batch.
+            uint32_t todo = 0;
+            if (kmax >= T0)
+                for (int b = 0; b < nb && b < kJsMaxBatches; ++b)
+                    if (s_bmax[b][tid] >= t16) todo |= 1u << b;
+            int b_next = kJsMaxBatches;                         // next unrecorded batch
+            const int b_end = kmax >= T0 ? nb : kJsMaxBatches;  // unrecorded batches end here
+            while (true) {
+                int b;
+                if (todo != 0) {
+                    b = __builtin_ctz(todo);
+                    todo &= todo - 1;
+                } else if (b_next < b_end) {
+                    b = b_next++;
+                } else {
+                    break;
+                }
+                const int64_t b0 = static_cast<int64_t>(tid) * P + static_cast<int64_t>(b) * kJsBatch * kStride;
+                u32x4 tb[kJsBatch];
+                load_batch<E>(ra, b0, a.K, kStride, tb);
+#pragma unroll
+                for (int d = 0; d < kJsBatch; ++d) {
+                    const int64_t i0 = b0 + d * kStride;
+                    if (i0 < a.K) {
+                        float v[P];
+                        E::values(tb[d], v);
+                        const int64_t left = a.K - i0;
+                        const int n = left >= P ? P : static_cast<int>(left);
+#pragma unroll
+                        for (int j = 0; j < P; ++j) {
+                            if (v[j] >= f0 && j < n) {
+                                const int slot = atomicAdd(&s_nsel, 1);
+                                if (slot < kCand) {
+                                    sm.cand.idx[slot] = static_cast<int32_t>(i0 + j);
+                                    sm.cand.key[slot] = E::key_of(v[j]);
+                                    sm.cand.val[slot] = v[j];
+                                }
+                            }
+                        }
                     }
                 }
             }
-        }
-        __syncthreads();
-        const int C = s_nsel;
-        fast = C <= kCand;  // the same in every thread
-        if (fast) {
-            for (int c = tid; c < C; c += kBlock) {
-                const uint32_t kc = sm.cand.key[c];
-                const int32_t ic = sm.cand.idx[c];
-                int rank = 0;
-                for (int j = 0; j < C; ++j) {
-                    const uint32_t kj = sm.cand.key[j];
-                    rank += (kj > kc || (kj == kc && sm.cand.idx[j] < ic)) ? 1 : 0;
-                }
-                if (rank < k) {
-                    sel_idx[rank] = ic;
-                    sel_val[rank] = sm.cand.val[c];
+            __syncthreads();
+            const int C = s_nsel;
+            fast = C <= kCand;  // the same in every thread
+            if (fast) {
+                // Pad to a multiple of 4 with key 0, below every candidate.
+                if (tid < 4 && C + tid < ((C + 3) & ~3)) sm.cand.key[C + tid] = 0;
+                __syncthreads();
+                for (int c = tid; c < C; c += kBlock) {
+                    const uint32_t kc = sm.cand.key[c];
+                    const int32_t ic = sm.cand.idx[c];
+                    int rank = 0;
+                    for (int j = 0; j < C; j += 4) {
+                        const u32x4 kj = *reinterpret_cast<const u32x4 *>(&sm.cand.key[j]);
+                        const u32x4 ij = *reinterpret_cast<const u32x4 *>(&sm.cand.idx[j]);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            rank += (kj[q] > kc || (kj[q] == kc && static_cast<int32_t>(ij[q]) < ic)) ? 1 : 0;
+                    }
+                    if (rank < k) {
+                        sel_idx[rank] = ic;
+                        sel_val[rank] = sm.cand.val[c];
+                    }
                 }
             }
+            __syncthreads();
         }
-        __syncthreads();
-    }
 
-    if (!fast) {
-        // Radix select of the k-th largest key, 8 bits per pass from the top.
-        uint32_t prefix = 0;
-        int need = k;
-        for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
-            const int shift = E::kKeyBits - 8 * (pass + 1);
-            hist[tid] = 0;
+        if (!fast) {
+            // Radix select of the k-th largest key, 8 bits per pass from the top.
+            uint32_t prefix = 0;
+            int need = k;
+            for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
+                const int shift = E::kKeyBits - 8 * (pass + 1);
+                hist[tid] = 0;
+                __syncthreads();
+                for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
+                    float v[P];
+                    uint32_t key[P];
+                    const int n = load_vec<E>(ra, i0, a.K, v, key);
+                    if (pass == 0) {
+#pragma unroll
+                        for (int j = 0; j < P; ++j)
+                            if (j < n) atomicAdd(&hist[key[j] >> shift], 1u);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < P; ++j)
+                            if (j < n && (key[j] >> (shift + 8)) == prefix)
+                                atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
+                    }
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    int above = 0, bin = 255;
+                    for (; bin > 0; --bin) {
+                        if (above + static_cast<int>(hist[bin]) >= need) break;
+                        above += hist[bin];
+                    }
+                    s_prefix = (prefix << 8) | static_cast<uint32_t>(bin);
+                    s_need = need - above;
+                    s_count_eq = hist[bin];
+                }
+                __syncthreads();
+                prefix = s_prefix;
+                need = s_need;
+            }
+            const uint32_t T = prefix;
+            const int need_eq = need;
+            const bool take_all_eq = s_count_eq == need_eq;
+
+            // Collect the keys above T (and those equal to T when all of them are
+            // taken); the list order does not matter, it is sorted below.
+            if (tid == 0) s_nsel = 0;
             __syncthreads();
             for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
                 float v[P];
                 uint32_t key[P];
                 const int n = load_vec<E>(ra, i0, a.K, v, key);
-                if (pass == 0) {
 #pragma unroll
-                    for (int j = 0; j < P; ++j)
-                        if (j < n) atomicAdd(&hist[key[j] >> shift], 1u);
-                } else {
-#pragma unroll
-                    for (int j = 0; j < P; ++j)
-                        if (j < n && (key[j] >> (shift + 8)) == prefix) atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
-                }
-            }
-            __syncthreads();
-            if (tid == 0) {
-                int above = 0, bin = 255;
-                for (; bin > 0; --bin) {
-                    if (above + static_cast<int>(hist[bin]) >= need) break;
-                    above += hist[bin];
-                }
-                s_prefix = (prefix << 8) | static_cast<uint32_t>(bin);
-                s_need = need - above;
-                s_count_eq = hist[bin];
-            }
-            __syncthreads();
-            prefix = s_prefix;
-            need = s_need;
-        }
-        const uint32_t T = prefix;
-        const int need_eq = need;
-        const bool take_all_eq = s_count_eq == need_eq;
-
-        // Collect the keys above T (and those equal to T when all of them are
-        // taken); the list order does not matter, it is sorted below.
-        if (tid == 0) s_nsel = 0;
-        __syncthreads();
-        for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
-            float v[P];
-            uint32_t key[P];
-            const int n = load_vec<E>(ra, i0, a.K, v, key);
-#pragma unroll
-            for (int j = 0; j < P; ++j) {
-                if (j < n && (key[j] > T || (take_all_eq && key[j] == T))) {
-                    const int slot = atomicAdd(&s_nsel, 1);
-                    sel_idx[slot] = static_cast<int32_t>(i0 + j);
-                    sel_val[slot] = v[j];
-                }
-            }
-        }
-        __syncthreads();
-        if (!take_all_eq) {
-            // Ties straddle the threshold: take the equal keys in index order,
-            // one block sweep at a time, until need_eq are taken.
-            int remaining = need_eq;
-            for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
-                const int64_t i0 = base + static_cast<int64_t>(tid) * P;
-                float v[P];
-                uint32_t key[P];
-                int n = 0, cnt = 0;
-                if (i0 < a.K) {
-                    n = load_vec<E>(ra, i0, a.K, v, key);
-#pragma unroll
-                    for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
-                }
-                s_scan[tid] = cnt;
-                __syncthreads();
-                if (tid == 0) {
-                    int run = 0;
-                    for (int t = 0; t < kBlock; ++t) {
-                        const int c = s_scan[t];
-                        s_scan[t] = run;
-                        run += c;
+                for (int j = 0; j < P; ++j) {
+                    if (j < n && (key[j] > T || (take_all_eq && key[j] == T))) {
+                        const int slot = atomicAdd(&s_nsel, 1);
+                        sel_idx[slot] = static_cast<int32_t>(i0 + j);
+                        sel_val[slot] = v[j];
                     }
                 }
-                __syncthreads();
-                int rank = s_scan[tid];
-                if (i0 < a.K) {
+            }
+            __syncthreads();
+            if (!take_all_eq) {
+                // Ties straddle the threshold: take the equal keys in index order,
+                // one block sweep at a time, until need_eq are taken.
+                int remaining = need_eq;
+                for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
+                    const int64_t i0 = base + static_cast<int64_t>(tid) * P;
+                    float v[P];
+                    uint32_t key[P];
+                    int n = 0, cnt = 0;
+                    if (i0 < a.K) {
+                        n = load_vec<E>(ra, i0, a.K, v, key);
 #pragma unroll
-                    for (int j = 0; j < P; ++j) {
-                        if (j < n && key[j] == T) {
-                            if (rank < remaining) {
-                                const int slot = atomicAdd(&s_nsel, 1);
-                                sel_idx[slot] = static_cast<int32_t>(i0 + j);
-                                sel_val[slot] = v[j];
-                            }
-                            ++rank;
+                        for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
+                    }
+                    s_scan[tid] = cnt;
+                    __syncthreads();
+                    if (tid == 0) {
+                        int run = 0;
+                        for (int t = 0; t < kBlock; ++t) {
+                            const int c = s_scan[t];
+                            s_scan[t] = run;
+                            run += c;
                         }
                     }
+                    __syncthreads();
+                    int rank = s_scan[tid];
+                    if (i0 < a.K) {
+#pragma unroll
+                        for (int j = 0; j < P; ++j) {
+                            if (j < n && key[j] == T) {
+                                if (rank < remaining) {
+                                    const int slot = atomicAdd(&s_nsel, 1);
+                                    sel_idx[slot] = static_cast<int32_t>(i0 + j);
+                                    sel_val[slot] = v[j];
+                                }
+                                ++rank;
+                            }
+                        }
+                    }
+                    __syncthreads();
+                    const int taken_total = s_nsel;
+                    remaining = k - taken_total;
+                    __syncthreads();
                 }
-                __syncthreads();
-                const int taken_total = s_nsel;
-                remaining = k - taken_total;
-                __syncthreads();
             }
         }
-    }
 
-    // Rank sort by token index (indices are distinct), then the averaged
-    // model's log-probabilities of the selected tokens.
-    for (int t = tid; t < k; t += kBlock) {
-        const int32_t my = sel_idx[t];
-        int r = 0;
-        for (int j = 0; j < k; ++j) r += sel_idx[j] < my ? 1 : 0;
-        sm.out.idx[r] = my;
-        sm.out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
-    }
-    __syncthreads();
-    if (a.topk_out)
-        for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = sm.out.idx[t];
-
-    // JS terms, kJsGroup workers at a time so that their gathers overlap.
-    constexpr double kLog2 = 0.69314718055994530942;
-    for (int w0 = 0; w0 < a.M; w0 += kJsGroup) {
-        const int nw = a.M - w0 < kJsGroup ? a.M - w0 : kJsGroup;
-        rsrc_t rw[kJsGroup];
-        double lse_w[kJsGroup], part[kJsGroup];
-#pragma unroll
-        for (int j = 0; j < kJsGroup; ++j) {
-            // lse_m, parked in d_out by js_lse_kernel; read before the
-            // barriers of block_sum_n, overwritten with d_m(u) after them.
-            const int64_t row = static_cast<int64_t>(w0 + (j < nw ? j : 0)) * a.U + u;
-            rw[j] = js_row(a.workers, row, a.ldk, E::kElem);
-            lse_w[j] = a.d_out[row];
-            part[j] = 0.0;
-        }
+        // Rank sort by token index (indices are distinct), then the averaged
+        // model's log-probabilities of the selected tokens.
+        // Pad to a multiple of 4 with an index above every token.
+        if (tid < 4 && k + tid < ((k + 3) & ~3)) sel_idx[k + tid] = INT32_MAX;
+        __syncthreads();
         for (int t = tid; t < k; t += kBlock) {
-            const int32_t idx = sm.out.idx[t];
-            const double lq = sm.out.la[t];
-            float z[kJsGroup];
+            const int32_t my = sel_idx[t];
+            int r = 0;
+            for (int j = 0; j < k; j += 4) {
+                const u32x4 o = *reinterpret_cast<const u32x4 *>(&sel_idx[j]);
 #pragma unroll
-            for (int j = 0; j < kJsGroup; ++j) z[j] = E::at(rw[j], idx);
-#pragma unroll
-            for (int j = 0; j < kJsGroup; ++j)
-                if (j < nw) part[j] += js_term(static_cast<double>(z[j]) - lse_w[j], lq);
+                for (int q = 0; q < 4; ++q) r += static_cast<int32_t>(o[q]) < my ? 1 : 0;
+            }
+            sm.out.idx[r] = my;
+            sm.out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
         }
-        const double js = block_sum_n<kJsGroup>(part, red_n);
-        if (tid < nw) a.d_out[static_cast<int64_t>(w0 + tid) * a.U + u] = sqrt((js > 0.0 ? js : 0.0) / kLog2);
+        __syncthreads();
+        if (a.topk_out)
+            for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = sm.out.idx[t];
+
+        // JS terms, kJsGroup workers at a time: each half of the block takes
+        // kJsHalf of them over the selected tokens, so that their gathers
+        // overlap.
+        constexpr double kLog2 = 0.69314718055994530942;
+        constexpr int kHalfThreads = kBlock / 2;
+        const int half = __builtin_amdgcn_readfirstlane(tid / kHalfThreads);  // uniform in a wave
+        const int th = tid % kHalfThreads;
+        for (int w0 = 0; w0 < a.M; w0 += kJsGroup) {
+            const int nw = a.M - w0 < kJsGroup ? a.M - w0 : kJsGroup;
+            rsrc_t rw[kJsHalf];
+            double lse_w[kJsHalf], ph[kJsHalf];
+#pragma unroll
+            for (int j = 0; j < kJsHalf; ++j) {
+                // lse_m, parked in d_out by the worker-row kernel; read before
+                // the barriers of block_sum_n, overwritten with d_m(u) after.
+                const int w = half * kJsHalf + j;
+                const int64_t row = static_cast<int64_t>(w0 + (w < nw ? w : 0)) * a.U + u;
+                rw[j] = js_row(a.workers, row, a.ldk, E::kElem);
+                lse_w[j] = a.d_out[row];
+                ph[j] = 0.0;
+            }
+            for (int t = th; t < k; t += kHalfThreads) {
+                const int32_t idx = sm.out.idx[t];
+                const double lq = sm.out.la[t];
+                float z[kJsHalf];
+#pragma unroll
+                for (int j = 0; j < kJsHalf; ++j) z[j] = E::at(rw[j], idx);
+#pragma unroll
+                for (int j = 0; j < kJsHalf; ++j)
+                    if (half * kJsHalf + j < nw) ph[j] += js_term(static_cast<double>(z[j]) - lse_w[j], lq);
+            }
+            double part[kJsGroup];
+#pragma unroll
+            for (int j = 0; j < kJsHalf; ++j) {
+                part[j] = half == 0 ? ph[j] : 0.0;
+                part[kJsHalf + j] = half == 0 ? 0.0 : ph[j];
+            }
+            const double js = block_sum_n<kJsGroup>(part, red_n);
+            if (tid < nw) a.d_out[static_cast<int64_t>(w0 + tid) * a.U + u] = sqrt((js > 0.0 ? js : 0.0) / kLog2);
+        }
+        __syncthreads();  // the next token reuses the shared arrays
     }
 }
 
@@ -644,15 +968,19 @@ __global__ __launch_bounds__(256) void js_mean_kernel(const double *d, int64_t U
 }
 
 bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
-               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, hipStream_t stream) {
+               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, int num_cus, hipStream_t stream) {
     JsParams p{avg, workers, d_out, topk_out, U, K, ldk, M, k};
-    const dim3 rows(static_cast<unsigned>(U), static_cast<unsigned>(M));
     if (bf16) {
-        hipLaunchKernelGGL(js_lse_kernel<JsBF16>, rows, dim3(kBlock), 0, stream, p);
-        hipLaunchKernelGGL(js_kernel<JsBF16>, dim3(static_cast<unsigned>(U)), dim3(kBlock), 0, stream, p);
+        const int64_t groups = (static_cast<int64_t>(M) * U + kBfRowsPerBlock - 1) / kBfRowsPerBlock;
+        const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kBfBlocksPerCu) * std::max(num_cus, 1));
+        hipLaunchKernelGGL(js_lse_bf16_table_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBfBlock), 0, stream, p);
+        const int64_t tgrid = std::min<int64_t>(U, static_cast<int64_t>(kJsBlocksPerCuBf16) * std::max(num_cus, 1));
+        hipLaunchKernelGGL(js_kernel<JsBF16>, dim3(static_cast<unsigned>(tgrid)), dim3(kBlock), 0, stream, p);
     } else {
+        const dim3 rows(static_cast<unsigned>(U), static_cast<unsigned>(M));
         hipLaunchKernelGGL(js_lse_kernel<JsF32>, rows, dim3(kBlock), 0, stream, p);
-        hipLaunchKernelGGL(js_kernel<JsF32>, dim3(static_cast<unsigned>(U)), dim3(kBlock), 0, stream, p);
+        const int64_t tgrid = std::min<int64_t>(U, static_cast<int64_t>(kJsBlocksPerCuF32) * std::max(num_cus, 1));
+        hipLaunchKernelGGL(js_kernel<JsF32>, dim3(static_cast<unsigned>(tgrid)), dim3(kBlock), 0, stream, p);
     }
     if (hipGetLastError() != hipSuccess) return false;
     if (mean_out) {

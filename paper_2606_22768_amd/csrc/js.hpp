@@ -1,0 +1,16 @@
+// js.hpp -- launcher of the Jensen--Shannon functional distance kernels
+// (Sec. 4.4, JS distance; Appendix D.2).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fgd {
+
+// Launches the worker-row log-sum-exp kernel, the per-token kernel and,
+// when mean_out is given, the per-worker mean on `stream`; num_cus sizes the
+// persistent grid of the bf16 worker-row kernel.  False if a launch failed.
+bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
+               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, int num_cus, hipStream_t stream);
+
+}  // namespace fgd

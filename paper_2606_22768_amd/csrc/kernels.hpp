@@ -1267,9 +1267,5 @@ bool split_kernels_bf16(int M, int k1, int k2, bool subset, bool mix_state, Spli
 // The access-pattern reference for exact M in {1, 2, 4, 8, 16, 32, 64}: the
 // pattern_kernel instance, its lane vector and the step's blocks per CU.
 bool pattern_kernel_for(int M, bool bf16, const void **kernel, int *v, int *blocks_per_cu);
-// Jensen--Shannon distance (js.hip): launches the per-token kernel and, when
-// mean_out is given, the per-worker mean; false if a launch failed.
-bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
-               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, hipStream_t stream);
 
 }  // namespace fgd

@@ -220,6 +220,62 @@ def test_js_wide_logit_range(env, dtype):
     _check(fgd, torch, A, W, dtype, K, k)
 
 
+# bf16 bit patterns on both sides of the worker-row kernel's exp table
+# (2^-16 <= |v| < 64): inside, just outside, zeros, the smallest subnormal
+# and -inf.
+BF16_TABLE_EDGES = [0x3780, 0x377F, 0x427F, 0x4280, 0xB780, 0xB77F, 0xC27F, 0xC280,
+                    0x0000, 0x8000, 0x0001, 0x8001, 0xFF80]
+
+
+def test_js_bf16_table_edges_single_lanes(env):
+    """Rows of ordinary bf16 logits (table terms) with one value from
+    BF16_TABLE_EDGES at a different position in each row: that value's
+    vector, and only it, takes the general path for the whole wave, and the
+    two partial sums are merged.  15 rows: the last row pair of the
+    two-row blocks is half empty."""
+    fgd, torch = env
+    M, U, K, k = 3, 5, 3001, 100
+    A, W = slog.numpy_logits(M, U, K, K + 7, "bf16", seed=31)
+    for m in range(M):
+        for u in range(U):
+            r = m * U + u
+            W[m, u, (r * 613) % K] = BF16_TABLE_EDGES[r % len(BF16_TABLE_EDGES)]
+    _check(fgd, torch, A, W, "bf16", K, k)
+
+
+def test_js_bf16_table_edges_dense(env):
+    """Every edge pattern many times in every row (most vectors of the rows
+    take the general path), logits of magnitude beyond the table on whole
+    rows (only the general path), and rows within it (only the table)."""
+    fgd, torch = env
+    M, U, K, k = 4, 6, 2500, 100
+    A, W = slog.numpy_logits(M, U, K, K + 4, "bf16", seed=37)
+    rng = np.random.default_rng(41)
+    edges = np.array(BF16_TABLE_EDGES, np.uint16)
+    for m in range(M):
+        pos = rng.choice(K, 200, replace=False)
+        W[m, 0, pos] = edges[rng.integers(0, edges.size, 200)]
+    big = (rng.standard_normal((M, K)) * 3 + 100).astype(np.float32)  # |v| >= 64: general path only
+    import torch as _t
+
+    W[:, 1, :K] = _t.from_numpy(big).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    W[:, 2, : K // 2] = W[:, 1, : K // 2]  # half general, half table
+    W[:, 3, ::2] = 0xFF80                  # every other token masked
+    _check(fgd, torch, A, W, "bf16", K, k)
+
+
+def test_js_bf16_rows_beyond_the_persistent_grid(env):
+    """More worker rows than the bf16 worker-row kernel's persistent grid
+    sums at once (3 blocks of two rows per compute unit), so blocks take
+    several row pairs in turn."""
+    fgd, torch = env
+    M, U, K, k = 4, 520, 700, 50
+    A, W = slog.numpy_logits(M, U, K, K + 4, "bf16", seed=43)
+    W[1, 7, 3] = 0xFF80
+    W[2, 519, 699] = 0x4280
+    _check(fgd, torch, A, W, "bf16", K, k)
+
+
 def _random_js_case(i):
     """Seeded random JS configuration: workers, tokens, vocabulary (tiny,
     mid, large), row stride, storage, k up to 1024, and a logit kind: plain,
