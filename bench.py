@@ -142,17 +142,32 @@ def js_bench(args, fgd, torch):
     elapsed = time.perf_counter() - t0
     step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
     nbytes = (M + 1) * U * K * es
-    exps = (M + 1) * U * K  # one float64 exp per logit (plus one, rarely, when a lane's shift moves)
+    logits = (M + 1) * U * K
     ms = elapsed * 1e3 / args.steps
-    out = {"metric": "JS distance: logits HBM GB/s and float64 exp/s", "mode": "js", "value": round(nbytes / ms / 1e6, 2),
+    avg = sum(step_ms) / len(step_ms)
+    achieved = nbytes / (avg * 1e-3) / 1e9
+    lib_hash = fgd.library_source_hash()
+    wl = f"js_m{M}_u{U}_v{K}_{w['dtype']}"
+    tr = read_traffic(wl[len("js_"):], nbytes, lib_hash["js"], kernel="js")
+    out = {"metric": "JS distance: logits HBM GB/s and logits/s", "mode": "js", "value": round(nbytes / ms / 1e6, 2),
            "unit": "GB/s", "ms_per_step": round(ms, 4), "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
            "step_ms_min": round(step_ms[0], 4), "steps": args.steps, "warmup": args.warmup,
            "pct_of_hbm_peak": round(100 * nbytes / ms / 1e6 / HBM_PEAK_GBS, 2),
-           "f64_exp_per_s": round(exps / (ms * 1e-3), 1), "tokens_workers_per_s": round(M * U / (ms * 1e-3), 1),
+           "logits_per_s": round(logits / (ms * 1e-3), 1), "tokens_workers_per_s": round(M * U / (ms * 1e-3), 1),
            "cd_js": float(mean.mean().item()),
-           "config": {"workload": f"js_m{M}_u{U}_v{K}_{w['dtype']}", "workers": M, "tokens": U, "vocab": K,
+           "config": {"workload": wl, "workers": M, "tokens": U, "vocab": K,
                       "top_k": k, "dtype": w["dtype"], "bytes_per_step": nbytes},
-           "kernel_source_hash": fgd.library_source_hash()["js"], "library_source_hash": fgd.library_source_hash()}
+           # Bound: HBM.  Every logit is read once by the worker-row kernel
+           # (M of the M + 1 rows) or the per-token kernel (the averaged
+           # rows, read once more where a batch may hold a top-k candidate);
+           # most bf16 logits cost a table read instead of a float64 exp.
+           "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(achieved / HBM_PEAK_GBS, 4),
+                        "traffic": None if tr is None else tr["total_bytes"], "traffic_detail": tr,
+                        "kernel": "one fgd_js_distance call (worker-row kernel, per-token kernel, mean kernel)",
+                        "kernel_avg_ms": round(avg, 4), "bytes_per_launch": nbytes},
+           "kernel_source_hash": lib_hash["js"], "library_source_hash": lib_hash}
+    out["copy_reference_gbs"] = copy_reference(fgd, torch, A.device, args.copy_gb)
     if not args.no_cpu_baseline:
         from oracle import js as ojs
 

@@ -39,8 +39,11 @@ def numpy_logits(M, U, K, ldk=None, dtype="f32", seed=0, scale=2.0, head=48, hea
 
 
 def torch_logits(M, U, K, ldk=None, dtype="bf16", seed=0, scale=2.0, head=48, head_boost=8.0, noise=0.2,
-                 device="cuda"):
-    """The same recipe drawn on the device with torch generators (large sizes)."""
+                 device="cuda", chunk=64):
+    """The same recipe drawn on the device with torch generators (large
+    sizes), `chunk` tokens at a time: the lifted head of each token is a
+    uniformly random set of `head` tokens (the first ones of a random
+    permutation, taken as an argsort of uniform draws)."""
     import torch
 
     ldk = K if ldk is None else ldk
@@ -51,11 +54,12 @@ def torch_logits(M, U, K, ldk=None, dtype="bf16", seed=0, scale=2.0, head=48, he
     W = torch.zeros((M, U, ldk), dtype=pdt, device=device)
     h = min(head, K)
     lift = head_boost / torch.sqrt(1.0 + torch.arange(h, device=device, dtype=torch.float32))
-    for u in range(U):
-        za = torch.randn(K, generator=g, device=device) * scale
-        idx = torch.randperm(K, generator=g, device=device)[:h]
-        za[idx] += lift
-        A[u, :K] = za.to(pdt)
+    for u0 in range(0, U, chunk):
+        n = min(chunk, U - u0)
+        za = torch.randn((n, K), generator=g, device=device) * scale
+        idx = torch.rand((n, K), generator=g, device=device).argsort(dim=1)[:, :h]
+        za.scatter_add_(1, idx, lift.expand(n, h).contiguous())
+        A[u0:u0 + n, :K] = za.to(pdt)
         for m in range(M):
-            W[m, u, :K] = (za + torch.randn(K, generator=g, device=device) * noise).to(pdt)
+            W[m, u0:u0 + n, :K] = (za + torch.randn((n, K), generator=g, device=device) * noise).to(pdt)
     return A, W

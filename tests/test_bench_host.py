@@ -52,6 +52,10 @@ def test_component_hashes_cover_their_sources(tree):
     _touch(tree, "js.hip")
     h1 = _hashes(tree)
     assert h1["step"] == h0["step"] and h1["js"] != h0["js"] and h1["all"] != h0["all"]  # JS is not the step
+    _touch(tree, "js.hpp")
+    h1b = _hashes(tree)
+    assert h1b["step"] == h1["step"] and h1b["js"] != h1["js"]  # the JS launcher's header
+    h1 = h1b
     _touch(tree, "engine.hip")
     h2 = _hashes(tree)
     assert h2["step"] != h1["step"] and h2["js"] == h1["js"]  # launch code belongs to the step only

@@ -56,6 +56,10 @@ def test_js_bench_line_is_one_json_object():
     assert d["mode"] == "js" and d["unit"] == "GB/s" and d["value"] > 0
     assert d["config"]["vocab"] == 128256 and d["config"]["top_k"] == 100
     assert 0.0 < d["cd_js"] < 1.0
+    r = d["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert r["bytes_per_launch"] == 9 * 2048 * 128256 * 2 and 0.0 < r["frac"] <= 1.0
+    assert abs(r["achieved"] - r["bytes_per_launch"] / (r["kernel_avg_ms"] * 1e6)) <= 1e-3 * r["achieved"] + 0.01
 
 
 def test_packed_placement_and_split_mode_lines():
