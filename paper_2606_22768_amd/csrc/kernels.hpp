@@ -792,16 +792,31 @@ void outer_step_kernel(StepParams a) {
     const uint32_t lo = static_cast<uint32_t>(c.tid) * V;  // lane offset inside a tile, in elements
     const const_seg_ptr seg = (const_seg_ptr)(a.seg);
     int s = 0;  // first segment that ends after the tile start; tiles ascend, so it only moves forward
+    // Bounds of segment s, kept in (scalar) registers: reloaded only when s
+    // moves, so a tile's classification costs no memory access.
+    int64_t s_begin = 0, s_end = 0;
+    if constexpr (SUB) {
+        if (a.n_seg > 0) {
+            s_begin = seg[0];
+            s_end = seg[1];
+        }
+    }
     for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
         const int64_t tb = tile * kTile;  // first parameter of the tile (uniform)
         uint32_t keep = 0;                // elements of this lane outside the Mix2 subset
         if constexpr (SUB) {
             if (a.n_seg > 0) {
                 const int64_t te = tb + kTile < a.P ? tb + kTile : a.P;
-                while (s < a.n_seg && seg[2 * s + 1] <= tb) ++s;
-                if (s == a.n_seg || seg[2 * s] >= te) {
+                while (s < a.n_seg && s_end <= tb) {
+                    ++s;
+                    if (s < a.n_seg) {
+                        s_begin = seg[2 * s];
+                        s_end = seg[2 * s + 1];
+                    }
+                }
+                if (s == a.n_seg || s_begin >= te) {
                     keep = (1u << V) - 1u;  // wholly outside
-                } else if (seg[2 * s] <= tb && seg[2 * s + 1] >= te) {
+                } else if (s_begin <= tb && s_end >= te) {
                     keep = 0u;  // wholly inside
                 } else {
                     keep = (1u << V) - 1u;
