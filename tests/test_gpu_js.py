@@ -276,6 +276,27 @@ def test_js_bf16_rows_beyond_the_persistent_grid(env):
     _check(fgd, torch, A, W, "bf16", K, k)
 
 
+@pytest.mark.parametrize("dtype,K", [("f32", 140_003), ("bf16", 270_001)])
+def test_js_rows_beyond_the_recorded_batches(env, dtype, K):
+    """Vocabularies long enough that a thread of the per-token kernel reads
+    more than the 16 batches of 8 vectors whose maxima it records, so the
+    candidate pass must read every batch past them too; a head of large
+    logits placed at the row's end lands in those batches."""
+    fgd, torch = env
+    M, U, k = 2, 3, 100
+    A, W = slog.numpy_logits(M, U, K, -(-K // 8) * 8, "f32", seed=K)  # 16-byte rows in both storages
+    rng = np.random.default_rng(K)
+    tail = rng.choice(np.arange(K - 20_000, K), 150, replace=False)
+    A[:, tail] += 12.0
+    W[:, :, tail] += 12.0
+    if dtype == "bf16":
+        import torch as _t
+
+        A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+        W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
 def _random_js_case(i):
     """Seeded random JS configuration: workers, tokens, vocabulary (tiny,
     mid, large), row stride, storage, k up to 1024, and a logit kind: plain,
