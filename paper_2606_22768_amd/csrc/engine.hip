@@ -213,6 +213,14 @@ int64_t tiles_of(int64_t P, int v) {
     return (P + per - 1) / per;
 }
 
+// Resident blocks per CU of the standalone consensus kernel, a read-only
+// stream of every row.  Up to 16 workers a lane already has a load of every
+// row in flight and more blocks only add DRAM contention (8 x 1.1e9 bf16:
+// 2.69 ms with 2 blocks, 2.72 with 4, 2.89 with 8, 4.32 with 1); with more
+// workers a lane holds one parameter and the occupancy covers the latency
+// (64 x 124M f32: 5.05 ms with 8, 5.16 with 2).
+constexpr int consensus_blocks_per_cu(int num_workers) { return num_workers <= 16 ? 2 : 8; }
+
 fgd_status grid_for_cus(int num_cus, const void *kernel, size_t lds, int64_t ntiles, int &grid,
                         int cap = kMaxBlocksPerCu) {
     int per_cu = 0;
@@ -937,7 +945,8 @@ fgd_status fgd_consensus_distance(fgd_engine *e, const void *x, int32_t dtype, d
     p.M = c.num_workers;
     p.partials = e->d_partials;
     int grid = 0;
-    if (fgd_status st = grid_for(e, ks.consensus, 0, p.ntiles, grid)) return st;
+    if (fgd_status st = grid_for(e, ks.consensus, 0, p.ntiles, grid, consensus_blocks_per_cu(c.num_workers)))
+        return st;
     if (static_cast<size_t>(grid) * c.num_workers > e->partials_capacity)
         return fail(FGD_ERR_UNSUPPORTED, "consensus scratch too small");
     if (fgd_status st = launch(ks.consensus, grid, 0, stream, &p)) return st;
@@ -972,7 +981,8 @@ fgd_status fgd_consensus_distance_noalloc(int32_t num_workers, int64_t num_param
     p.M = num_workers;
     p.partials = partials;
     int grid = 0;
-    if (fgd_status st = grid_for_cus(num_cus, ks.consensus, 0, p.ntiles, grid)) return st;
+    if (fgd_status st = grid_for_cus(num_cus, ks.consensus, 0, p.ntiles, grid, consensus_blocks_per_cu(num_workers)))
+        return st;
     // The grid of fgd_consensus_distance (so the same sums in the same
     // order), capped to the blocks the scratch holds on a larger device.
     grid = std::min(grid, kNoAllocDoubles / num_workers);
