@@ -297,6 +297,28 @@ def test_js_rows_beyond_the_recorded_batches(env, dtype, K):
     _check(fgd, torch, A, W, dtype, K, k)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_row_padding_is_never_used(env, dtype):
+    """Elements in [K, ldk) of every row are read with the vectors that
+    straddle K but never enter a sum, a maximum or the selection: padding of
+    NaN, +-inf and huge values gives the same distances and token sets as
+    zero padding."""
+    fgd, torch = env
+    M, U, K, k = 3, 4, 1001, 100
+    per = 8 if dtype == "bf16" else 4
+    ldk = -(-K // per) * per + per  # a ragged last vector and one whole vector of padding
+    A, W = slog.numpy_logits(M, U, K, ldk, dtype, seed=61)
+    d0, m0, t0 = _run(fgd, torch, A, W, dtype, K, k)
+    junk = np.array([0x7FC0, 0x7F80, 0xFF80, 0x7F7F, 0xFF7F], np.uint16) if dtype == "bf16" else \
+        np.array([np.nan, np.inf, -np.inf, 3e38, -3e38], np.float32)
+    pad = np.resize(junk, ldk - K)
+    A[:, K:] = pad
+    W[:, :, K:] = pad
+    d1, m1, t1 = _run(fgd, torch, A, W, dtype, K, k)
+    assert np.array_equal(t0, t1)
+    assert np.array_equal(d0, d1) and np.array_equal(m0, m1)
+
+
 def _random_js_case(i):
     """Seeded random JS configuration: workers, tokens, vocabulary (tiny,
     mid, large), row stride, storage, k up to 1024, and a logit kind: plain,
