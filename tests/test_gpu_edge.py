@@ -11,6 +11,9 @@ dropped for a round, and subnormal float32 values, through the C ABI.
                  momentum propagate exactly where the oracle's do: the same
                  elements of theta' and v' are NaN or infinite (with the same
                  sign), and so are the same consensus entries.
+  row padding    elements in [P, ld) of every row are read with the lane
+                 vectors that straddle P but never enter the step, its sums
+                 or its consensus, and are never written.
   subnormal      float32 subnormals are kept, not flushed: with g0 = 0 the
                  momentum update v' = mu v is one rounding of an exact product
                  on both sides, so v' matches the oracle bit for bit; with
@@ -286,3 +289,41 @@ def test_subnormal_parameters_exact_step(env, dtype):
         assert np.array_equal(got_t[:, :P].view(np.uint32), ref_t[:, :P].view(np.uint32))
     else:
         assert np.array_equal(got_t[:, :P], ref_t[:, :P])
+
+
+PAD_CASES = [
+    # (M, P, dtype, mix1, k1, mix2, k2): the lane-per-parameter kernel and the worker-group kernel
+    (8, 3 * 1024 + 5, "bf16", G, 1, RING_MH, 1),
+    (8, 777, "f32", G, 1, RING_MH, 1),
+    (64, 2 * 256 + 3, "f32", REG4, 1, REG4, 3),
+]
+
+
+@pytest.mark.parametrize("case", PAD_CASES, ids=lambda c: f"M{c[0]}-P{c[1]}-{c[2]}")
+def test_row_padding_is_never_used(env, case):
+    """NaN, infinities and huge values in [P, ld) of theta_prev, theta_local
+    and the momentum give bit-identical outputs and consensus rows to zero
+    padding, and stay as they were."""
+    fgd, torch = env
+    M, P, dtype, s1, k1, s2, k2 = case
+    ld = pa.aligned_ld(P) + 8  # a ragged last lane vector and whole vectors of padding
+    tp, tl, v = tensors.numpy_inputs(M, P, ld=ld, dtype=dtype, seed=5)
+    for a in (tp, tl, v):
+        a[:, P:] = 0
+    t1, t2 = pa.topo(s1, M, k1, 3), pa.topo(s2, M, k2, 4)
+    ref = pa.run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp.copy(), tl.copy(), v.copy())
+    junk = np.array([np.nan, np.inf, -np.inf, 3e38, -3e38], np.float32)
+    for a in (tp, tl, v):
+        fill = np.resize(junk, a[:, P:].shape)
+        a[:, P:] = tensors.f32_to_bf16_bits(fill) if a.dtype == np.uint16 else fill
+    got = pa.run_engine(fgd, torch, M, P, ld, dtype, t1, t2, tp.copy(), tl.copy(), v.copy())
+    for r, g, what in zip(ref, got, ("theta'", "v'", "consensus rows")):
+        r, g = np.asarray(r), np.asarray(g)
+        if what == "consensus rows":
+            assert np.array_equal(r, g), what
+        else:
+            assert np.array_equal(r[:, :P], g[:, :P]), what
+    # bit patterns: NaN padding compares unequal to itself as floats
+    bits = lambda a: np.ascontiguousarray(a).view(np.uint16 if a.dtype == np.uint16 else np.uint32)
+    assert np.array_equal(bits(np.asarray(got[0])[:, P:]), bits(tp[:, P:]))
+    assert np.array_equal(bits(np.asarray(got[1])[:, P:]), bits(v[:, P:]))
