@@ -124,10 +124,11 @@ def js_bench(args, fgd, torch):
     A, W = slog.torch_logits(M, U, K, K, w["dtype"], seed=w["seed"])
     d = torch.empty((M, U), dtype=torch.float64, device=A.device)
     mean = torch.empty(M, dtype=torch.float64, device=A.device)
+    ws = torch.empty(fgd.fgd_js_workspace_size(w["dtype"], M, U), dtype=torch.uint8, device=A.device)
     stream = torch.cuda.current_stream()
 
     def step():
-        fgd.fgd_js_distance(A, W, w["dtype"], M, U, K, K, k, d, mean, None, stream)
+        fgd.fgd_js_distance(A, W, w["dtype"], M, U, K, K, k, d, mean, None, ws, None, stream)
 
     for _ in range(args.warmup):
         step()
@@ -157,14 +158,15 @@ def js_bench(args, fgd, torch):
            "cd_js": float(mean.mean().item()),
            "config": {"workload": wl, "workers": M, "tokens": U, "vocab": K,
                       "top_k": k, "dtype": w["dtype"], "bytes_per_step": nbytes},
-           # Bound: HBM.  Every logit is read once by the worker-row kernel
-           # (M of the M + 1 rows) or the per-token kernel (the averaged
-           # rows, read once more where a batch may hold a top-k candidate);
-           # most bf16 logits cost a table read instead of a float64 exp.
+           # Bound: HBM.  Every logit is read once by the row kernel (all
+           # M + 1 rows per token); the per-token kernel reads the averaged
+           # rows once more only where a batch may hold a top-k candidate,
+           # and gathers the workers' logits of the selected tokens.  Most
+           # bf16 logits cost a table read instead of a float64 exp.
            "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(achieved / HBM_PEAK_GBS, 4),
                         "traffic": None if tr is None else tr["total_bytes"], "traffic_detail": tr,
-                        "kernel": "one fgd_js_distance call (worker-row kernel, per-token kernel, mean kernel)",
+                        "kernel": "one fgd_js_distance call (row kernel, per-token kernel, mean kernel)",
                         "kernel_avg_ms": round(avg, 4), "bytes_per_launch": nbytes},
            "kernel_source_hash": lib_hash["js"], "library_source_hash": lib_hash}
     out["copy_reference_gbs"] = copy_reference(fgd, torch, A.device, args.copy_gb)

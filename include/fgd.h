@@ -370,19 +370,32 @@ fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count);
  *                   starts at element (m * U + u) * ldk
  *   dtype           FGD_F32 or FGD_BF16; logits must not be NaN or +inf
  *                   (-inf, a masked token, is allowed)
- *   num_workers     M in [1, FGD_MAX_JS_WORKERS]; num_tokens U >= 1
+ *   num_workers     M in [1, FGD_MAX_JS_WORKERS]; num_tokens U in [1, 2^31)
  *   vocab, ldk      K <= ldk; ldk * elem_size a multiple of 16 (16-byte
- *                   aligned rows); elements [K, ldk) are read, never used
+ *                   aligned rows) and below 2^31 bytes; elements [K, ldk)
+ *                   are read, never used
  *   top_k           in [1, min(K, FGD_MAX_JS_TOPK)]
- *   d_out           device double[M][U]: d_m(u) (between the call's two
- *                   kernels it holds the workers' log-sum-exps)
+ *   d_out           device double[M][U]: d_m(u)
  *   mean_out        device double[M] or NULL: the mean of d_m(u) over u
  *                   (the paper's CD_JS is the mean of these M values)
  *   topk_out        device int32[U][top_k] or NULL: T(u) in ascending order
- * Enqueued on `stream`; deterministic. */
+ *   workspace       device memory of at least fgd_js_workspace_size bytes,
+ *                   16-byte aligned, owned by the caller, overlapping none
+ *                   of the arrays above; the call leaves it undefined (it
+ *                   carries each row's log-sum-exp parts and the averaged
+ *                   rows' per-thread batch maxima from the call's first
+ *                   kernel to its second)
+ * Enqueued on `stream`; deterministic.  Calls that share a workspace must
+ * not run concurrently. */
 fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, int32_t dtype, int32_t num_workers,
                            int64_t num_tokens, int64_t vocab, int64_t ldk, int32_t top_k, double *d_out,
-                           double *mean_out, int32_t *topk_out, void *stream);
+                           double *mean_out, int32_t *topk_out, void *workspace, int64_t workspace_bytes,
+                           void *stream);
+
+/* Device workspace fgd_js_distance needs for these sizes: 64 bytes per row
+ * ((M + 1) U rows) and 4 KiB (bfloat16) or 8 KiB (float32) per token.  Host
+ * only. */
+fgd_status fgd_js_workspace_size(int32_t dtype, int32_t num_workers, int64_t num_tokens, int64_t *bytes);
 
 /* Streaming reference with the fused step's memory traffic and none of its
  * arithmetic: the tiles, lane vectors, cache hints and launch shape of

@@ -80,7 +80,8 @@ def _load():
         "fgd_read_timing": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
         "fgd_stream_copy": (I32, [P, P, I64, P]),
         "fgd_stream_step_pattern": (I32, [P, P, P, P, P]),
-        "fgd_js_distance": (I32, [P, P, I32, I32, I64, I64, I64, I32, P, P, P, P]),
+        "fgd_js_distance": (I32, [P, P, I32, I32, I64, I64, I64, I32, P, P, P, P, I64, P]),
+        "fgd_js_workspace_size": (I32, [I32, I32, I64, ctypes.POINTER(I64)]),
         "fgd_status_string": (ctypes.c_char_p, [I32]),
         "fgd_last_error": (ctypes.c_char_p, []),
         "fgd_source_hash": (ctypes.c_char_p, [I32]),
@@ -290,17 +291,31 @@ def fgd_read_timing(h):
     return ms.value, n.value
 
 
+def fgd_js_workspace_size(dtype, num_workers, num_tokens) -> int:
+    n = ctypes.c_int64()
+    _check(lib.fgd_js_workspace_size(DTYPES.get(dtype, dtype), int(num_workers), int(num_tokens), ctypes.byref(n)),
+           "fgd_js_workspace_size")
+    return n.value
+
+
 def fgd_js_distance(logits_avg, logits_workers, dtype, num_workers, num_tokens, vocab, ldk, top_k, d_out,
-                    mean_out=None, topk_out=None, stream=None):
+                    mean_out=None, topk_out=None, workspace=None, workspace_bytes=None, stream=None):
+    """The C call; `workspace` is device memory of at least
+    fgd_js_workspace_size bytes (a tensor's size is taken when
+    workspace_bytes is None)."""
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.fgd_js_distance(_dev(logits_avg), _dev(logits_workers), DTYPES.get(dtype, dtype), int(num_workers),
                                int(num_tokens), int(vocab), int(ldk), int(top_k), _dev(d_out), _dev(mean_out),
-                               _dev(topk_out), _stream(stream)), "fgd_js_distance")
+                               _dev(topk_out), _dev(workspace), int(workspace_bytes), _stream(stream)),
+           "fgd_js_distance")
 
 
 def js_distance(logits_avg, logits_workers, top_k=100, vocab=None, d_out=None, mean_out=None, topk_out=None,
-                stream=None):
+                workspace=None, stream=None):
     """Tensor-level call: logits_avg [U][ldk], logits_workers [M][U][ldk]
-    (float32 or bfloat16, rows contiguous); returns (d [M][U], mean [M])."""
+    (float32 or bfloat16, rows contiguous); returns (d [M][U], mean [M]).
+    The workspace (a uint8 device tensor) is allocated when not given."""
     import torch
 
     dtype = {torch.float32: "f32", torch.bfloat16: "bf16"}[logits_avg.dtype]
@@ -315,7 +330,10 @@ def js_distance(logits_avg, logits_workers, top_k=100, vocab=None, d_out=None, m
     dev = logits_avg.device
     d_out = torch.empty((M, U), dtype=torch.float64, device=dev) if d_out is None else d_out
     mean_out = torch.empty(M, dtype=torch.float64, device=dev) if mean_out is None else mean_out
-    fgd_js_distance(logits_avg, logits_workers, dtype, M, U, K, ldk, top_k, d_out, mean_out, topk_out, stream)
+    if workspace is None:
+        workspace = torch.empty(fgd_js_workspace_size(dtype, M, U), dtype=torch.uint8, device=dev)
+    fgd_js_distance(logits_avg, logits_workers, dtype, M, U, K, ldk, top_k, d_out, mean_out, topk_out, workspace,
+                    None, stream)
     return d_out, mean_out
 
 

@@ -5,29 +5,41 @@
 // For token u, in float64 and in the log domain:
 //   lse_m      = log sum_i exp(z_m,i)               every worker row
 //   lse_a      = log sum_i exp(zbar_i)              the averaged model's row
-//   T          = the k largest zbar_i (ties: lower index first), found by a
-//                radix select over order-preserving integer keys of the
-//                stored logits (exact comparisons: no rounding decides it)
+//   T          = the k largest zbar_i (ties: lower index first), selected on
+//                order-preserving integer keys of the stored logits (exact
+//                comparisons: no rounding decides it)
 //   JS_m       = sum over i in T of the per-token terms
 //                1/2 p (lp - lmix) + 1/2 q (lq - lmix), lp = z_m,i - lse_m,
 //                lq = zbar_i - lse_a, lmix = log((p + q) / 2)
 //   d_m(u)     = sqrt(max(JS_m, 0) / log 2)
 // Probabilities are those of the full softmax; only the sum is restricted to
-// T.  Two kernels: the worker-row kernel computes every lse_m (M of the
-// M + 1 rows per token, the bulk of the work) and parks it in d_out;
-// js_kernel takes one token per block: the averaged row, the selection and
-// the JS terms, and overwrites d_out with d_m(u).
+// T.  Kernels, in order on the call's stream, with a caller workspace between
+// them:
+//   js_rows_kernel         streams all (M + 1) U rows once (persistent, no
+//                          barriers): per row, each wave's (shift, sum) part
+//                          of the log-sum-exp; per averaged row, each row
+//                          thread's largest key and its batches' largest keys
+//   js_token_wave_kernel   (k <= 256) one wave per token: the averaged row's
+//                          lse from its parts, the selection (a threshold from
+//                          the row threads' maxima, a second read of only the
+//                          batches that reach it), the JS terms; a token with
+//                          too many candidates is flagged
+//   js_token_radix_kernel  per token, a radix select over the whole row: every
+//                          token when k > 256, else only the flagged ones
+//   js_mean_kernel         the per-worker mean of d
 //
-// Worker rows.  bf16 logits take only 65536 bit patterns, and the exp of
-// every bf16 value v with 2^-16 <= |v| < 64 (22 binades, both signs: 5632
-// values) is a table of 44 KB in LDS, filled once per block with the
-// library's float64 exp.  Such terms need no shift: each is below e^64, so
-// their plain sum cannot overflow; a term costs an index from the bit
-// pattern, one LDS read and one add.  A 16-byte vector of logits in which
-// any lane of the wave holds another value (0, |v| < 2^-16, |v| >= 64,
-// -inf, or the ragged end of the row) goes through the general path below,
-// whose shifted sum is merged with the table sum at the end of the row.
-// float32 logits always take the general path.
+// Rows.  bf16 logits take only 65536 bit patterns, and the exp of every bf16
+// value v with 2^-16 <= |v| < 64 (22 binades, both signs: 5632 values) is a
+// table of 44 KB in LDS, filled once per block with the library's float64
+// exp.  Such terms need no shift: each is below e^64, so their plain sum
+// cannot overflow; a term costs an index from the bit pattern, one LDS read
+// and one add.  A 16-byte vector of logits in which any lane of the wave
+// holds another value (0, |v| < 2^-16, |v| >= 64, -inf, or the ragged end of
+// the row) goes through the general path below, whose shifted sum is merged
+// with the table sum at the end of the row.  float32 logits always take the
+// general path.  The averaged rows and the worker rows run the same sums in
+// the same lane order, so a worker whose logits equal the averaged model's
+// gets exactly d = 0.
 //
 // General path.  The log-sum-exp of a row is a (shift, scaled sum)
 // reduction: the shift is a lane's first finite value and moves only when a
@@ -41,14 +53,15 @@
 // entry is stored with j << 12 already subtracted from its high word, so
 // adding n << 12 leaves the mantissa alone and adds n >> 8 to the
 // exponent); x is clamped at -708 so that the scaled entry stays a normal
-// double.  Lanes are combined through the block's largest shift (one exp
-// per lane, no pairwise rescaling).  Every reduction has a fixed order, so
-// results are deterministic.  The selected indices are rank-sorted so that
-// the JS sum runs in index order.
+// double.  Lanes, then a row's waves, are combined through the largest
+// shift (one exp per part, no pairwise rescaling).  Every reduction has a
+// fixed order, so results are deterministic.  The selected indices are
+// rank-sorted so that the JS sum runs in index order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "js.hpp"
 #include "kernels.hpp"
@@ -84,9 +97,8 @@ struct JsF32 {
 #pragma unroll
         for (int j = 0; j < 4; ++j) v[j] = __uint_as_float(t[j]);
     }
-    __device__ static float at(rsrc_t r, int64_t i) {
-        return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, static_cast<uint32_t>(i * 4), 0, 0));
-    }
+    // Element i of the row that starts at `row` (a gather).
+    __device__ static float at_ptr(const char *row, int64_t i) { return reinterpret_cast<const float *>(row)[i]; }
     // The key of a value, and the value of a key that some value has.
     __device__ static uint32_t key_of(float v) {
         uint32_t b = __float_as_uint(v);
@@ -117,9 +129,9 @@ struct JsBF16 {
             v[2 * j + 1] = __uint_as_float(t[j] & 0xFFFF0000u);
         }
     }
-    __device__ static float at(rsrc_t r, int64_t i) {
-        const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(r, static_cast<uint32_t>(i * 2), 0, 0);
-        return __uint_as_float(h << 16);
+    // Element i of the row that starts at `row` (a gather).
+    __device__ static float at_ptr(const char *row, int64_t i) {
+        return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t *>(row)[i]) << 16);
     }
     // The key of a value (a bf16 widened to float), and the value of a key
     // that some value has.
@@ -143,18 +155,6 @@ __device__ inline double shfl_xor_d(double x, int mask) {
     const int lo = __shfl_xor(static_cast<int>(b & 0xFFFFFFFF), mask);
     const int hi = __shfl_xor(static_cast<int>(b >> 32), mask);
     return __longlong_as_double((static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo));
-}
-
-// Block-wide sum in a fixed order; every thread gets the result.
-__device__ inline double block_sum(double x, double *red) {
-    for (int o = kWave / 2; o > 0; o >>= 1) x += shfl_xor_d(x, o);
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    __syncthreads();
-    if (lane == 0) red[wave] = x;
-    __syncthreads();
-    double t = red[0];
-    for (int w = 1; w < kWavesPerBlock; ++w) t += red[w];
-    return t;
 }
 
 // ------------------------------------------------------------ float64 exp
@@ -357,65 +357,9 @@ __device__ inline void lse_add(double &m, float &thr, double &s, const float (&v
     s += e[0];
 }
 
-// log-sum-exp over the threads [g * G, (g + 1) * G) of the block (G a
-// multiple of the wave, g the caller's group) from per-thread (m, s): the
-// group's largest shift M, then sum s exp(m - M) in a fixed order; every
-// thread of the group gets the result.  Block-wide barriers: every thread
-// of the block calls it.  `red` holds 2 doubles per wave of the block.
-template <int G>
-__device__ inline double group_lse(double m, double s, double *red, const double *tab) {
-    constexpr int kW = G / kWave;
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave, g0 = (threadIdx.x / G) * kW;
-    double M = m;
-    for (int o = kWave / 2; o > 0; o >>= 1) M = fmax(M, shfl_xor_d(M, o));
-    __syncthreads();
-    if (lane == 0) red[2 * wave] = M;
-    __syncthreads();
-    M = red[2 * g0];
-    for (int w = 1; w < kW; ++w) M = fmax(M, red[2 * (g0 + w)]);
-    double t = s == 0.0 ? 0.0 : s * exp_table(m - M, tab);
-    for (int o = kWave / 2; o > 0; o >>= 1) t += shfl_xor_d(t, o);
-    if (lane == 0) red[2 * wave + 1] = t;
-    __syncthreads();
-    double S = red[2 * g0 + 1];
-    for (int w = 1; w < kW; ++w) S += red[2 * (g0 + w) + 1];
-    return S == 0.0 ? -INFINITY : M + log(S);
-}
-
 // A lane's (shift, sum) at the end of a row: an empty lane reports no terms.
 __device__ inline void lane_state(double &m, double &s) {
     if (m == kLseEmpty) s = 0.0;
-}
-
-// lse of worker rows, general path (float32 logits): one row per block
-// (token blockIdx.x, worker blockIdx.y) into d_out[w][u]; the next vector of
-// the row is loaded while the current one is summed.
-template <class E>
-__global__ __launch_bounds__(kBlock) void js_lse_kernel(JsParams a) {
-    constexpr int P = E::kPer;
-    constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;
-    __shared__ double tab[kTab];
-    __shared__ double red[2 * kWavesPerBlock];
-    load_exp_table(tab);
-    const int64_t row = static_cast<int64_t>(blockIdx.y) * a.U + blockIdx.x;
-    const rsrc_t r = js_row(a.workers, row, a.ldk, E::kElem);
-    double m = kLseEmpty, s = 0.0;
-    float thr = -INFINITY;
-    int64_t i0 = static_cast<int64_t>(threadIdx.x) * P;
-    u32x4 nxt = {0, 0, 0, 0};
-    if (i0 < a.K) nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy);
-    for (; i0 < a.K; i0 += kStride) {
-        const u32x4 cur = nxt;
-        if (i0 + kStride < a.K)
-            nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * E::kElem), 0,
-                                                        kLoadPolicy);
-        float v[P];
-        vec_values<E>(cur, i0, a.K, v);
-        lse_add<P>(m, thr, s, v, tab);
-    }
-    lane_state(m, s);
-    const double lse = group_lse<kBlock>(m, s, red, tab);
-    if (threadIdx.x == 0) a.d_out[row] = lse;
 }
 
 // ------------------------------------------------ bf16 rows: exp table
@@ -424,10 +368,6 @@ constexpr int kBfTabE1 = 132;                              // exponent field of 
 constexpr uint32_t kBfTabLo = kBfTabE0 << 7;               // first magnitude pattern in the table
 constexpr uint32_t kBfTabN = (kBfTabE1 - kBfTabE0 + 1) << 7;  // magnitudes per sign (2816)
 constexpr int kBfTabEntries = 2 * kBfTabN;
-constexpr int kBfRowThreads = kBlock;                      // threads per row (js_kernel's block)
-constexpr int kBfRowsPerBlock = 2;                         // rows a worker-row block sums at once
-constexpr int kBfBlock = kBfRowThreads * kBfRowsPerBlock;
-constexpr int kBfBlocksPerCu = 3;                          // LDS: 3 x 47 KB of the CU's 160 KB
 
 // Entry 2 (a - kBfTabLo) + s = exp of the bf16 value with magnitude
 // pattern a and sign s, from the library's float64 exp.  Block-wide, no
@@ -506,285 +446,285 @@ __device__ inline void row_lse_lane(RowLse st, double &ml, double &sl, const dou
     }
 }
 
-// Worker rows of bf16 logits, persistent: block b sums rows 2p and 2p + 1
-// for p = b, b + gridDim.x, ...; thread lt of a row takes the same elements
-// as thread lt of js_kernel does on the averaged row.
-__global__ __launch_bounds__(kBfBlock) __attribute__((amdgpu_waves_per_eu(6, 8)))
-void js_lse_bf16_table_kernel(JsParams a) {
-    constexpr int P = JsBF16::kPer;
-    constexpr int64_t kStride = static_cast<int64_t>(kBfRowThreads) * P;
-    __shared__ double etab[kBfTabEntries];
-    __shared__ double tab[kTab];
-    __shared__ double red[2 * kBfBlock / kWave];
-    fill_bf16_exp_table(etab);
-    load_exp_table(tab);  // its barrier also covers etab
-    const int g = threadIdx.x / kBfRowThreads, lt = threadIdx.x % kBfRowThreads;
-    const int64_t rows = static_cast<int64_t>(a.M) * a.U;
-    const int64_t groups = (rows + kBfRowsPerBlock - 1) / kBfRowsPerBlock;
-    for (int64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
-        const int64_t row = grp * kBfRowsPerBlock + g;
-        const bool valid = row < rows;
-        RowLse st;
-        if (valid) {
-            const rsrc_t r = js_row(a.workers, row, a.ldk, JsBF16::kElem);
-            int64_t i0 = static_cast<int64_t>(lt) * P;
-            u32x4 nxt = {0, 0, 0, 0};
-            if (i0 < a.K) nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i0 * 2), 0, kLoadPolicy);
-            for (; i0 < a.K; i0 += kStride) {
-                const u32x4 cur = nxt;
-                if (i0 + kStride < a.K)
-                    nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * 2), 0,
-                                                                kLoadPolicy);
-                bf16_lse_add(st, cur, i0, a.K, etab, tab);
-            }
-        }
-        double ml, sl;
-        row_lse_lane(st, ml, sl, tab);
-        const double lse = group_lse<kBfRowThreads>(ml, sl, red, tab);
-        if (valid && lt == 0) a.d_out[row] = lse;
-    }
-}
-
-// One token's term of the JS sum from the two log-probabilities; a side of
-// probability 0 adds nothing (0 log 0 = 0).
+// One token's term of the JS sum, 1/2 p log(p / mix) + 1/2 q log(q / mix),
+// from the two log-probabilities.  With hi >= lo the larger and smaller of
+// them and r = exp(lo - hi): log mix = hi + log1p(r) - log 2, so the term is
+// 1/2 exp(hi) [(log 2 - log1p(r)) + r ((lo - hi) + log 2 - log1p(r))].  A
+// side of probability 0 adds nothing (0 log 0 = 0), and equal sides add
+// exactly 0 (p = q = mix).
 __device__ inline double js_term(double lp, double lq) {
     constexpr double kLog2 = 0.69314718055994530942;
     const double hi = lp > lq ? lp : lq, lo = lp > lq ? lq : lp;
-    if (hi == -INFINITY) return 0.0;  // probability 0 on both sides
-    const double lmix = hi + log1p(exp(lo - hi)) - kLog2;
-    double t = 0.0;
-    if (lp != -INFINITY) t += 0.5 * exp(lp) * (lp - lmix);
-    if (lq != -INFINITY) t += 0.5 * exp(lq) * (lq - lmix);
-    return t;
-}
-
-// Block-wide sums of N values per thread in a fixed order: thread j < N
-// returns the sum of everyone's x[j]; the others return 0.
-template <int N>
-__device__ inline double block_sum_n(double (&x)[N], double *red) {
-    for (int o = kWave / 2; o > 0; o >>= 1)
-#pragma unroll
-        for (int j = 0; j < N; ++j) x[j] += shfl_xor_d(x[j], o);
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    __syncthreads();
-    if (lane == 0)
-#pragma unroll
-        for (int j = 0; j < N; ++j) red[wave * N + j] = x[j];
-    __syncthreads();
-    double t = 0.0;
-    if (threadIdx.x < N) {
-        t = red[threadIdx.x];
-        for (int w = 1; w < kWavesPerBlock; ++w) t += red[w * N + threadIdx.x];
-    }
-    return t;
+    if (hi == -INFINITY || lo == hi) return 0.0;
+    const double r = exp(lo - hi);  // 0 when lo = -inf
+    const double c = kLog2 - log1p(r);
+    double t = c;
+    if (r != 0.0) t += r * ((lo - hi) + c);
+    return 0.5 * exp(hi) * t;
 }
 
 constexpr int kJsGroup = 8;  // workers whose logits are gathered together
-constexpr int kJsHalf = kJsGroup / 2;  // of them, per half of the block
-#ifndef FGD_JS_BATCH
-#define FGD_JS_BATCH 8
-#endif
-constexpr int kJsBatch = FGD_JS_BATCH;  // vectors of the averaged row a thread loads before using them
-constexpr int kJsMaxBatches = 16;       // batches per thread whose largest keys js_kernel records
+constexpr int kJsBatch = 4;   // vectors of the averaged row a thread loads before using them
 
-// Loads the vectors of a row at i0, i0 + stride, ... (kJsBatch of them) so
-// that their latencies overlap; those at or past K read as zero and are
-// never used.
+// Loads the vectors of a row at i0, i0 + stride, ... (the first nd <=
+// kJsBatch of them) so that their latencies overlap; the others, and those
+// at or past K, read as zero and are never used.
 template <class E>
-__device__ inline void load_batch(rsrc_t r, int64_t i0, int64_t K, int64_t stride, u32x4 (&t)[kJsBatch]) {
+__device__ inline void load_batch(rsrc_t r, int64_t i0, int64_t K, int64_t stride, int nd, u32x4 (&t)[kJsBatch]) {
 #pragma unroll
     for (int d = 0; d < kJsBatch; ++d) {
         const int64_t i = i0 + d * stride;
         t[d] = u32x4{0, 0, 0, 0};
-        if (i < K) t[d] = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i * E::kElem), 0, kLoadPolicy);
+        if (d < nd && i < K)
+            t[d] = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i * E::kElem), 0, kLoadPolicy);
     }
 }
-// Resident blocks of js_kernel per CU (its persistent grid): LDS bounds the
-// bf16 kernel (79 KB with the exp table), registers the float32 one.
-constexpr int kJsBlocksPerCuBf16 = 2;
-constexpr int kJsBlocksPerCuF32 = 2;
+// ------------------------------------------------------------ workspace
+// Between the call's two kernels: per row, the (shift, sum) of each of its
+// kRowWaves waves; per token, the averaged row's largest key in each batch
+// of every thread.
+constexpr int kRowThreads = kBlock;                     // threads (lanes) per row, js_token_kernel's block
+constexpr int kRowWaves = kRowThreads / kWave;          // wave partials per row
+constexpr int kRowsPerBlock = 2;                        // rows a js_rows_kernel block streams at once
+constexpr int kRowsBlock = kRowThreads * kRowsPerBlock;
+constexpr int kRowsBlocksPerCu = 3;                     // bf16 LDS: 3 x 46 KB of the CU's 160 KB
+constexpr int kJsBatches = 16;                          // batches per thread of the averaged row
 
-// One token at a time per block (persistent: tokens blockIdx.x,
-// blockIdx.x + gridDim.x, ...): the averaged row's log-sum-exp and top-k
-// set, then JS_m for every worker from the lse_m that the worker-row kernel
-// left in d_out.
-//
-// Selection.  Fast path (k <= kBlock): the k-th largest of the threads'
-// largest keys, T0, is at most the k-th largest key of the row, so the
-// selected tokens are among the candidates with key >= T0 (on these inputs
-// a few hundred); they are collected in LDS and each takes its exact rank
-// under (key descending, index ascending).  Otherwise (k > kBlock, or more
-// candidates than fit): a radix select, 8 key bits per pass from the top,
-// then a collection pass that splits the tie at the threshold in index
-// order.
+// A wave's part of a row's log-sum-exp: sum exp(z - m) over its lanes'
+// elements (s = 0: none).
+struct LsePart {
+    double m, s;
+};
+
+struct JsWork {
+    LsePart *part;   // [(M + 1) U][kRowWaves]: row u < U is token u's averaged row, U + m U + u worker m's
+    void *bmax;      // [U][kRowThreads][kJsBatches] keys: uint16 (bf16) or uint32 (float32); 0 = no batch
+    void *tmax;      // [U][kRowThreads] keys: each row thread's largest (0: no element)
+    int32_t *flag;   // [U]: 1 where the per-token wave kernel left the token to the radix kernel
+    int32_t bvec;    // vectors per batch
+};
+
+// A row thread's batch maxima in registers: two uint16 keys per register
+// (bf16) or one uint32 key (float32); 16-byte vectors in memory.
 template <class E>
-__global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
+struct BatchKeys {
+    static constexpr int kRegs = E::kBf16 ? kJsBatches / 2 : kJsBatches;
+    static constexpr int kVecs = kRegs / 4;
+    uint32_t r[kRegs];
+    // Batch b's key.
+    __device__ uint32_t key(int b) const {
+        if constexpr (E::kBf16)
+            return (r[b / 2] >> (16 * (b % 2))) & 0xFFFFu;
+        else
+            return r[b];
+    }
+};
+
+// Vectors per batch: every thread's vectors of a row fit in kJsBatches batches.
+inline int32_t js_batch_vectors(int64_t K, int per) {
+    const int64_t vecs = (K + per - 1) / per;                       // 16-byte vectors per row
+    const int64_t nvec = (vecs + kRowThreads - 1) / kRowThreads;    // per thread, at most
+    return static_cast<int32_t>(std::max<int64_t>(1, (nvec + kJsBatches - 1) / kJsBatches));
+}
+
+// A wave's (shift, sum) from its lanes' (m, s): the largest shift, then
+// sum s exp(m - shift) in a fixed order; lane 0's copy is the one used.
+__device__ inline LsePart wave_lse(double m, double s, const double *tab) {
+    double M = m;
+    for (int o = kWave / 2; o > 0; o >>= 1) M = fmax(M, shfl_xor_d(M, o));
+    double t = s == 0.0 ? 0.0 : s * exp_table(m - M, tab);
+    for (int o = kWave / 2; o > 0; o >>= 1) t += shfl_xor_d(t, o);
+    return LsePart{M, t};
+}
+
+// A row's log-sum-exp from its wave parts, in wave order (-inf for a row of
+// -inf logits).
+__device__ inline double row_lse(const LsePart *p, const double *tab) {
+    LsePart q[kRowWaves];
+#pragma unroll
+    for (int j = 0; j < kRowWaves; ++j) q[j] = p[j];
+    double M = q[0].m;
+#pragma unroll
+    for (int j = 1; j < kRowWaves; ++j) M = fmax(M, q[j].m);
+    double S = 0.0;
+#pragma unroll
+    for (int j = 0; j < kRowWaves; ++j)
+        if (q[j].s != 0.0) S += q[j].s * exp_table(q[j].m - M, tab);
+    return S == 0.0 ? -INFINITY : M + log(S);
+}
+
+// One row's log-sum-exp terms for the thread's elements i_first, i_first +
+// kStride, ... into st.  `nxt` holds the row's first vector on entry and,
+// when has_next, the first vector of row rn on return, so that the next
+// row's load overlaps this row's end.  With kAvg it also keeps the largest
+// key of each batch of bvec vectors (bm, at most kJsBatches; all 0 on
+// entry) and the thread's largest key (kmax, 0 on entry).
+template <class E, bool kAvg>
+__device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_first, int64_t K, int bvec,
+                                 u32x4 &nxt, RowLse &st, const double *etab, const double *tab, BatchKeys<E> &bm,
+                                 uint32_t &kmax) {
     constexpr int P = E::kPer;
-    constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;  // elements per block sweep
-    constexpr int kCand = kJsMaxTopK;                              // candidate capacity
-    __shared__ uint32_t hist[256];
-    __shared__ __align__(16) int32_t sel_idx[kJsMaxTopK];
-    __shared__ float sel_val[kJsMaxTopK];
-    __shared__ __align__(16) union {
-        struct {
-            int32_t idx[kCand];
-            uint32_t key[kCand];
-            float val[kCand];
-        } cand;  // fast selection
-        struct {
-            int32_t idx[kJsMaxTopK];
-            double la[kJsMaxTopK];
-        } out;   // the selected tokens in index order, log pbar
-    } sm;
-    __shared__ double red[2 * kWavesPerBlock];
-    __shared__ double red_n[kJsGroup * kWavesPerBlock];
-    __shared__ __align__(16) uint32_t s_tkey[kBlock];
-    __shared__ uint16_t s_bmax[kJsMaxBatches][kBlock];  // per thread: largest key of each batch, top 16 bits
-    __shared__ uint32_t s_prefix, s_thr;
-    __shared__ int s_need, s_count_eq, s_nsel;
-    __shared__ int s_scan[kBlock];
-    __shared__ double tab[kTab];
+    constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * P;
+    int b = 0, left = bvec;
+    uint32_t bmax = 0;
+    for (int64_t i0 = i_first; i0 < K; i0 += kStride) {
+        const u32x4 cur = nxt;
+        if (i0 + kStride < K)
+            nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * E::kElem), 0,
+                                                        kLoadPolicy);
+        else if (has_next)
+            nxt = __builtin_amdgcn_raw_buffer_load_b128(rn, static_cast<uint32_t>(i_first * E::kElem), 0, kLoadPolicy);
+        float x[P];
+        if constexpr (kAvg || !E::kBf16) vec_values<E>(cur, i0, K, x);  // past K: -inf
+        if constexpr (kAvg) {
+            bmax = max(bmax, E::key_of(vec_max<P>(x)));
+            if (--left == 0 || i0 + kStride >= K) {
+                if constexpr (E::kBf16) {
+                    const uint32_t put = (b & 1) ? bmax << 16 : bmax;
+#pragma unroll
+                    for (int j = 0; j < BatchKeys<E>::kRegs; ++j) bm.r[j] |= j == b / 2 ? put : 0u;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < BatchKeys<E>::kRegs; ++j) bm.r[j] = j == b ? bmax : bm.r[j];
+                }
+                kmax = max(kmax, bmax);
+                ++b;
+                left = bvec;
+                bmax = 0;
+            }
+        }
+        if constexpr (E::kBf16)
+            bf16_lse_add(st, cur, i0, K, etab, tab);
+        else
+            lse_add<P>(st.m, st.thr, st.s1, x, tab);
+    }
+}
+
+// Every row's wave parts of its log-sum-exp, and the averaged rows' batch
+// and thread maxima, into the workspace.  Persistent: thread group g
+// (kRowThreads threads; two per block) streams rows g, g + G, ... (G
+// groups) of the streaming order below; thread lt of a group takes the
+// elements lt * P + j * kStride of its row.  No barriers after the tables
+// are loaded: each wave streams on its own, its next row's first load
+// issued before its row ends.
+template <class E>
+__global__ __launch_bounds__(kRowsBlock) __attribute__((amdgpu_waves_per_eu(6, 8)))
+void js_rows_kernel(JsParams a, JsWork w) {
     __shared__ double etab[E::kBf16 ? kBfTabEntries : 1];
+    __shared__ double tab[kTab];
+    if constexpr (E::kBf16) fill_bf16_exp_table(etab);
+    load_exp_table(tab);  // its barrier also covers etab
+    const int lt = threadIdx.x % kRowThreads;
+    const int64_t i_first = static_cast<int64_t>(lt) * E::kPer;
+    const int64_t G = static_cast<int64_t>(gridDim.x) * kRowsPerBlock;
+    const int64_t R = static_cast<int64_t>(a.M + 1) * a.U;
+    // Streaming order: the averaged rows (token u at r = u), then the worker
+    // rows (row m U + u at r = U + m U + u), the order of the workspace parts.
+    auto row_of = [&](int64_t r) -> rsrc_t {
+        return r < a.U ? js_row(a.avg, r, a.ldk, E::kElem) : js_row(a.workers, r - a.U, a.ldk, E::kElem);
+    };
+    // The group index is uniform in a wave: in a scalar register, the row's
+    // buffer descriptor stays scalar (no per-load waterfall).
+    const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kRowThreads));
+    int64_t r = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + g;
+    u32x4 nxt = {0, 0, 0, 0};
+    if (r < R && i_first < a.K)
+        nxt = __builtin_amdgcn_raw_buffer_load_b128(row_of(r), static_cast<uint32_t>(i_first * E::kElem), 0,
+                                                    kLoadPolicy);
+    for (; r < R; r += G) {
+        const bool has_next = r + G < R;
+        const rsrc_t rr = row_of(r);
+        const rsrc_t rn = has_next ? row_of(r + G) : rr;
+        RowLse st;
+        BatchKeys<E> bm;
+#pragma unroll
+        for (int j = 0; j < BatchKeys<E>::kRegs; ++j) bm.r[j] = 0;
+        uint32_t kmax = 0;
+        const bool avg = r < a.U;
+        if (avg)
+            row_terms<E, true>(rr, rn, has_next, i_first, a.K, w.bvec, nxt, st, etab, tab, bm, kmax);
+        else
+            row_terms<E, false>(rr, rn, has_next, i_first, a.K, w.bvec, nxt, st, etab, tab, bm, kmax);
+        double ml, sl;
+        row_lse_lane(st, ml, sl, tab);
+        const LsePart p = wave_lse(ml, sl, tab);
+        if ((threadIdx.x & (kWave - 1)) == 0) w.part[r * kRowWaves + lt / kWave] = p;
+        if (avg) {
+            using Key = typename std::conditional<E::kBf16, uint16_t, uint32_t>::type;
+            u32x4 *dst = reinterpret_cast<u32x4 *>(static_cast<Key *>(w.bmax) + (r * kRowThreads + lt) * kJsBatches);
+#pragma unroll
+            for (int v = 0; v < BatchKeys<E>::kVecs; ++v)
+                dst[v] = u32x4{bm.r[4 * v], bm.r[4 * v + 1], bm.r[4 * v + 2], bm.r[4 * v + 3]};
+            static_cast<Key *>(w.tmax)[r * kRowThreads + lt] = static_cast<Key>(kmax);
+        }
+    }
+}
+
+// The bin of a 256-bin digit histogram in which the need-th largest of the
+// counted keys falls, and how many keys of that bin are still needed:
+// thread t takes bin 255 - t, and an inclusive scan over the threads finds
+// the first bin (from the top) at which the running count reaches need
+// (need <= the histogram's total).  Block-wide barriers; every thread gets
+// the result.  s_wsum: kWavesPerBlock ints; s_pick: 2 ints.
+__device__ inline void hist_pick(const uint32_t *hist, int need, int *s_wsum, int *s_pick, int &bin, int &need_in) {
+    static_assert(kBlock == 256, "one histogram bin per thread");
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int c = static_cast<int>(hist[255 - tid]);
+    int incl = c;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    if (lane == kWave - 1) s_wsum[wave] = incl;
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) incl += s_wsum[w];
+    if (incl >= need && incl - c < need) {
+        s_pick[0] = 255 - tid;
+        s_pick[1] = need - (incl - c);
+    }
+    __syncthreads();
+    bin = s_pick[0];
+    need_in = s_pick[1];
+}
+
+// Per token (block u; thread t the row thread lt = t of js_rows_kernel):
+// the averaged row's log-sum-exp from its wave parts, its top-k set by a
+// radix select over the row (8 key bits per pass from the top, then a
+// collection pass that splits the tie at the threshold in index order), then
+// JS_m for every worker.  Any k up to kJsMaxTopK: the path for k above a
+// block's threads, and for the tokens the wave kernel flags (flag !=
+// nullptr: only those).
+template <class E>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4, 8)))
+void js_token_radix_kernel(JsParams a, JsWork w, const int32_t *flag) {
+    constexpr int P = E::kPer;
+    constexpr int kMaxK = kJsMaxTopK;
+    constexpr int64_t kStride = static_cast<int64_t>(kBlock) * P;  // elements per block sweep
+    constexpr int kWorkerLanes = kBlock / kJsGroup;                // threads per worker in the JS terms
+    __shared__ uint32_t hist[256];
+    __shared__ __align__(16) int32_t sel_idx[kMaxK];
+    __shared__ float sel_val[kMaxK];
+    __shared__ __align__(16) struct {
+        int32_t idx[kMaxK];
+        double la[kMaxK];
+    } out;  // the selected tokens in index order, log pbar
+    __shared__ double s_lse[kJsGroup];
+    __shared__ int s_wsum[kWavesPerBlock], s_pick[2];
+    __shared__ int s_nsel;
+    __shared__ double tab[kTab];
 
     const int tid = threadIdx.x;
     const int k = a.k;
-    if constexpr (E::kBf16) fill_bf16_exp_table(etab);
-    load_exp_table(tab);  // its barrier also covers etab
+    load_exp_table(tab);
 
     for (int64_t u = blockIdx.x; u < a.U; u += gridDim.x) {
+        if (flag && flag[u] == 0) continue;  // the same in every thread
         const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
-
-        // Pass 1 over the averaged row: log-sum-exp (the same sums, in the same
-        // lane order, as the worker rows get) and this thread's largest key
-        // (key 0 lies below the key of every value).
-        RowLse st;
-        uint32_t kmax = 0;
-        int nb = 0;  // batches this thread reads
-        for (int64_t b0 = static_cast<int64_t>(tid) * P; b0 < a.K; b0 += kJsBatch * kStride, ++nb) {
-            u32x4 tb[kJsBatch];
-            load_batch<E>(ra, b0, a.K, kStride, tb);
-            uint32_t bmax = 0;
-#pragma unroll
-            for (int d = 0; d < kJsBatch; ++d) {
-                const int64_t i0 = b0 + d * kStride;
-                if (i0 < a.K) {
-                    float v[P];
-                    vec_values<E>(tb[d], i0, a.K, v);  // past K: -inf, below every value in the vector
-                    bmax = max(bmax, E::key_of(vec_max<P>(v)));
-                    if constexpr (E::kBf16)
-                        bf16_lse_add(st, tb[d], i0, a.K, etab, tab);
-                    else
-                        lse_add<P>(st.m, st.thr, st.s1, v, tab);
-                }
-            }
-            kmax = max(kmax, bmax);
-            if (nb < kJsMaxBatches) s_bmax[nb][tid] = static_cast<uint16_t>(bmax >> (E::kKeyBits - 16));
-        }
-        double ml, sl;
-        row_lse_lane(st, ml, sl, tab);
-        const double lse_a = group_lse<kBlock>(ml, sl, red, tab);
-
-        bool fast = k <= kBlock;
-        if (fast) {
-            // T0: the thread maxima ranked with ties by thread index form a
-            // permutation, so exactly one thread holds rank k - 1.
-            s_tkey[tid] = kmax;
-            if (tid == 0) s_nsel = 0;
-            __syncthreads();
-            int r = 0;
-#pragma unroll 4
-            for (int j = 0; j < kBlock; j += 4) {
-                const u32x4 o = *reinterpret_cast<const u32x4 *>(&s_tkey[j]);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) r += (o[q] > kmax || (o[q] == kmax && j + q < tid)) ? 1 : 0;
-            }
-            if (r == k - 1) s_thr = kmax;
-            __syncthreads();
-            const uint32_t T0 = s_thr;
-            // The candidates are the row's elements with key >= T0, that is
-            // with value >= the value of T0 (-0 and +0 share a key and
-            // compare equal; T0 = 0 takes every element).  A thread reads
-            // again only the batches whose recorded largest key (its top 16
-            // bits, a monotone coarsening) reaches T0's, and a thread whose
-            // largest key is below T0 reads nothing.
-            const float f0 = T0 == 0 ? -INFINITY : E::value_of(T0);
-            const uint16_t t16 = static_cast<uint16_t>(T0 >> (E::kKeyBits - 16));
-            // Batches to read again: a bit per recorded batch whose largest
-            // key may reach T0, and every batch past the recorded ones.  A
-            // lane walks its own set bits, so a wave takes as many trips as
-            // its busiest lane rather than one per batch.
-            uint32_t todo = 0;
-            if (kmax >= T0)
-                for (int b = 0; b < nb && b < kJsMaxBatches; ++b)
-                    if (s_bmax[b][tid] >= t16) todo |= 1u << b;
-            int b_next = kJsMaxBatches;                         // next unrecorded batch
-            const int b_end = kmax >= T0 ? nb : kJsMaxBatches;  // unrecorded batches end here
-            while (true) {
-                int b;
-                if (todo != 0) {
-                    b = __builtin_ctz(todo);
-                    todo &= todo - 1;
-                } else if (b_next < b_end) {
-                    b = b_next++;
-                } else {
-                    break;
-                }
-                const int64_t b0 = static_cast<int64_t>(tid) * P + static_cast<int64_t>(b) * kJsBatch * kStride;
-                u32x4 tb[kJsBatch];
-                load_batch<E>(ra, b0, a.K, kStride, tb);
-#pragma unroll
-                for (int d = 0; d < kJsBatch; ++d) {
-                    const int64_t i0 = b0 + d * kStride;
-                    if (i0 < a.K) {
-                        float v[P];
-                        E::values(tb[d], v);
-                        const int64_t left = a.K - i0;
-                        const int n = left >= P ? P : static_cast<int>(left);
-#pragma unroll
-                        for (int j = 0; j < P; ++j) {
-                            if (v[j] >= f0 && j < n) {
-                                const int slot = atomicAdd(&s_nsel, 1);
-                                if (slot < kCand) {
-                                    sm.cand.idx[slot] = static_cast<int32_t>(i0 + j);
-                                    sm.cand.key[slot] = E::key_of(v[j]);
-                                    sm.cand.val[slot] = v[j];
-                                }
-                            }
-                        }
-                    }
-                }
-            }
-            __syncthreads();
-            const int C = s_nsel;
-            fast = C <= kCand;  // the same in every thread
-            if (fast) {
-                // Pad to a multiple of 4 with key 0, below every candidate.
-                if (tid < 4 && C + tid < ((C + 3) & ~3)) sm.cand.key[C + tid] = 0;
-                __syncthreads();
-                for (int c = tid; c < C; c += kBlock) {
-                    const uint32_t kc = sm.cand.key[c];
-                    const int32_t ic = sm.cand.idx[c];
-                    int rank = 0;
-                    for (int j = 0; j < C; j += 4) {
-                        const u32x4 kj = *reinterpret_cast<const u32x4 *>(&sm.cand.key[j]);
-                        const u32x4 ij = *reinterpret_cast<const u32x4 *>(&sm.cand.idx[j]);
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            rank += (kj[q] > kc || (kj[q] == kc && static_cast<int32_t>(ij[q]) < ic)) ? 1 : 0;
-                    }
-                    if (rank < k) {
-                        sel_idx[rank] = ic;
-                        sel_val[rank] = sm.cand.val[c];
-                    }
-                }
-            }
-            __syncthreads();
-        }
-
-        if (!fast) {
+        const double lse_a = row_lse(w.part + u * kRowWaves, tab);
+        {
             // Radix select of the k-th largest key, 8 bits per pass from the top.
             uint32_t prefix = 0;
-            int need = k;
+            int need = k, count_eq = 0;
             for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
                 const int shift = E::kKeyBits - 8 * (pass + 1);
                 hist[tid] = 0;
@@ -793,35 +733,22 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
                     float v[P];
                     uint32_t key[P];
                     const int n = load_vec<E>(ra, i0, a.K, v, key);
-                    if (pass == 0) {
 #pragma unroll
-                        for (int j = 0; j < P; ++j)
-                            if (j < n) atomicAdd(&hist[key[j] >> shift], 1u);
-                    } else {
-#pragma unroll
-                        for (int j = 0; j < P; ++j)
-                            if (j < n && (key[j] >> (shift + 8)) == prefix)
-                                atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
-                    }
+                    for (int j = 0; j < P; ++j)
+                        if (j < n && (pass == 0 || (key[j] >> (shift + 8)) == prefix))
+                            atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
                 }
                 __syncthreads();
-                if (tid == 0) {
-                    int above = 0, bin = 255;
-                    for (; bin > 0; --bin) {
-                        if (above + static_cast<int>(hist[bin]) >= need) break;
-                        above += hist[bin];
-                    }
-                    s_prefix = (prefix << 8) | static_cast<uint32_t>(bin);
-                    s_need = need - above;
-                    s_count_eq = hist[bin];
-                }
+                int bin, need_in;
+                hist_pick(hist, need, s_wsum, s_pick, bin, need_in);
+                count_eq = static_cast<int>(hist[bin]);  // read before the next pass clears it
+                prefix = (prefix << 8) | static_cast<uint32_t>(bin);
+                need = need_in;
                 __syncthreads();
-                prefix = s_prefix;
-                need = s_need;
             }
             const uint32_t T = prefix;
             const int need_eq = need;
-            const bool take_all_eq = s_count_eq == need_eq;
+            const bool take_all_eq = count_eq == need_eq;
 
             // Collect the keys above T (and those equal to T when all of them are
             // taken); the list order does not matter, it is sorted below.
@@ -843,7 +770,9 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
             __syncthreads();
             if (!take_all_eq) {
                 // Ties straddle the threshold: take the equal keys in index order,
-                // one block sweep at a time, until need_eq are taken.
+                // one block sweep at a time (thread order is element order within
+                // a sweep), until need_eq are taken.
+                const int lane = tid & (kWave - 1), wave = tid / kWave;
                 int remaining = need_eq;
                 for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
                     const int64_t i0 = base + static_cast<int64_t>(tid) * P;
@@ -855,18 +784,15 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
 #pragma unroll
                         for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
                     }
-                    s_scan[tid] = cnt;
-                    __syncthreads();
-                    if (tid == 0) {
-                        int run = 0;
-                        for (int t = 0; t < kBlock; ++t) {
-                            const int c = s_scan[t];
-                            s_scan[t] = run;
-                            run += c;
-                        }
+                    int incl = cnt;  // inclusive prefix over the wave's lanes
+                    for (int o = 1; o < kWave; o <<= 1) {
+                        const int t = __shfl_up(incl, o);
+                        if (lane >= o) incl += t;
                     }
+                    if (lane == kWave - 1) s_wsum[wave] = incl;
                     __syncthreads();
-                    int rank = s_scan[tid];
+                    int rank = incl - cnt;
+                    for (int wv = 0; wv < wave; ++wv) rank += s_wsum[wv];
                     if (i0 < a.K) {
 #pragma unroll
                         for (int j = 0; j < P; ++j) {
@@ -881,9 +807,8 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
                         }
                     }
                     __syncthreads();
-                    const int taken_total = s_nsel;
-                    remaining = k - taken_total;
-                    __syncthreads();
+                    remaining = k - s_nsel;
+                    __syncthreads();  // every thread has read s_nsel before s_wsum is rewritten
                 }
             }
         }
@@ -901,55 +826,328 @@ __global__ __launch_bounds__(kBlock) void js_kernel(JsParams a) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) r += static_cast<int32_t>(o[q]) < my ? 1 : 0;
             }
-            sm.out.idx[r] = my;
-            sm.out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
+            out.idx[r] = my;
+            out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
         }
         __syncthreads();
         if (a.topk_out)
-            for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = sm.out.idx[t];
+            for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = out.idx[t];
 
-        // JS terms, kJsGroup workers at a time: each half of the block takes
-        // kJsHalf of them over the selected tokens, so that their gathers
-        // overlap.
+        // JS terms, kJsGroup workers at a time: worker j of the group takes
+        // threads [j, j + 1) * kWorkerLanes (half a wave), thread l of them
+        // the selected tokens l, l + kWorkerLanes, ... in index order; the
+        // half-wave sum is d's.
         constexpr double kLog2 = 0.69314718055994530942;
-        constexpr int kHalfThreads = kBlock / 2;
-        const int half = __builtin_amdgcn_readfirstlane(tid / kHalfThreads);  // uniform in a wave
-        const int th = tid % kHalfThreads;
-        for (int w0 = 0; w0 < a.M; w0 += kJsGroup) {
-            const int nw = a.M - w0 < kJsGroup ? a.M - w0 : kJsGroup;
-            rsrc_t rw[kJsHalf];
-            double lse_w[kJsHalf], ph[kJsHalf];
+        const int j = tid / kWorkerLanes, l = tid % kWorkerLanes;
+        for (int64_t w0 = 0; w0 < a.M; w0 += kJsGroup) {
+            const int nw = a.M - w0 < kJsGroup ? static_cast<int>(a.M - w0) : kJsGroup;
+            if (tid < nw) s_lse[tid] = row_lse(w.part + (a.U + (w0 + tid) * a.U + u) * kRowWaves, tab);
+            __syncthreads();
+            double acc = 0.0;
+            const int64_t row = (w0 + (j < nw ? j : 0)) * a.U + u;
+            if (j < nw) {
+                const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
+                const double lse_w = s_lse[j];
+                constexpr int kGather = 4;  // gathers a thread has in flight
+                for (int t0 = l; t0 < k; t0 += kGather * kWorkerLanes) {
+                    float z[kGather];
 #pragma unroll
-            for (int j = 0; j < kJsHalf; ++j) {
-                // lse_m, parked in d_out by the worker-row kernel; read before
-                // the barriers of block_sum_n, overwritten with d_m(u) after.
-                const int w = half * kJsHalf + j;
-                const int64_t row = static_cast<int64_t>(w0 + (w < nw ? w : 0)) * a.U + u;
-                rw[j] = js_row(a.workers, row, a.ldk, E::kElem);
-                lse_w[j] = a.d_out[row];
-                ph[j] = 0.0;
+                    for (int q = 0; q < kGather; ++q) {
+                        const int t = t0 + q * kWorkerLanes;
+                        z[q] = t < k ? E::at_ptr(zrow, out.idx[t]) : 0.0f;
+                    }
+#pragma unroll
+                    for (int q = 0; q < kGather; ++q) {
+                        const int t = t0 + q * kWorkerLanes;
+                        if (t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, out.la[t]);
+                    }
+                }
             }
-            for (int t = th; t < k; t += kHalfThreads) {
-                const int32_t idx = sm.out.idx[t];
-                const double lq = sm.out.la[t];
-                float z[kJsHalf];
-#pragma unroll
-                for (int j = 0; j < kJsHalf; ++j) z[j] = E::at(rw[j], idx);
-#pragma unroll
-                for (int j = 0; j < kJsHalf; ++j)
-                    if (half * kJsHalf + j < nw) ph[j] += js_term(static_cast<double>(z[j]) - lse_w[j], lq);
-            }
-            double part[kJsGroup];
-#pragma unroll
-            for (int j = 0; j < kJsHalf; ++j) {
-                part[j] = half == 0 ? ph[j] : 0.0;
-                part[kJsHalf + j] = half == 0 ? 0.0 : ph[j];
-            }
-            const double js = block_sum_n<kJsGroup>(part, red_n);
-            if (tid < nw) a.d_out[static_cast<int64_t>(w0 + tid) * a.U + u] = sqrt((js > 0.0 ? js : 0.0) / kLog2);
+            for (int o = kWorkerLanes / 2; o > 0; o >>= 1) acc += shfl_xor_d(acc, o);
+            if (l == 0 && j < nw) a.d_out[row] = sqrt((acc > 0.0 ? acc : 0.0) / kLog2);
+            __syncthreads();  // s_lse is rewritten by the next group
         }
-        __syncthreads();  // the next token reuses the shared arrays
+        // The next token reuses the shared arrays: the last barrier above
+        // follows every read of them.
     }
+}
+
+// ------------------------------------------------- per token, one wave each
+constexpr int kWaveTokens = kBlock / kWave;       // tokens per block of js_token_wave_kernel
+constexpr int kRtPerLane = kRowThreads / kWave;   // row threads whose batch maxima a lane takes
+constexpr int kWaveCand = 512;                    // candidates a token may have
+constexpr int kCandPerLane = kWaveCand / kWave;
+constexpr int kWaveMaxK = kRowThreads;            // the selection ranks one maximum per row thread
+constexpr int kJsLanes = kWave / kJsGroup;        // lanes per worker in the JS terms
+
+// Orders a wave's LDS accesses: what a lane wrote before it is visible to
+// every lane of the wave after it.
+__device__ inline void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One wave's LDS in js_token_wave_kernel.
+struct __align__(16) WaveLds {
+    union {
+        struct {
+            uint64_t comp[kWaveCand];  // key << 32 | ~index: larger = earlier in (key desc, index asc)
+            float val[kWaveCand];
+        } cand;
+        struct {
+            int32_t idx[kWaveMaxK];
+            double la[kWaveMaxK];
+        } out;  // the selected tokens in index order, log pbar
+    } u;
+    int32_t sel_idx[kWaveMaxK + 4];
+    float sel_val[kWaveMaxK];
+    uint32_t hist[256];
+    double lse[kJsGroup];
+    int nsel;
+};
+
+// Per token, one wave (token u = blockIdx.x * kWaveTokens + wave; no block
+// barriers after the exp table): the averaged row's log-sum-exp from its
+// wave parts; T0, the k-th largest of the row threads' largest keys (a
+// radix select over the 256 keys, four per lane), which is at most the row's
+// k-th largest key, so the selected tokens are among the elements with key
+// >= T0 (on these inputs a few hundred); the lanes read again only the
+// batches whose largest key reaches T0, collect those elements in LDS, and
+// each candidate takes its exact rank under (key descending, index
+// ascending) from one 64-bit comparison per other candidate; the selected
+// tokens in index order; then the JS terms, kJsLanes lanes per worker.  A
+// token with more than kWaveCand candidates (a row of many equal logits) is
+// flagged and left to js_token_radix_kernel.  k <= kWaveMaxK.
+template <class E>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4, 8)))
+void js_token_wave_kernel(JsParams a, JsWork w) {
+    constexpr int P = E::kPer;
+    constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * P;  // elements per row sweep
+    __shared__ double tab[kTab];
+    __shared__ WaveLds lds[kWaveTokens];
+    load_exp_table(tab);
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t u = static_cast<int64_t>(blockIdx.x) * kWaveTokens + wave;
+    if (u >= a.U) return;  // the whole wave
+    WaveLds &L = lds[wave];
+    const int k = a.k;
+    const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
+    const double lse_a = row_lse(w.part + u * kRowWaves, tab);
+
+    // The largest keys of row threads lane + q kWave (key 0: no element).
+    using Key = typename std::conditional<E::kBf16, uint16_t, uint32_t>::type;
+    uint32_t km[kRtPerLane];
+#pragma unroll
+    for (int q = 0; q < kRtPerLane; ++q) km[q] = static_cast<const Key *>(w.tmax)[u * kRowThreads + lane + q * kWave];
+
+    // T0: radix select of the k-th largest of the 256 row-thread maxima, 8
+    // bits per pass; lane l takes the bins 255 - 4l .. 252 - 4l.
+    uint32_t prefix = 0;
+    int need = k;
+    for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
+        const int shift = E::kKeyBits - 8 * (pass + 1);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) L.hist[lane + i * kWave] = 0;
+        wave_sync();
+#pragma unroll
+        for (int q = 0; q < kRtPerLane; ++q)
+            if (pass == 0 || (km[q] >> (shift + 8)) == prefix) atomicAdd(&L.hist[(km[q] >> shift) & 255u], 1u);
+        wave_sync();
+        int c[4], c4 = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            c[i] = static_cast<int>(L.hist[255 - 4 * lane - i]);
+            c4 += c[i];
+        }
+        int incl = c4;
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int t = __shfl_up(incl, o);
+            if (lane >= o) incl += t;
+        }
+        int bin = -1, nin = 0, run = incl - c4;
+        if (run < need && need <= incl) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (bin < 0 && run + c[i] >= need) {
+                    bin = 255 - 4 * lane - i;
+                    nin = need - run;
+                }
+                run += c[i];
+            }
+        }
+        const int src = __ffsll(static_cast<unsigned long long>(__ballot(bin >= 0))) - 1;
+        prefix = (prefix << 8) | static_cast<uint32_t>(__shfl(bin, src));
+        need = __shfl(nin, src);
+        wave_sync();  // every lane has read the histogram before the next pass clears it
+    }
+    const uint32_t T0 = prefix;
+
+    // Candidates: the elements with key >= T0, that is with value >= the
+    // value of T0 (-0 and +0 share a key and compare equal; T0 = 0 takes
+    // every element), from the batches whose largest key reaches it; a lane
+    // walks its own set bits.
+    if (lane == 0) L.nsel = 0;
+    wave_sync();
+    const float f0 = T0 == 0 ? -INFINITY : E::value_of(T0);
+    // Batches to read again: bit q kJsBatches + b for batch b of row thread
+    // lane + q kWave; only a row thread whose largest key reaches T0 loads
+    // its batch maxima.
+    uint64_t todo = 0;
+#pragma unroll
+    for (int q = 0; q < kRtPerLane; ++q) {
+        if (km[q] != 0 && km[q] >= T0) {
+            BatchKeys<E> bk;
+            const u32x4 *src = reinterpret_cast<const u32x4 *>(static_cast<const Key *>(w.bmax) +
+                                                               (u * kRowThreads + lane + q * kWave) * kJsBatches);
+#pragma unroll
+            for (int v = 0; v < BatchKeys<E>::kVecs; ++v) {
+                const u32x4 t = src[v];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) bk.r[4 * v + i] = t[i];
+            }
+#pragma unroll
+            for (int b = 0; b < kJsBatches; ++b) {
+                const uint32_t bb = bk.key(b);
+                if (bb != 0 && bb >= T0) todo |= 1ull << (q * kJsBatches + b);
+            }
+        }
+    }
+    while (todo != 0) {
+        const int bit = __builtin_ctzll(todo);
+        todo &= todo - 1;
+        const int64_t rt = lane + (bit / kJsBatches) * kWave, b = bit % kJsBatches;
+        for (int c0 = 0; c0 < w.bvec; c0 += kJsBatch) {
+            const int64_t b0 = rt * P + (b * w.bvec + c0) * kStride;
+            const int nd = w.bvec - c0 < kJsBatch ? w.bvec - c0 : kJsBatch;
+            u32x4 tb[kJsBatch];
+            load_batch<E>(ra, b0, a.K, kStride, nd, tb);
+#pragma unroll
+            for (int d = 0; d < kJsBatch; ++d) {
+                const int64_t i0 = b0 + d * kStride;
+                if (d < nd && i0 < a.K) {
+                    float v[P];
+                    E::values(tb[d], v);
+                    const int64_t left = a.K - i0;
+                    const int n = left >= P ? P : static_cast<int>(left);
+#pragma unroll
+                    for (int j = 0; j < P; ++j) {
+                        if (v[j] >= f0 && j < n) {
+                            const int slot = atomicAdd(&L.nsel, 1);
+                            if (slot < kWaveCand) {
+                                L.u.cand.comp[slot] = (static_cast<uint64_t>(E::key_of(v[j])) << 32) |
+                                                      (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
+                                L.u.cand.val[slot] = v[j];
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+    wave_sync();
+    const int C = L.nsel;
+    if (C > kWaveCand) {  // the same in every lane
+        if (lane == 0) w.flag[u] = 1;
+        return;
+    }
+    if (lane == 0 && (C & 1)) L.u.cand.comp[C] = 0;  // pad to even: below every candidate
+    wave_sync();
+
+    // Each candidate's rank; the first k are selected.
+    const int nc = (C + kWave - 1) / kWave;
+    uint64_t mine[kCandPerLane];
+    int rk[kCandPerLane];
+#pragma unroll
+    for (int q = 0; q < kCandPerLane; ++q) {
+        const int c = lane + q * kWave;
+        mine[q] = c < C ? L.u.cand.comp[c] : 0;
+        rk[q] = 0;
+    }
+    for (int j = 0; j < C; j += 2) {
+        const u32x4 o = *reinterpret_cast<const u32x4 *>(&L.u.cand.comp[j]);
+        const uint64_t c0 = (static_cast<uint64_t>(o[1]) << 32) | o[0];
+        const uint64_t c1 = (static_cast<uint64_t>(o[3]) << 32) | o[2];
+#pragma unroll
+        for (int q = 0; q < kCandPerLane; ++q)
+            if (q < nc) rk[q] += (c0 > mine[q] ? 1 : 0) + (c1 > mine[q] ? 1 : 0);
+    }
+#pragma unroll
+    for (int q = 0; q < kCandPerLane; ++q) {
+        const int c = lane + q * kWave;
+        if (c < C && rk[q] < k) {
+            L.sel_idx[rk[q]] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(mine[q]));
+            L.sel_val[rk[q]] = L.u.cand.val[c];
+        }
+    }
+    if (lane < 4 && k + lane < ((k + 3) & ~3)) L.sel_idx[k + lane] = INT32_MAX;  // above every token
+    wave_sync();
+
+    // The selected tokens in index order (indices are distinct), with the
+    // averaged model's log-probabilities; the candidates are no longer read.
+    constexpr int kSelPerLane = kWaveMaxK / kWave;
+    int32_t my[kSelPerLane];
+    int pos[kSelPerLane];
+#pragma unroll
+    for (int q = 0; q < kSelPerLane; ++q) {
+        const int t = lane + q * kWave;
+        my[q] = t < k ? L.sel_idx[t] : INT32_MAX;
+        pos[q] = 0;
+    }
+    for (int j = 0; j < k; j += 4) {
+        const u32x4 o = *reinterpret_cast<const u32x4 *>(&L.sel_idx[j]);
+#pragma unroll
+        for (int q = 0; q < kSelPerLane; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pos[q] += static_cast<int32_t>(o[i]) < my[q] ? 1 : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < kSelPerLane; ++q) {
+        const int t = lane + q * kWave;
+        if (t < k) {
+            L.u.out.idx[pos[q]] = my[q];
+            L.u.out.la[pos[q]] = static_cast<double>(L.sel_val[t]) - lse_a;
+        }
+    }
+    wave_sync();
+    if (a.topk_out)
+        for (int t = lane; t < k; t += kWave) a.topk_out[u * k + t] = L.u.out.idx[t];
+
+    // JS terms, kJsGroup workers at a time: worker jw of the group takes
+    // lanes [jw, jw + 1) * kJsLanes, lane l of them the selected tokens l,
+    // l + kJsLanes, ... in index order; their sum is d's.
+    constexpr double kLog2 = 0.69314718055994530942;
+    const int jw = lane / kJsLanes, l = lane % kJsLanes;
+    for (int64_t w0 = 0; w0 < a.M; w0 += kJsGroup) {
+        const int nw = a.M - w0 < kJsGroup ? static_cast<int>(a.M - w0) : kJsGroup;
+        if (lane < nw) L.lse[lane] = row_lse(w.part + (a.U + (w0 + lane) * a.U + u) * kRowWaves, tab);
+        wave_sync();
+        double acc = 0.0;
+        const int64_t row = (w0 + (jw < nw ? jw : 0)) * a.U + u;
+        if (jw < nw) {
+            const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
+            const double lse_w = L.lse[jw];
+            constexpr int kGather = 4;  // gathers a lane has in flight
+            for (int t0 = l; t0 < k; t0 += kGather * kJsLanes) {
+                float z[kGather];
+#pragma unroll
+                for (int q = 0; q < kGather; ++q) {
+                    const int t = t0 + q * kJsLanes;
+                    z[q] = t < k ? E::at_ptr(zrow, L.u.out.idx[t]) : 0.0f;
+                }
+#pragma unroll
+                for (int q = 0; q < kGather; ++q) {
+                    const int t = t0 + q * kJsLanes;
+                    if (t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, L.u.out.la[t]);
+                }
+            }
+        }
+        for (int o = kJsLanes / 2; o > 0; o >>= 1) acc += shfl_xor_d(acc, o);
+        if (l == 0 && jw < nw) a.d_out[row] = sqrt((acc > 0.0 ? acc : 0.0) / kLog2);
+        wave_sync();  // L.lse is rewritten by the next group
+    }
+    if (lane == 0) w.flag[u] = 0;
 }
 
 // mean[m] = (1/U) sum_u d[m][u], one block per worker, fixed order.
@@ -967,20 +1165,42 @@ __global__ __launch_bounds__(256) void js_mean_kernel(const double *d, int64_t U
     if (t == 0) mean[m] = s[0] / static_cast<double>(U);
 }
 
+namespace {
+int64_t js_part_bytes(int32_t M, int64_t U) {
+    return (static_cast<int64_t>(M) + 1) * U * kRowWaves * static_cast<int64_t>(sizeof(LsePart));
+}
+int64_t js_bmax_bytes(int32_t bf16, int64_t U) { return U * kRowThreads * kJsBatches * (bf16 ? 2 : 4); }
+int64_t js_tmax_bytes(int32_t bf16, int64_t U) { return U * kRowThreads * (bf16 ? 2 : 4); }
+}  // namespace
+
+int64_t js_workspace_bytes(int32_t bf16, int32_t M, int64_t U) {
+    return js_part_bytes(M, U) + js_bmax_bytes(bf16, U) + js_tmax_bytes(bf16, U) + (U * 4 + 15) / 16 * 16;
+}
+
 bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
-               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, int num_cus, hipStream_t stream) {
+               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, void *workspace, int num_cus,
+               hipStream_t stream) {
     JsParams p{avg, workers, d_out, topk_out, U, K, ldk, M, k};
+    char *ws = static_cast<char *>(workspace);
+    const int64_t o_bmax = js_part_bytes(M, U), o_tmax = o_bmax + js_bmax_bytes(bf16, U);
+    const int64_t o_flag = o_tmax + js_tmax_bytes(bf16, U);
+    JsWork w{reinterpret_cast<LsePart *>(ws), ws + o_bmax, ws + o_tmax, reinterpret_cast<int32_t *>(ws + o_flag),
+             js_batch_vectors(K, bf16 ? JsBF16::kPer : JsF32::kPer)};
+    const int64_t groups = ((static_cast<int64_t>(M) + 1) * U + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kRowsBlocksPerCu) * std::max(num_cus, 1));
+    const dim3 tokens(static_cast<unsigned>(U));
+    const dim3 token_waves(static_cast<unsigned>((U + kWaveTokens - 1) / kWaveTokens));
+    const bool wave_path = k <= kWaveMaxK;
     if (bf16) {
-        const int64_t groups = (static_cast<int64_t>(M) * U + kBfRowsPerBlock - 1) / kBfRowsPerBlock;
-        const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kBfBlocksPerCu) * std::max(num_cus, 1));
-        hipLaunchKernelGGL(js_lse_bf16_table_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBfBlock), 0, stream, p);
-        const int64_t tgrid = std::min<int64_t>(U, static_cast<int64_t>(kJsBlocksPerCuBf16) * std::max(num_cus, 1));
-        hipLaunchKernelGGL(js_kernel<JsBF16>, dim3(static_cast<unsigned>(tgrid)), dim3(kBlock), 0, stream, p);
+        hipLaunchKernelGGL(js_rows_kernel<JsBF16>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
+        if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsBF16>, token_waves, dim3(kBlock), 0, stream, p, w);
+        hipLaunchKernelGGL(js_token_radix_kernel<JsBF16>, tokens, dim3(kBlock), 0, stream, p, w,
+                           wave_path ? w.flag : nullptr);
     } else {
-        const dim3 rows(static_cast<unsigned>(U), static_cast<unsigned>(M));
-        hipLaunchKernelGGL(js_lse_kernel<JsF32>, rows, dim3(kBlock), 0, stream, p);
-        const int64_t tgrid = std::min<int64_t>(U, static_cast<int64_t>(kJsBlocksPerCuF32) * std::max(num_cus, 1));
-        hipLaunchKernelGGL(js_kernel<JsF32>, dim3(static_cast<unsigned>(tgrid)), dim3(kBlock), 0, stream, p);
+        hipLaunchKernelGGL(js_rows_kernel<JsF32>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
+        if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsF32>, token_waves, dim3(kBlock), 0, stream, p, w);
+        hipLaunchKernelGGL(js_token_radix_kernel<JsF32>, tokens, dim3(kBlock), 0, stream, p, w,
+                           wave_path ? static_cast<const int32_t *>(w.flag) : nullptr);
     }
     if (hipGetLastError() != hipSuccess) return false;
     if (mean_out) {

@@ -7,10 +7,15 @@
 
 namespace fgd {
 
-// Launches the worker-row log-sum-exp kernel, the per-token kernel and,
-// when mean_out is given, the per-worker mean on `stream`; num_cus sizes the
-// persistent grid of the bf16 worker-row kernel.  False if a launch failed.
+// Device workspace bytes of one JS distance call (both dtypes' layouts).
+int64_t js_workspace_bytes(int32_t bf16, int32_t M, int64_t U);
+
+// Launches the row kernel, the per-token kernel and, when mean_out is given,
+// the per-worker mean on `stream`; `workspace` holds js_workspace_bytes
+// bytes (16-byte aligned) and num_cus sizes the row kernel's persistent
+// grid.  False if a launch failed.
 bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
-               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, int num_cus, hipStream_t stream);
+               int32_t k, double *d_out, double *mean_out, int32_t *topk_out, void *workspace, int num_cus,
+               hipStream_t stream);
 
 }  // namespace fgd

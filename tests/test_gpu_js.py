@@ -60,6 +60,12 @@ def _values(a, dtype):
     return tensors.bf16_bits_to_f32(a) if dtype == "bf16" else a
 
 
+def _workspace(fgd, torch, dtype, M, U):
+    """The call's workspace, filled with a byte pattern: the kernels must
+    not depend on what it held before."""
+    return torch.full((fgd.fgd_js_workspace_size(dtype, M, U),), 0xA5, dtype=torch.uint8, device="cuda")
+
+
 def _run(fgd, torch, A, W, dtype, K, k):
     U, ldk = A.shape
     M = W.shape[0]
@@ -69,7 +75,7 @@ def _run(fgd, torch, A, W, dtype, K, k):
     d = torch.full((M, U), float("nan"), dtype=torch.float64, device="cuda")
     mean = torch.full((M,), float("nan"), dtype=torch.float64, device="cuda")
     tops = torch.full((U, k), -1, dtype=torch.int32, device="cuda")
-    fgd.fgd_js_distance(gA, gW, dtype, M, U, K, ldk, k, d, mean, tops)
+    fgd.fgd_js_distance(gA, gW, dtype, M, U, K, ldk, k, d, mean, tops, _workspace(fgd, torch, dtype, M, U))
     torch.cuda.synchronize()
     return d.cpu().numpy(), mean.cpu().numpy(), tops.cpu().numpy()
 
@@ -161,14 +167,24 @@ def test_js_rejections(env):
     A = torch.zeros((2, 64), device="cuda")
     W = torch.zeros((3, 2, 64), device="cuda")
     d = torch.zeros((3, 2), dtype=torch.float64, device="cuda")
+    need = fgd.fgd_js_workspace_size("f32", 3, 2)
+    ws = torch.zeros(need + 64, dtype=torch.uint8, device="cuda")
     for kw in (dict(top_k=0), dict(top_k=65), dict(top_k=2000), dict(ldk=62, vocab=60), dict(vocab=65),
-               dict(num_tokens=0), dict(dtype=7), dict(num_workers=0)):
-        args = dict(dtype="f32", num_workers=3, num_tokens=2, vocab=64, ldk=64, top_k=10)
+               dict(num_tokens=0), dict(dtype=7), dict(num_workers=0), dict(workspace=None),
+               dict(workspace_bytes=need - 1), dict(workspace=ws[8:]), dict(workspace=d)):
+        args = dict(dtype="f32", num_workers=3, num_tokens=2, vocab=64, ldk=64, top_k=10, workspace=ws,
+                    workspace_bytes=None)
         args.update(kw)
         with pytest.raises(fgd.FgdError) as e:
             fgd.fgd_js_distance(A, W, args["dtype"], args["num_workers"], args["num_tokens"], args["vocab"],
-                                args["ldk"], args["top_k"], d)
+                                args["ldk"], args["top_k"], d, workspace=args["workspace"],
+                                workspace_bytes=args["workspace_bytes"] if args["workspace"] is not d else need)
         assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+    for bad in (dict(dtype=7), dict(num_workers=0), dict(num_tokens=0)):
+        args = dict(dtype="f32", num_workers=3, num_tokens=2)
+        args.update(bad)
+        with pytest.raises(fgd.FgdError):
+            fgd.fgd_js_workspace_size(args["dtype"], args["num_workers"], args["num_tokens"])
 
 
 def test_js_full_size_sampled_tokens(env):
@@ -184,7 +200,7 @@ def test_js_full_size_sampled_tokens(env):
     d = torch.empty((M, U), dtype=torch.float64, device="cuda")
     mean = torch.empty(M, dtype=torch.float64, device="cuda")
     tops = torch.empty((U, k), dtype=torch.int32, device="cuda")
-    fgd.fgd_js_distance(A, W, "bf16", M, U, K, K, k, d, mean, tops)
+    fgd.fgd_js_distance(A, W, "bf16", M, U, K, K, k, d, mean, tops, _workspace(fgd, torch, "bf16", M, U))
     torch.cuda.synchronize()
     rng = np.random.default_rng(0)
     sample = np.unique(np.concatenate([[0, U - 1], rng.integers(0, U, 14)]))
@@ -265,9 +281,9 @@ def test_js_bf16_table_edges_dense(env):
 
 
 def test_js_bf16_rows_beyond_the_persistent_grid(env):
-    """More worker rows than the bf16 worker-row kernel's persistent grid
-    sums at once (3 blocks of two rows per compute unit), so blocks take
-    several row pairs in turn."""
+    """More rows than the bf16 row kernel's persistent grid streams at once
+    (3 blocks of two rows per compute unit), so its thread groups take
+    several rows in turn, averaged and worker rows alike."""
     fgd, torch = env
     M, U, K, k = 4, 520, 700, 50
     A, W = slog.numpy_logits(M, U, K, K + 4, "bf16", seed=43)
@@ -277,11 +293,11 @@ def test_js_bf16_rows_beyond_the_persistent_grid(env):
 
 
 @pytest.mark.parametrize("dtype,K", [("f32", 140_003), ("bf16", 270_001)])
-def test_js_rows_beyond_the_recorded_batches(env, dtype, K):
-    """Vocabularies long enough that a thread of the per-token kernel reads
-    more than the 16 batches of 8 vectors whose maxima it records, so the
-    candidate pass must read every batch past them too; a head of large
-    logits placed at the row's end lands in those batches."""
+def test_js_batches_longer_than_one_load(env, dtype, K):
+    """Vocabularies long enough that a thread's batch of the averaged row
+    holds more than the 4 vectors the candidate pass loads at once (9 here),
+    so a batch is read again in several loads; a head of large logits placed
+    at the row's end lands in the last batches."""
     fgd, torch = env
     M, U, k = 2, 3, 100
     A, W = slog.numpy_logits(M, U, K, -(-K // 8) * 8, "f32", seed=K)  # 16-byte rows in both storages
@@ -317,6 +333,41 @@ def test_js_row_padding_is_never_used(env, dtype):
     d1, m1, t1 = _run(fgd, torch, A, W, dtype, K, k)
     assert np.array_equal(t0, t1)
     assert np.array_equal(d0, d1) and np.array_equal(m0, m1)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_candidate_overflow_mixed_with_ordinary_tokens(env, dtype):
+    """Tokens whose averaged row is one repeated logit give every element as
+    a candidate of the per-token wave selection (more than it holds); those
+    tokens alone are handed to the radix kernel, in the same call as
+    ordinary tokens that the wave kernel finishes, and the workspace's junk
+    flags must not make either kernel take or skip the wrong token."""
+    fgd, torch = env
+    M, U, K, k = 3, 9, 3000, 100
+    A, W = slog.numpy_logits(M, U, K, K, dtype, seed=77)
+    for u in (1, 4, 8):
+        A[u, :K] = A[u, 0]
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+def test_js_workspace_reused_across_shapes(env):
+    """One workspace serves calls of different sizes in turn (bf16, then
+    float32 over fewer tokens, then bf16 again): each call writes what it
+    reads, so the results equal those of calls with fresh workspaces."""
+    fgd, torch = env
+    shapes = [(4, 9, 3001, 3008, "bf16", 100), (2, 5, 777, 780, "f32", 300), (3, 11, 1500, 1504, "bf16", 10)]
+    need = max(fgd.fgd_js_workspace_size(dt, M, U) for M, U, _, _, dt, _ in shapes)
+    ws = torch.full((need,), 0x5A, dtype=torch.uint8, device="cuda")
+    for i, (M, U, K, ldk, dtype, k) in enumerate(shapes):
+        A, W = slog.numpy_logits(M, U, K, ldk, dtype, seed=900 + i)
+        d0, _, t0 = _run(fgd, torch, A, W, dtype, K, k)
+        conv = (lambda x: torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)) if dtype == "bf16" \
+            else (lambda x: torch.from_numpy(x).cuda())
+        d = torch.empty((M, U), dtype=torch.float64, device="cuda")
+        tops = torch.empty((U, k), dtype=torch.int32, device="cuda")
+        fgd.fgd_js_distance(conv(A), conv(W), dtype, M, U, K, ldk, k, d, None, tops, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(d.cpu().numpy(), d0) and np.array_equal(tops.cpu().numpy(), t0)
 
 
 def _random_js_case(i):
