@@ -143,6 +143,15 @@ def js_bench(args, fgd, torch):
     elapsed = time.perf_counter() - t0
     step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
     nbytes = (M + 1) * U * K * es
+    # The row kernel's access pattern without its arithmetic, on the same
+    # logits, timed the same way right after the calls.
+    pev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    pev[0].record(stream)
+    for i in range(args.steps):
+        fgd.fgd_stream_js_pattern(A, W, w["dtype"], M, U, K, K, ws, None, stream)
+        pev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    pat_ms = sum(pev[i].elapsed_time(pev[i + 1]) for i in range(args.steps)) / args.steps
     logits = (M + 1) * U * K
     ms = elapsed * 1e3 / args.steps
     avg = sum(step_ms) / len(step_ms)
@@ -169,6 +178,10 @@ def js_bench(args, fgd, torch):
                         "kernel": "one fgd_js_distance call (row kernel, per-token kernel, mean kernel)",
                         "kernel_avg_ms": round(avg, 4), "bytes_per_launch": nbytes},
            "kernel_source_hash": lib_hash["js"], "library_source_hash": lib_hash}
+    out["pattern_reference"] = {"ms": round(pat_ms, 4), "gbs": round(nbytes / (pat_ms * 1e-3) / 1e9, 1),
+                                "call_rate_vs_pattern": round(pat_ms / avg, 4),
+                                "what": "the row kernel's loads (same grid, rows, lanes, cache hints, prefetch) "
+                                        "without its arithmetic; the call adds the per-token kernels"}
     out["copy_reference_gbs"] = copy_reference(fgd, torch, A.device, args.copy_gb)
     if not args.no_cpu_baseline:
         from oracle import js as ojs

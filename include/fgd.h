@@ -54,11 +54,13 @@
  *  - The engine's compute calls are not meant to be recorded by HIP stream
  *    capture: a topology upload copies from a pinned host staging slot that
  *    later uploads reuse, after waiting on the slot's event from the host.
- *    fgd_js_distance and fgd_stream_copy enqueue kernels only.
+ *    fgd_js_distance, fgd_stream_js_pattern and fgd_stream_copy enqueue
+ *    kernels only.
  *  - Engine calls run on the engine's device (fgd_config.device): they make
  *    it current for their duration and restore the caller's current device
  *    before returning.  The engine-free calls (fgd_js_distance,
- *    fgd_stream_copy) run on the caller's current device.
+ *    fgd_stream_js_pattern, fgd_stream_copy) run on the caller's current
+ *    device.
  */
 #ifndef FGD_H
 #define FGD_H
@@ -410,6 +412,16 @@ fgd_status fgd_js_workspace_size(int32_t dtype, int32_t num_workers, int64_t num
  * 16, 32, 64} (else FGD_ERR_UNSUPPORTED).  Enqueued on `stream`. */
 fgd_status fgd_stream_step_pattern(fgd_engine *e, void *theta_prev, const void *theta_local, float *momentum,
                                    void *stream);
+
+/* Streaming reference for fgd_js_distance: the loads of its row kernel (the
+ * same grid, rows, lane elements, cache hints and prefetch) and none of its
+ * arithmetic; the logits are only read, and the workspace is left undefined.
+ * Its rate is the practical ceiling of that kernel's access pattern.  Same
+ * logits, sizes and workspace rules as fgd_js_distance.  Enqueued on
+ * `stream`. */
+fgd_status fgd_stream_js_pattern(const void *logits_avg, const void *logits_workers, int32_t dtype,
+                                 int32_t num_workers, int64_t num_tokens, int64_t vocab, int64_t ldk, void *workspace,
+                                 int64_t workspace_bytes, void *stream);
 
 /* Plain device copy of `bytes` bytes (16-byte aligned pointers, bytes % 16 ==
  * 0) on `stream`: the streaming reference against which the step's

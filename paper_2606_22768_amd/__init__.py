@@ -82,6 +82,7 @@ def _load():
         "fgd_stream_step_pattern": (I32, [P, P, P, P, P]),
         "fgd_js_distance": (I32, [P, P, I32, I32, I64, I64, I64, I32, P, P, P, P, I64, P]),
         "fgd_js_workspace_size": (I32, [I32, I32, I64, ctypes.POINTER(I64)]),
+        "fgd_stream_js_pattern": (I32, [P, P, I32, I32, I64, I64, I64, P, I64, P]),
         "fgd_status_string": (ctypes.c_char_p, [I32]),
         "fgd_last_error": (ctypes.c_char_p, []),
         "fgd_source_hash": (ctypes.c_char_p, [I32]),
@@ -309,6 +310,17 @@ def fgd_js_distance(logits_avg, logits_workers, dtype, num_workers, num_tokens, 
                                int(num_tokens), int(vocab), int(ldk), int(top_k), _dev(d_out), _dev(mean_out),
                                _dev(topk_out), _dev(workspace), int(workspace_bytes), _stream(stream)),
            "fgd_js_distance")
+
+
+def fgd_stream_js_pattern(logits_avg, logits_workers, dtype, num_workers, num_tokens, vocab, ldk, workspace,
+                          workspace_bytes=None, stream=None):
+    """The JS row kernel's loads without its arithmetic (a streaming
+    reference); same arguments as fgd_js_distance's logits and workspace."""
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.fgd_stream_js_pattern(_dev(logits_avg), _dev(logits_workers), DTYPES.get(dtype, dtype),
+                                     int(num_workers), int(num_tokens), int(vocab), int(ldk), _dev(workspace),
+                                     int(workspace_bytes), _stream(stream)), "fgd_stream_js_pattern")
 
 
 def js_distance(logits_avg, logits_workers, top_k=100, vocab=None, d_out=None, mean_out=None, topk_out=None,

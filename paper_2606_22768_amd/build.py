@@ -31,7 +31,7 @@ LIB = os.path.join(PKG, "libfgd.so")
 
 HIP_SOURCES = ["engine.hip", "kernels_f32.hip", "kernels_bf16.hip", "kernels_f32_ms.hip", "kernels_bf16_ms.hip",
                "kernels_f32_split.hip", "kernels_bf16_split.hip", "kernels_wg.hip", "kernels_common.hip",
-               "js.hip"]
+               "js.hip", "js_api.hip"]
 CXX_SOURCES = ["topology.cpp"]
 
 ARCH = "gfx950"
@@ -49,9 +49,9 @@ def source_hashes(root: str = ROOT) -> dict:
     all   every file under paper_2606_22768_amd/csrc and include/fgd.h;
     step  the HIP sources of the outer step, its split halves, consensus,
           finalize and copy kernels and their launches (every .hip/.hpp but
-          the JS distance's js.hip and js.hpp);
-    js    the JS distance kernels, their launcher header and the kernel
-          header they include.
+          the JS distance's js.hip, js.hpp and js_api.hip);
+    js    the JS distance kernels, their launcher header, their C entry
+          points and the headers those include (kernels.hpp, api.hpp).
     Traffic counters and timings are valid only for the hash they were
     taken with."""
     csrc = os.path.join(root, "paper_2606_22768_amd", "csrc")
@@ -62,9 +62,9 @@ def source_hashes(root: str = ROOT) -> dict:
             data = name.encode() + b"\0" + f.read()
         hs["all"].update(data)
         if name.endswith((".hip", ".hpp")):
-            if name not in ("js.hip", "js.hpp"):
+            if name not in ("js.hip", "js.hpp", "js_api.hip"):
                 hs["step"].update(data)
-            if name in ("js.hip", "js.hpp", "kernels.hpp"):
+            if name in ("js.hip", "js.hpp", "js_api.hip", "kernels.hpp", "api.hpp"):
                 hs["js"].update(data)
     with open(os.path.join(root, "include", "fgd.h"), "rb") as f:
         hs["all"].update(b"fgd.h\0" + f.read())

@@ -872,6 +872,47 @@ void js_token_radix_kernel(JsParams a, JsWork w, const int32_t *flag) {
     }
 }
 
+// The row kernel's loads without its arithmetic: the same grid, row groups,
+// streaming order, lane elements and prefetch, and no LDS table; each wave
+// folds what it loads into one word (an XOR) and stores it over its part in
+// the workspace, so no load can be dropped.  Its rate is the practical
+// ceiling of the row kernel's access pattern.
+template <class E>
+__global__ __launch_bounds__(kRowsBlock) void js_rows_pattern_kernel(JsParams a, JsWork w) {
+    const int lt = threadIdx.x % kRowThreads;
+    const int64_t i_first = static_cast<int64_t>(lt) * E::kPer;
+    constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * E::kPer;
+    const int64_t G = static_cast<int64_t>(gridDim.x) * kRowsPerBlock;
+    const int64_t R = static_cast<int64_t>(a.M + 1) * a.U;
+    auto row_of = [&](int64_t r) -> rsrc_t {
+        return r < a.U ? js_row(a.avg, r, a.ldk, E::kElem) : js_row(a.workers, r - a.U, a.ldk, E::kElem);
+    };
+    const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kRowThreads));
+    int64_t r = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + g;
+    u32x4 nxt = {0, 0, 0, 0};
+    if (r < R && i_first < a.K)
+        nxt = __builtin_amdgcn_raw_buffer_load_b128(row_of(r), static_cast<uint32_t>(i_first * E::kElem), 0,
+                                                    kLoadPolicy);
+    for (; r < R; r += G) {
+        const bool has_next = r + G < R;
+        const rsrc_t rr = row_of(r);
+        const rsrc_t rn = has_next ? row_of(r + G) : rr;
+        uint32_t acc = 0;
+        for (int64_t i0 = i_first; i0 < a.K; i0 += kStride) {
+            const u32x4 cur = nxt;
+            if (i0 + kStride < a.K)
+                nxt = __builtin_amdgcn_raw_buffer_load_b128(rr, static_cast<uint32_t>((i0 + kStride) * E::kElem), 0,
+                                                            kLoadPolicy);
+            else if (has_next)
+                nxt = __builtin_amdgcn_raw_buffer_load_b128(rn, static_cast<uint32_t>(i_first * E::kElem), 0,
+                                                            kLoadPolicy);
+            acc ^= cur[0] ^ cur[1] ^ cur[2] ^ cur[3];
+        }
+        for (int o = kWave / 2; o > 0; o >>= 1) acc ^= static_cast<uint32_t>(__shfl_xor(static_cast<int>(acc), o));
+        if ((threadIdx.x & (kWave - 1)) == 0) reinterpret_cast<uint32_t *>(w.part)[r * kRowWaves + lt / kWave] = acc;
+    }
+}
+
 // ------------------------------------------------- per token, one wave each
 constexpr int kWaveTokens = kBlock / kWave;       // tokens per block of js_token_wave_kernel
 constexpr int kRtPerLane = kRowThreads / kWave;   // row threads whose batch maxima a lane takes
@@ -1208,6 +1249,21 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
         if (hipGetLastError() != hipSuccess) return false;
     }
     return true;
+}
+
+bool js_pattern_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K,
+                       int64_t ldk, void *workspace, int num_cus, hipStream_t stream) {
+    JsParams p{avg, workers, nullptr, nullptr, U, K, ldk, M, 1};
+    JsWork w{static_cast<LsePart *>(workspace), nullptr, nullptr, nullptr, 1};
+    const int64_t groups = ((static_cast<int64_t>(M) + 1) * U + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kRowsBlocksPerCu) * std::max(num_cus, 1));
+    if (bf16)
+        hipLaunchKernelGGL(js_rows_pattern_kernel<JsBF16>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0,
+                           stream, p, w);
+    else
+        hipLaunchKernelGGL(js_rows_pattern_kernel<JsF32>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0,
+                           stream, p, w);
+    return hipGetLastError() == hipSuccess;
 }
 
 }  // namespace fgd

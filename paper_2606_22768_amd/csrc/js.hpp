@@ -18,4 +18,10 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
                int32_t k, double *d_out, double *mean_out, int32_t *topk_out, void *workspace, int num_cus,
                hipStream_t stream);
 
+// Launches the row kernel's access pattern without its arithmetic on
+// `stream` (see js_rows_pattern_kernel); it writes only the workspace's
+// log-sum-exp parts.  False if the launch failed.
+bool js_pattern_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K,
+                       int64_t ldk, void *workspace, int num_cus, hipStream_t stream);
+
 }  // namespace fgd

@@ -55,7 +55,13 @@ def test_component_hashes_cover_their_sources(tree):
     _touch(tree, "js.hpp")
     h1b = _hashes(tree)
     assert h1b["step"] == h1["step"] and h1b["js"] != h1["js"]  # the JS launcher's header
-    h1 = h1b
+    _touch(tree, "js_api.hip")
+    h1c = _hashes(tree)
+    assert h1c["step"] == h1b["step"] and h1c["js"] != h1b["js"]  # the JS entry points
+    _touch(tree, "api.hpp")
+    h1d = _hashes(tree)
+    assert h1d["step"] != h1c["step"] and h1d["js"] != h1c["js"]  # the error helpers both use
+    h1 = h1d
     _touch(tree, "engine.hip")
     h2 = _hashes(tree)
     assert h2["step"] != h1["step"] and h2["js"] == h1["js"]  # launch code belongs to the step only

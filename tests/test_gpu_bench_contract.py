@@ -60,6 +60,8 @@ def test_js_bench_line_is_one_json_object():
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
     assert r["bytes_per_launch"] == 9 * 2048 * 128256 * 2 and 0.0 < r["frac"] <= 1.0
     assert abs(r["achieved"] - r["bytes_per_launch"] / (r["kernel_avg_ms"] * 1e6)) <= 1e-3 * r["achieved"] + 0.01
+    pr = d["pattern_reference"]                       # the row kernel's loads without arithmetic
+    assert pr["ms"] > 0 and pr["gbs"] > 0 and 0.0 < pr["call_rate_vs_pattern"] <= 1.5
 
 
 def test_packed_placement_and_split_mode_lines():

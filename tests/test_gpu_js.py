@@ -370,6 +370,34 @@ def test_js_workspace_reused_across_shapes(env):
         assert np.array_equal(d.cpu().numpy(), d0) and np.array_equal(tops.cpu().numpy(), t0)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_pattern_reference_reads_only(env, dtype):
+    """The row kernel's access pattern without arithmetic (the bench's
+    streaming reference) leaves the logits bit-identical, and takes the same
+    argument checks as the distance."""
+    fgd, torch = env
+    M, U, K = 3, 700, 1001
+    ldk = -(-K // 8) * 8
+    A, W = slog.numpy_logits(M, U, K, ldk, dtype, seed=88)
+    conv = (lambda x: torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)) if dtype == "bf16" \
+        else (lambda x: torch.from_numpy(x).cuda())
+    gA, gW = conv(A), conv(W)
+    ws = _workspace(fgd, torch, dtype, M, U)
+    fgd.fgd_stream_js_pattern(gA, gW, dtype, M, U, K, ldk, ws)
+    torch.cuda.synchronize()
+    raw = (lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)) if dtype == "bf16" \
+        else (lambda t: t.cpu().numpy())
+    assert np.array_equal(raw(gA).view(np.uint8), A.view(np.uint8))
+    assert np.array_equal(raw(gW).view(np.uint8), W.view(np.uint8))
+    for kw in (dict(workspace_bytes=ws.numel() - 1), dict(vocab=ldk + 1), dict(num_workers=0)):
+        args = dict(num_workers=M, vocab=K, workspace_bytes=None)
+        args.update(kw)
+        with pytest.raises(fgd.FgdError) as e:
+            fgd.fgd_stream_js_pattern(gA, gW, dtype, args["num_workers"], U, args["vocab"], ldk, ws,
+                                      args["workspace_bytes"])
+        assert e.value.status == fgd.FGD_ERR_INVALID_ARG
+
+
 def _random_js_case(i):
     """Seeded random JS configuration: workers, tokens, vocabulary (tiny,
     mid, large), row stride, storage, k up to 1024, and a logit kind: plain,
