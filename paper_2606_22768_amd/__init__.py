@@ -339,14 +339,47 @@ def js_distance(logits_avg, logits_workers, top_k=100, vocab=None, d_out=None, m
             or not logits_avg.is_contiguous():
         raise ValueError("expected contiguous logits_avg [U][ldk] and logits_workers [M][U][ldk]")
     K = ldk if vocab is None else int(vocab)
+    # The kernels write through the raw pointers, so a caller's buffer of
+    # another dtype, a smaller one or a non-contiguous one is refused here,
+    # before anything is enqueued; then every tensor must share the logits'
+    # GPU.
+    _check_js_buffer(d_out, "d_out", torch.float64, M * U)
+    _check_js_buffer(mean_out, "mean_out", torch.float64, M)
+    _check_js_buffer(topk_out, "topk_out", torch.int32, U * int(top_k))
+    need_ws = fgd_js_workspace_size(dtype, M, U)
+    _check_js_buffer(workspace, "workspace", None, need_ws)
     dev = logits_avg.device
+    for name, t in (("logits_avg", logits_avg), ("logits_workers", logits_workers), ("d_out", d_out),
+                    ("mean_out", mean_out), ("topk_out", topk_out), ("workspace", workspace)):
+        if t is not None and (not t.is_cuda or t.device != dev):
+            raise ValueError(f"{name}: expected a tensor on the logits' GPU, got {t.device}")
     d_out = torch.empty((M, U), dtype=torch.float64, device=dev) if d_out is None else d_out
     mean_out = torch.empty(M, dtype=torch.float64, device=dev) if mean_out is None else mean_out
     if workspace is None:
-        workspace = torch.empty(fgd_js_workspace_size(dtype, M, U), dtype=torch.uint8, device=dev)
+        workspace = torch.empty(need_ws, dtype=torch.uint8, device=dev)
     fgd_js_distance(logits_avg, logits_workers, dtype, M, U, K, ldk, top_k, d_out, mean_out, topk_out, workspace,
                     None, stream)
     return d_out, mean_out
+
+
+def _check_js_buffer(t, name, dtype, need):
+    """A caller-supplied js_distance buffer: a contiguous tensor of `dtype`
+    (any dtype when None) holding at least `need` elements (bytes when dtype
+    is None)."""
+    import torch
+
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    size = t.numel() if dtype is not None else t.numel() * t.element_size()
+    if size < need:
+        unit = "elements" if dtype is not None else "bytes"
+        raise ValueError(f"{name}: needs at least {need} {unit}, got {size}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
 
 
 def fgd_stream_step_pattern(h, theta_prev, theta_local, momentum, stream=None):

@@ -475,6 +475,40 @@ def test_consensus_outputs_are_checked_before_any_launch(call):
     eng.close()
 
 
+@pytest.mark.parametrize("dtype", [None, "bf16"])
+def test_js_buffers_are_checked_before_any_launch(dtype):
+    """js_distance writes d, the means, the token sets and its workspace
+    through raw pointers, so a caller's buffer of another dtype, a smaller
+    one or a non-contiguous one is refused before anything is enqueued, and
+    so are tensors off the GPU (host tensors here: any call that got through
+    the checks would stop at the last one)."""
+    import torch
+    M, U, K, k = 3, 5, 64, 10
+    t = torch.float32 if dtype is None else torch.bfloat16
+    A, W = torch.zeros((U, K), dtype=t), torch.zeros((M, U, K), dtype=t)
+    ws = fgd.fgd_js_workspace_size("f32" if dtype is None else dtype, M, U)
+
+    def run(**kw):
+        fgd.js_distance(A, W, top_k=k, **kw)
+
+    with pytest.raises(TypeError, match="float64"):
+        run(d_out=torch.zeros((M, U), dtype=torch.float32))
+    with pytest.raises(ValueError, match="needs at least"):
+        run(d_out=torch.zeros(M * U - 1, dtype=torch.float64))
+    with pytest.raises(ValueError, match="contiguous"):
+        run(d_out=torch.zeros((M, 2 * U), dtype=torch.float64)[:, ::2])
+    with pytest.raises(ValueError, match="needs at least"):
+        run(mean_out=torch.zeros(M - 1, dtype=torch.float64))
+    with pytest.raises(TypeError, match="int32"):
+        run(topk_out=torch.zeros((U, k), dtype=torch.int64))
+    with pytest.raises(ValueError, match="needs at least"):
+        run(topk_out=torch.zeros((U, k - 1), dtype=torch.int32))
+    with pytest.raises(ValueError, match="needs at least"):
+        run(workspace=torch.zeros(ws - 1, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="GPU"):
+        run(workspace=torch.zeros(ws, dtype=torch.uint8))
+
+
 def test_noalloc_consensus_rejects_arguments_before_any_device_call():
     """The scratch-free consensus call checks its arguments first: more workers
     than its static scratch holds, bad sizes, dtype or alignment."""
