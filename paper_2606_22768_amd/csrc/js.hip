@@ -480,10 +480,11 @@ __device__ inline void load_batch(rsrc_t r, int64_t i0, int64_t K, int64_t strid
     }
 }
 // ------------------------------------------------------------ workspace
-// Between the call's two kernels: per row, the (shift, sum) of each of its
-// kRowWaves waves; per token, the averaged row's largest key in each batch
-// of every thread.
-constexpr int kRowThreads = kBlock;                     // threads (lanes) per row, js_token_kernel's block
+// From the row kernel to the per-token kernels: per row, the (shift, sum)
+// of each of its kRowWaves waves; per token, each row thread's largest key
+// of the averaged row and the largest key of each of its batches; a flag per
+// token.
+constexpr int kRowThreads = kBlock;                     // threads per row (the radix kernel's block)
 constexpr int kRowWaves = kRowThreads / kWave;          // wave partials per row
 constexpr int kRowsPerBlock = 2;                        // rows a js_rows_kernel block streams at once
 constexpr int kRowsBlock = kRowThreads * kRowsPerBlock;
@@ -1236,7 +1237,7 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
         hipLaunchKernelGGL(js_rows_kernel<JsBF16>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
         if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsBF16>, token_waves, dim3(kBlock), 0, stream, p, w);
         hipLaunchKernelGGL(js_token_radix_kernel<JsBF16>, tokens, dim3(kBlock), 0, stream, p, w,
-                           wave_path ? w.flag : nullptr);
+                           wave_path ? static_cast<const int32_t *>(w.flag) : nullptr);
     } else {
         hipLaunchKernelGGL(js_rows_kernel<JsF32>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
         if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsF32>, token_waves, dim3(kBlock), 0, stream, p, w);
