@@ -716,10 +716,13 @@ void js_token_radix_kernel(JsParams a, JsWork w, const int32_t *flag) {
 
     const int tid = threadIdx.x;
     const int k = a.k;
-    load_exp_table(tab);
-
+    bool have_tab = false;
     for (int64_t u = blockIdx.x; u < a.U; u += gridDim.x) {
         if (flag && flag[u] == 0) continue;  // the same in every thread
+        if (!have_tab) {  // the blocks of unflagged tokens leave without it
+            load_exp_table(tab);
+            have_tab = true;
+        }
         const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
         const double lse_a = row_lse(w.part + u * kRowWaves, tab);
         {
