@@ -385,8 +385,8 @@ fgd_status fgd_read_timing(fgd_engine *e, double *total_ms, int64_t *count);
  *                   16-byte aligned, owned by the caller, overlapping none
  *                   of the arrays above; the call leaves it undefined (it
  *                   carries each row's log-sum-exp parts and the averaged
- *                   rows' per-thread batch maxima from the call's first
- *                   kernel to its second)
+ *                   rows' largest vector maxima per thread from the call's
+ *                   first kernel to the next)
  * Enqueued on `stream`; deterministic.  Calls that share a workspace must
  * not run concurrently. */
 fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, int32_t dtype, int32_t num_workers,
@@ -395,7 +395,7 @@ fgd_status fgd_js_distance(const void *logits_avg, const void *logits_workers, i
                            void *stream);
 
 /* Device workspace fgd_js_distance needs for these sizes: 64 bytes per row
- * ((M + 1) U rows) and 4 KiB (bfloat16) or 8 KiB (float32) per token.  Host
+ * ((M + 1) U rows) and 4 KiB plus 4 bytes per token (either dtype).  Host
  * only. */
 fgd_status fgd_js_workspace_size(int32_t dtype, int32_t num_workers, int64_t num_tokens, int64_t *bytes);
 

@@ -18,11 +18,11 @@
 //   js_rows_kernel         streams all (M + 1) U rows once (persistent, no
 //                          barriers): per row, each wave's (shift, sum) part
 //                          of the log-sum-exp; per averaged row, each row
-//                          thread's largest key and its batches' largest keys
+//                          thread's four largest vector maxima (key, index)
 //   js_token_wave_kernel   (k <= 256) one wave per token: the averaged row's
 //                          lse from its parts, the selection (a threshold from
-//                          the row threads' maxima, a second read of only the
-//                          batches that reach it), the JS terms; a token with
+//                          the recorded maxima, a second read of only the
+//                          vectors that reach it), the JS terms; a token with
 //                          too many candidates is flagged
 //   js_token_radix_kernel  per token, a radix select over the whole row: every
 //                          token when k > 256, else only the flagged ones
@@ -464,32 +464,18 @@ __device__ inline double js_term(double lp, double lq) {
 }
 
 constexpr int kJsGroup = 8;  // workers whose logits are gathered together
-constexpr int kJsBatch = 4;   // vectors of the averaged row a thread loads before using them
 
-// Loads the vectors of a row at i0, i0 + stride, ... (the first nd <=
-// kJsBatch of them) so that their latencies overlap; the others, and those
-// at or past K, read as zero and are never used.
-template <class E>
-__device__ inline void load_batch(rsrc_t r, int64_t i0, int64_t K, int64_t stride, int nd, u32x4 (&t)[kJsBatch]) {
-#pragma unroll
-    for (int d = 0; d < kJsBatch; ++d) {
-        const int64_t i = i0 + d * stride;
-        t[d] = u32x4{0, 0, 0, 0};
-        if (d < nd && i < K)
-            t[d] = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>(i * E::kElem), 0, kLoadPolicy);
-    }
-}
 // ------------------------------------------------------------ workspace
 // From the row kernel to the per-token kernels: per row, the (shift, sum)
-// of each of its kRowWaves waves; per token, each row thread's largest key
-// of the averaged row and the largest key of each of its batches; a flag per
-// token.
+// of each of its kRowWaves waves; per token and row thread, the averaged
+// row's kTopVecs largest vector maxima; a flag per token.
 constexpr int kRowThreads = kBlock;                     // threads per row (the radix kernel's block)
 constexpr int kRowWaves = kRowThreads / kWave;          // wave partials per row
 constexpr int kRowsPerBlock = 2;                        // rows a js_rows_kernel block streams at once
 constexpr int kRowsBlock = kRowThreads * kRowsPerBlock;
 constexpr int kRowsBlocksPerCu = 3;                     // bf16 LDS: 3 x 46 KB of the CU's 160 KB
-constexpr int kJsBatches = 16;                          // batches per thread of the averaged row
+constexpr int kTopVecs = 4;                             // vector maxima a row thread of an averaged row keeps
+constexpr int64_t kTopIndexLimit = 1 << 16;             // vectors per row thread their 16-bit indices can name
 
 // A wave's part of a row's log-sum-exp: sum exp(z - m) over its lanes'
 // elements (s = 0: none).
@@ -499,33 +485,31 @@ struct LsePart {
 
 struct JsWork {
     LsePart *part;   // [(M + 1) U][kRowWaves]: row u < U is token u's averaged row, U + m U + u worker m's
-    void *bmax;      // [U][kRowThreads][kJsBatches] keys: uint16 (bf16) or uint32 (float32); 0 = no batch
-    void *tmax;      // [U][kRowThreads] keys: each row thread's largest (0: no element)
+    u32x4 *top;      // [U][kRowThreads]: top entries, largest first (0: none; see TopVecs)
     int32_t *flag;   // [U]: 1 where the per-token wave kernel left the token to the radix kernel
-    int32_t bvec;    // vectors per batch
 };
 
-// A row thread's batch maxima in registers: two uint16 keys per register
-// (bf16) or one uint32 key (float32); 16-byte vectors in memory.
+// The kTopVecs largest vector maxima of a row thread, each entry the
+// 16-bit key of the vector's largest element (the key itself for bf16, its
+// top 16 bits for float32) above the vector's index among the thread's
+// vectors: key16 << 16 | index, so entries order by key, then index.
 template <class E>
-struct BatchKeys {
-    static constexpr int kRegs = E::kBf16 ? kJsBatches / 2 : kJsBatches;
-    static constexpr int kVecs = kRegs / 4;
-    uint32_t r[kRegs];
-    // Batch b's key.
-    __device__ uint32_t key(int b) const {
-        if constexpr (E::kBf16)
-            return (r[b / 2] >> (16 * (b % 2))) & 0xFFFFu;
-        else
-            return r[b];
+struct TopVecs {
+    uint32_t t[kTopVecs] = {0, 0, 0, 0};  // largest first; 0: no vector
+    __device__ static uint32_t key16(uint32_t key) { return E::kBf16 ? key : key >> 16; }
+    // Takes entry e in (entries are distinct): each slot keeps the median of
+    // itself, the slot above and e, from the bottom up.
+    __device__ void insert(uint32_t e) {
+#pragma unroll
+        for (int i = kTopVecs - 1; i > 0; --i) t[i] = med3(t[i], t[i - 1], e);
+        t[0] = max(t[0], e);
     }
+    __device__ static uint32_t med3(uint32_t a, uint32_t b, uint32_t c) { return max(min(a, b), min(max(a, b), c)); }
 };
 
-// Vectors per batch: every thread's vectors of a row fit in kJsBatches batches.
-inline int32_t js_batch_vectors(int64_t K, int per) {
-    const int64_t vecs = (K + per - 1) / per;                       // 16-byte vectors per row
-    const int64_t nvec = (vecs + kRowThreads - 1) / kRowThreads;    // per thread, at most
-    return static_cast<int32_t>(std::max<int64_t>(1, (nvec + kJsBatches - 1) / kJsBatches));
+// Vectors per row thread, at most (a row of K logits, P per vector).
+inline int64_t js_thread_vectors(int64_t K, int per) {
+    return ((K + per - 1) / per + kRowThreads - 1) / kRowThreads;
 }
 
 // A wave's (shift, sum) from its lanes' (m, s): the largest shift, then
@@ -557,18 +541,16 @@ __device__ inline double row_lse(const LsePart *p, const double *tab) {
 // One row's log-sum-exp terms for the thread's elements i_first, i_first +
 // kStride, ... into st.  `nxt` holds the row's first vector on entry and,
 // when has_next, the first vector of row rn on return, so that the next
-// row's load overlaps this row's end.  With kAvg it also keeps the largest
-// key of each batch of bvec vectors (bm, at most kJsBatches; all 0 on
-// entry) and the thread's largest key (kmax, 0 on entry).
+// row's load overlaps this row's end.  With kAvg it also keeps the thread's
+// kTopVecs largest vector maxima (top, empty on entry; indices past 16 bits
+// wrap, and the per-token wave kernel is then not used).
 template <class E, bool kAvg>
-__device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_first, int64_t K, int bvec,
-                                 u32x4 &nxt, RowLse &st, const double *etab, const double *tab, BatchKeys<E> &bm,
-                                 uint32_t &kmax) {
+__device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_first, int64_t K, u32x4 &nxt,
+                                 RowLse &st, const double *etab, const double *tab, TopVecs<E> &top) {
     constexpr int P = E::kPer;
     constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * P;
-    int b = 0, left = bvec;
-    uint32_t bmax = 0;
-    for (int64_t i0 = i_first; i0 < K; i0 += kStride) {
+    uint32_t v = 0;
+    for (int64_t i0 = i_first; i0 < K; i0 += kStride, ++v) {
         const u32x4 cur = nxt;
         if (i0 + kStride < K)
             nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * E::kElem), 0,
@@ -577,23 +559,7 @@ __device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_f
             nxt = __builtin_amdgcn_raw_buffer_load_b128(rn, static_cast<uint32_t>(i_first * E::kElem), 0, kLoadPolicy);
         float x[P];
         if constexpr (kAvg || !E::kBf16) vec_values<E>(cur, i0, K, x);  // past K: -inf
-        if constexpr (kAvg) {
-            bmax = max(bmax, E::key_of(vec_max<P>(x)));
-            if (--left == 0 || i0 + kStride >= K) {
-                if constexpr (E::kBf16) {
-                    const uint32_t put = (b & 1) ? bmax << 16 : bmax;
-#pragma unroll
-                    for (int j = 0; j < BatchKeys<E>::kRegs; ++j) bm.r[j] |= j == b / 2 ? put : 0u;
-                } else {
-#pragma unroll
-                    for (int j = 0; j < BatchKeys<E>::kRegs; ++j) bm.r[j] = j == b ? bmax : bm.r[j];
-                }
-                kmax = max(kmax, bmax);
-                ++b;
-                left = bvec;
-                bmax = 0;
-            }
-        }
+        if constexpr (kAvg) top.insert((TopVecs<E>::key16(E::key_of(vec_max<P>(x))) << 16) | (v & 0xFFFFu));
         if constexpr (E::kBf16)
             bf16_lse_add(st, cur, i0, K, etab, tab);
         else
@@ -601,8 +567,8 @@ __device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_f
     }
 }
 
-// Every row's wave parts of its log-sum-exp, and the averaged rows' batch
-// and thread maxima, into the workspace.  Persistent: thread group g
+// Every row's wave parts of its log-sum-exp, and the averaged rows'
+// largest vector maxima per thread, into the workspace.  Persistent: thread group g
 // (kRowThreads threads; two per block) streams rows g, g + G, ... (G
 // groups) of the streaming order below; thread lt of a group takes the
 // elements lt * P + j * kStride of its row.  No barriers after the tables
@@ -637,27 +603,17 @@ void js_rows_kernel(JsParams a, JsWork w) {
         const rsrc_t rr = row_of(r);
         const rsrc_t rn = has_next ? row_of(r + G) : rr;
         RowLse st;
-        BatchKeys<E> bm;
-#pragma unroll
-        for (int j = 0; j < BatchKeys<E>::kRegs; ++j) bm.r[j] = 0;
-        uint32_t kmax = 0;
+        TopVecs<E> top;
         const bool avg = r < a.U;
         if (avg)
-            row_terms<E, true>(rr, rn, has_next, i_first, a.K, w.bvec, nxt, st, etab, tab, bm, kmax);
+            row_terms<E, true>(rr, rn, has_next, i_first, a.K, nxt, st, etab, tab, top);
         else
-            row_terms<E, false>(rr, rn, has_next, i_first, a.K, w.bvec, nxt, st, etab, tab, bm, kmax);
+            row_terms<E, false>(rr, rn, has_next, i_first, a.K, nxt, st, etab, tab, top);
         double ml, sl;
         row_lse_lane(st, ml, sl, tab);
         const LsePart p = wave_lse(ml, sl, tab);
         if ((threadIdx.x & (kWave - 1)) == 0) w.part[r * kRowWaves + lt / kWave] = p;
-        if (avg) {
-            using Key = typename std::conditional<E::kBf16, uint16_t, uint32_t>::type;
-            u32x4 *dst = reinterpret_cast<u32x4 *>(static_cast<Key *>(w.bmax) + (r * kRowThreads + lt) * kJsBatches);
-#pragma unroll
-            for (int v = 0; v < BatchKeys<E>::kVecs; ++v)
-                dst[v] = u32x4{bm.r[4 * v], bm.r[4 * v + 1], bm.r[4 * v + 2], bm.r[4 * v + 3]};
-            static_cast<Key *>(w.tmax)[r * kRowThreads + lt] = static_cast<Key>(kmax);
-        }
+        if (avg) w.top[r * kRowThreads + lt] = u32x4{top.t[0], top.t[1], top.t[2], top.t[3]};
     }
 }
 
@@ -919,7 +875,7 @@ __global__ __launch_bounds__(kRowsBlock) void js_rows_pattern_kernel(JsParams a,
 
 // ------------------------------------------------- per token, one wave each
 constexpr int kWaveTokens = kBlock / kWave;       // tokens per block of js_token_wave_kernel
-constexpr int kRtPerLane = kRowThreads / kWave;   // row threads whose batch maxima a lane takes
+constexpr int kRtPerLane = kRowThreads / kWave;   // row threads whose recorded maxima a lane takes
 constexpr int kWaveCand = 512;                    // candidates a token may have
 constexpr int kCandPerLane = kWaveCand / kWave;
 constexpr int kWaveMaxK = kRowThreads;            // the selection ranks one maximum per row thread
@@ -954,11 +910,11 @@ struct __align__(16) WaveLds {
 
 // Per token, one wave (token u = blockIdx.x * kWaveTokens + wave; no block
 // barriers after the exp table): the averaged row's log-sum-exp from its
-// wave parts; T0, the k-th largest of the row threads' largest keys (a
-// radix select over the 256 keys, four per lane), which is at most the row's
-// k-th largest key, so the selected tokens are among the elements with key
-// >= T0 (on these inputs a few hundred); the lanes read again only the
-// batches whose largest key reaches T0, collect those elements in LDS, and
+// wave parts; T0, the k-th largest of the 1024 recorded vector maxima (a
+// radix select, sixteen per lane), which is at most the row's k-th largest
+// key, so the selected tokens are among the elements with key >= T0 (on
+// these inputs a little over k); the lanes read again only the vectors
+// whose maxima reach T0, collect those elements in LDS, and
 // each candidate takes its exact rank under (key descending, index
 // ascending) from one 64-bit comparison per other candidate; the selected
 // tokens in index order; then the JS terms, kJsLanes lanes per worker.  A
@@ -981,24 +937,28 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
     const double lse_a = row_lse(w.part + u * kRowWaves, tab);
 
-    // The largest keys of row threads lane + q kWave (key 0: no element).
-    using Key = typename std::conditional<E::kBf16, uint16_t, uint32_t>::type;
-    uint32_t km[kRtPerLane];
+    // The largest vector maxima of row threads lane + q kWave (entries
+    // key16 << 16 | vector index, largest first; 0: none).
+    u32x4 tq[kRtPerLane];
 #pragma unroll
-    for (int q = 0; q < kRtPerLane; ++q) km[q] = static_cast<const Key *>(w.tmax)[u * kRowThreads + lane + q * kWave];
+    for (int q = 0; q < kRtPerLane; ++q) tq[q] = w.top[u * kRowThreads + lane + q * kWave];
 
-    // T0: radix select of the k-th largest of the 256 row-thread maxima, 8
-    // bits per pass; lane l takes the bins 255 - 4l .. 252 - 4l.
+    // T0: radix select of the k-th largest 16-bit key among the 1024
+    // entries, 8 bits per pass; lane l takes the bins 255 - 4l .. 252 - 4l.
     uint32_t prefix = 0;
     int need = k;
-    for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
-        const int shift = E::kKeyBits - 8 * (pass + 1);
+    for (int pass = 0; pass < 2; ++pass) {
+        const int shift = 8 - 8 * pass;
 #pragma unroll
         for (int i = 0; i < 4; ++i) L.hist[lane + i * kWave] = 0;
         wave_sync();
 #pragma unroll
         for (int q = 0; q < kRtPerLane; ++q)
-            if (pass == 0 || (km[q] >> (shift + 8)) == prefix) atomicAdd(&L.hist[(km[q] >> shift) & 255u], 1u);
+#pragma unroll
+            for (int i = 0; i < kTopVecs; ++i) {
+                const uint32_t k16 = tq[q][i] >> 16;
+                if (pass == 0 || (k16 >> 8) == prefix) atomicAdd(&L.hist[(k16 >> shift) & 255u], 1u);
+            }
         wave_sync();
         int c[4], c4 = 0;
 #pragma unroll
@@ -1029,66 +989,65 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     }
     const uint32_t T0 = prefix;
 
-    // Candidates: the elements with key >= T0, that is with value >= the
-    // value of T0 (-0 and +0 share a key and compare equal; T0 = 0 takes
-    // every element), from the batches whose largest key reaches it; a lane
-    // walks its own set bits.
+    // The k-th largest of distinct vectors' maxima is at most the row's
+    // k-th largest key, so the selected tokens are among the candidates: the
+    // elements whose key reaches kthr (key16 T0, widened to a full key for
+    // float32; T0 = 0 takes every element).  They lie in vectors whose maxima
+    // reach T0: a row thread's recorded ones, or any of its vectors when even
+    // its fourth entry reaches T0 (it may have more).
+    const uint32_t kthr = E::kBf16 ? T0 : T0 << 16;
     if (lane == 0) L.nsel = 0;
     wave_sync();
-    const float f0 = T0 == 0 ? -INFINITY : E::value_of(T0);
-    // Batches to read again: bit q kJsBatches + b for batch b of row thread
-    // lane + q kWave; only a row thread whose largest key reaches T0 loads
-    // its batch maxima.
-    uint64_t todo = 0;
+    auto collect = [&](u32x4 t, int64_t i0) {
+        float v[P];
+        E::values(t, v);
+        const int64_t left = a.K - i0;
+        const int n = left >= P ? P : static_cast<int>(left);
 #pragma unroll
-    for (int q = 0; q < kRtPerLane; ++q) {
-        if (km[q] != 0 && km[q] >= T0) {
-            BatchKeys<E> bk;
-            const u32x4 *src = reinterpret_cast<const u32x4 *>(static_cast<const Key *>(w.bmax) +
-                                                               (u * kRowThreads + lane + q * kWave) * kJsBatches);
-#pragma unroll
-            for (int v = 0; v < BatchKeys<E>::kVecs; ++v) {
-                const u32x4 t = src[v];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) bk.r[4 * v + i] = t[i];
-            }
-#pragma unroll
-            for (int b = 0; b < kJsBatches; ++b) {
-                const uint32_t bb = bk.key(b);
-                if (bb != 0 && bb >= T0) todo |= 1ull << (q * kJsBatches + b);
-            }
-        }
-    }
-    while (todo != 0) {
-        const int bit = __builtin_ctzll(todo);
-        todo &= todo - 1;
-        const int64_t rt = lane + (bit / kJsBatches) * kWave, b = bit % kJsBatches;
-        for (int c0 = 0; c0 < w.bvec; c0 += kJsBatch) {
-            const int64_t b0 = rt * P + (b * w.bvec + c0) * kStride;
-            const int nd = w.bvec - c0 < kJsBatch ? w.bvec - c0 : kJsBatch;
-            u32x4 tb[kJsBatch];
-            load_batch<E>(ra, b0, a.K, kStride, nd, tb);
-#pragma unroll
-            for (int d = 0; d < kJsBatch; ++d) {
-                const int64_t i0 = b0 + d * kStride;
-                if (d < nd && i0 < a.K) {
-                    float v[P];
-                    E::values(tb[d], v);
-                    const int64_t left = a.K - i0;
-                    const int n = left >= P ? P : static_cast<int>(left);
-#pragma unroll
-                    for (int j = 0; j < P; ++j) {
-                        if (v[j] >= f0 && j < n) {
-                            const int slot = atomicAdd(&L.nsel, 1);
-                            if (slot < kWaveCand) {
-                                L.u.cand.comp[slot] = (static_cast<uint64_t>(E::key_of(v[j])) << 32) |
-                                                      (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
-                                L.u.cand.val[slot] = v[j];
-                            }
-                        }
-                    }
+        for (int j = 0; j < P; ++j) {
+            if (j < n && E::key_of(v[j]) >= kthr) {
+                const int slot = atomicAdd(&L.nsel, 1);
+                if (slot < kWaveCand) {
+                    L.u.cand.comp[slot] = (static_cast<uint64_t>(E::key_of(v[j])) << 32) |
+                                          (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
+                    L.u.cand.val[slot] = v[j];
                 }
             }
+        }
+    };
+#pragma unroll
+    for (int q = 0; q < kRtPerLane; ++q) {
+        const uint32_t last = tq[q][kTopVecs - 1];
+        if (last != 0 && (last >> 16) >= T0) continue;  // read below, by the whole wave
+        const int64_t rt = lane + q * kWave;
+        u32x4 t[kTopVecs];
+        int64_t at[kTopVecs];
+        bool use[kTopVecs];
+#pragma unroll
+        for (int i = 0; i < kTopVecs; ++i) {
+            const uint32_t e = tq[q][i];
+            at[i] = rt * P + static_cast<int64_t>(e & 0xFFFFu) * kStride;
+            use[i] = e != 0 && (e >> 16) >= T0 && at[i] < a.K;
+            t[i] = u32x4{0, 0, 0, 0};
+            if (use[i]) t[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>(at[i] * E::kElem), 0,
+                                                                     kLoadPolicy);
+        }
+#pragma unroll
+        for (int i = 0; i < kTopVecs; ++i)
+            if (use[i]) collect(t[i], at[i]);
+    }
+    // A row thread whose fourth entry reaches T0 may have more such vectors
+    // (rare): the whole wave reads all of its vectors, one per lane.
+#pragma unroll
+    for (int q = 0; q < kRtPerLane; ++q) {
+        const uint32_t last = tq[q][kTopVecs - 1];
+        uint64_t scan = __ballot(last != 0 && (last >> 16) >= T0);
+        while (scan != 0) {
+            const int64_t rt = __builtin_ctzll(scan) + q * kWave;
+            scan &= scan - 1;
+            for (int64_t i0 = rt * P + lane * kStride; i0 < a.K; i0 += kWave * kStride)
+                collect(__builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy),
+                        i0);
         }
     }
     wave_sync();
@@ -1214,12 +1173,12 @@ namespace {
 int64_t js_part_bytes(int32_t M, int64_t U) {
     return (static_cast<int64_t>(M) + 1) * U * kRowWaves * static_cast<int64_t>(sizeof(LsePart));
 }
-int64_t js_bmax_bytes(int32_t bf16, int64_t U) { return U * kRowThreads * kJsBatches * (bf16 ? 2 : 4); }
-int64_t js_tmax_bytes(int32_t bf16, int64_t U) { return U * kRowThreads * (bf16 ? 2 : 4); }
+int64_t js_top_bytes(int64_t U) { return U * kRowThreads * static_cast<int64_t>(sizeof(u32x4)); }
 }  // namespace
 
 int64_t js_workspace_bytes(int32_t bf16, int32_t M, int64_t U) {
-    return js_part_bytes(M, U) + js_bmax_bytes(bf16, U) + js_tmax_bytes(bf16, U) + (U * 4 + 15) / 16 * 16;
+    (void)bf16;
+    return js_part_bytes(M, U) + js_top_bytes(U) + (U * 4 + 15) / 16 * 16;
 }
 
 bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K, int64_t ldk,
@@ -1227,15 +1186,16 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
                hipStream_t stream) {
     JsParams p{avg, workers, d_out, topk_out, U, K, ldk, M, k};
     char *ws = static_cast<char *>(workspace);
-    const int64_t o_bmax = js_part_bytes(M, U), o_tmax = o_bmax + js_bmax_bytes(bf16, U);
-    const int64_t o_flag = o_tmax + js_tmax_bytes(bf16, U);
-    JsWork w{reinterpret_cast<LsePart *>(ws), ws + o_bmax, ws + o_tmax, reinterpret_cast<int32_t *>(ws + o_flag),
-             js_batch_vectors(K, bf16 ? JsBF16::kPer : JsF32::kPer)};
+    const int64_t o_top = js_part_bytes(M, U), o_flag = o_top + js_top_bytes(U);
+    JsWork w{reinterpret_cast<LsePart *>(ws), reinterpret_cast<u32x4 *>(ws + o_top),
+             reinterpret_cast<int32_t *>(ws + o_flag)};
     const int64_t groups = ((static_cast<int64_t>(M) + 1) * U + kRowsPerBlock - 1) / kRowsPerBlock;
     const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kRowsBlocksPerCu) * std::max(num_cus, 1));
     const dim3 tokens(static_cast<unsigned>(U));
     const dim3 token_waves(static_cast<unsigned>((U + kWaveTokens - 1) / kWaveTokens));
-    const bool wave_path = k <= kWaveMaxK;
+    // The wave kernel names a row thread's vectors by 16-bit indices.
+    const bool wave_path =
+        k <= kWaveMaxK && js_thread_vectors(K, bf16 ? JsBF16::kPer : JsF32::kPer) <= kTopIndexLimit;
     if (bf16) {
         hipLaunchKernelGGL(js_rows_kernel<JsBF16>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
         if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsBF16>, token_waves, dim3(kBlock), 0, stream, p, w);
@@ -1258,7 +1218,7 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
 bool js_pattern_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, int64_t U, int64_t K,
                        int64_t ldk, void *workspace, int num_cus, hipStream_t stream) {
     JsParams p{avg, workers, nullptr, nullptr, U, K, ldk, M, 1};
-    JsWork w{static_cast<LsePart *>(workspace), nullptr, nullptr, nullptr, 1};
+    JsWork w{static_cast<LsePart *>(workspace), nullptr, nullptr};
     const int64_t groups = ((static_cast<int64_t>(M) + 1) * U + kRowsPerBlock - 1) / kRowsPerBlock;
     const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kRowsBlocksPerCu) * std::max(num_cus, 1));
     if (bf16)

@@ -293,11 +293,11 @@ def test_js_bf16_rows_beyond_the_persistent_grid(env):
 
 
 @pytest.mark.parametrize("dtype,K", [("f32", 140_003), ("bf16", 270_001)])
-def test_js_batches_longer_than_one_load(env, dtype, K):
-    """Vocabularies long enough that a thread's batch of the averaged row
-    holds more than the 4 vectors the candidate pass loads at once (9 here),
-    so a batch is read again in several loads; a head of large logits placed
-    at the row's end lands in the last batches."""
+def test_js_long_vocabularies(env, dtype, K):
+    """Vocabularies of 140003 and 270001 logits: a row thread of the
+    averaged row streams 137 (float32) or 132 (bf16) vectors and records
+    four of them; a head of large logits placed at the row's end lies in
+    its last vectors."""
     fgd, torch = env
     M, U, k = 2, 3, 100
     A, W = slog.numpy_logits(M, U, K, -(-K // 8) * 8, "f32", seed=K)  # 16-byte rows in both storages
@@ -305,6 +305,32 @@ def test_js_batches_longer_than_one_load(env, dtype, K):
     tail = rng.choice(np.arange(K - 20_000, K), 150, replace=False)
     A[:, tail] += 12.0
     W[:, :, tail] += 12.0
+    if dtype == "bf16":
+        import torch as _t
+
+        A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+        W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_top_tokens_crowded_in_one_row_thread(env, dtype):
+    """Most of a token's top logits in the vectors of one row thread (every
+    one of its first 24 vectors holds one): its four recorded vector maxima
+    all reach the threshold, so the candidate pass reads all of that
+    thread's vectors; a second token crowds them into two threads' vectors,
+    a third into one vector."""
+    fgd, torch = env
+    M, U, K, k = 2, 3, 60_000, 100
+    A, W = slog.numpy_logits(M, U, K, K, "f32", seed=99)
+    per = 8 if dtype == "bf16" else 4
+    stride = 256 * per                                   # elements between a row thread's vectors
+    pos0 = np.array([5 * per + v * stride + (v % per) for v in range(24)])
+    pos1 = np.concatenate([pos0, pos0 + 37 * per])
+    A[0, pos0] += 15.0
+    A[1, pos1] += 15.0
+    A[2, 7 * per: 8 * per] += 15.0
+    W[:, 0, pos0] += 15.0
     if dtype == "bf16":
         import torch as _t
 
