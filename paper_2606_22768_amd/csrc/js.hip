@@ -524,10 +524,7 @@ __device__ inline LsePart wave_lse(double m, double s, const double *tab) {
 
 // A row's log-sum-exp from its wave parts, in wave order (-inf for a row of
 // -inf logits).
-__device__ inline double row_lse(const LsePart *p, const double *tab) {
-    LsePart q[kRowWaves];
-#pragma unroll
-    for (int j = 0; j < kRowWaves; ++j) q[j] = p[j];
+__device__ inline double lse_of_parts(const LsePart (&q)[kRowWaves], const double *tab) {
     double M = q[0].m;
 #pragma unroll
     for (int j = 1; j < kRowWaves; ++j) M = fmax(M, q[j].m);
@@ -537,46 +534,128 @@ __device__ inline double row_lse(const LsePart *p, const double *tab) {
         if (q[j].s != 0.0) S += q[j].s * exp_table(q[j].m - M, tab);
     return S == 0.0 ? -INFINITY : M + log(S);
 }
+__device__ inline double row_lse(const LsePart *p, const double *tab) {
+    LsePart q[kRowWaves];
+#pragma unroll
+    for (int j = 0; j < kRowWaves; ++j) q[j] = p[j];
+    return lse_of_parts(q, tab);
+}
 
-// One row's log-sum-exp terms for the thread's elements i_first, i_first +
-// kStride, ... into st.  `nxt` holds the row's first vector on entry and,
-// when has_next, the first vector of row rn on return, so that the next
-// row's load overlaps this row's end.  With kAvg it also keeps the thread's
-// kTopVecs largest vector maxima (top, empty on entry; indices past 16 bits
-// wrap, and the per-token wave kernel is then not used).
-template <class E, bool kAvg>
-__device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_first, int64_t K, u32x4 &nxt,
-                                 RowLse &st, const double *etab, const double *tab, TopVecs<E> &top) {
-    constexpr int P = E::kPer;
-    constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * P;
-    uint32_t v = 0;
-    for (int64_t i0 = i_first; i0 < K; i0 += kStride, ++v) {
-        const u32x4 cur = nxt;
-        if (i0 + kStride < K)
-            nxt = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<uint32_t>((i0 + kStride) * E::kElem), 0,
-                                                        kLoadPolicy);
-        else if (has_next)
-            nxt = __builtin_amdgcn_raw_buffer_load_b128(rn, static_cast<uint32_t>(i_first * E::kElem), 0, kLoadPolicy);
-        float x[P];
-        if constexpr (kAvg || !E::kBf16) vec_values<E>(cur, i0, K, x);  // past K: -inf
-        if constexpr (kAvg) top.insert((TopVecs<E>::key16(E::key_of(vec_max<P>(x))) << 16) | (v & 0xFFFFu));
-        if constexpr (E::kBf16)
-            bf16_lse_add(st, cur, i0, K, etab, tab);
-        else
-            lse_add<P>(st.m, st.thr, st.s1, x, tab);
+// Packed 16-bit lanes: two bf16 logits of a 32-bit word at once.
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u16x2 as_u16x2(uint32_t x) {
+    u16x2 r;
+    __builtin_memcpy(&r, &x, sizeof(r));
+    return r;
+}
+
+// bf16_lse_add for a whole vector inside the row (elements i0 .. i0 + 7 all
+// below K): the table indices 2 (magnitude - kBfTabLo) + sign of both
+// halves of a word at once.  Same terms, order and path choice.
+__device__ inline void bf16_lse_add_whole(RowLse &st, u32x4 t, const double *etab, const double *tab) {
+    constexpr int P = JsBF16::kPer;
+    u16x2 d[4];
+    u16x2 mx = {0, 0};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const u16x2 h = as_u16x2(t[j]);
+        d[j] = ((h << 1) | (h >> 15)) - static_cast<u16x2>(static_cast<uint16_t>(2 * kBfTabLo));
+        mx = __builtin_elementwise_max(mx, d[j]);
     }
+    const uint32_t m = mx.x > mx.y ? mx.x : mx.y;
+    if (__all(m < static_cast<uint32_t>(kBfTabEntries))) {
+        double e[P];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            e[2 * j] = etab[d[j].x];
+            e[2 * j + 1] = etab[d[j].y];
+        }
+#pragma unroll
+        for (int w = 1; w < P; w *= 2)
+#pragma unroll
+            for (int j = 0; j + w < P; j += 2 * w) e[j] += e[j + w];
+        st.s0 += e[0];
+    } else {
+        float v[P];
+        JsBF16::values(t, v);
+        const float vm = vec_max<P>(v);
+        if (vm > st.thr) {
+            const double dm = vm;
+            st.s1 *= exp_table(st.m - dm, tab);
+            st.m = dm;
+            st.thr = static_cast<float>(dm + kLseSlack);
+        }
+#pragma unroll 1
+        for (int j = 0; j < P; ++j) st.s1 += exp_table(static_cast<double>(v[j]) - st.m, tab);
+    }
+}
+
+// One vector's terms: whole (every element below K) or the row's last,
+// which may be partial.  With kAvg it also updates the thread's largest
+// vector maxima (v: the vector's sweep).
+template <class E, bool kAvg, bool kWhole>
+__device__ __forceinline__ void vec_terms(u32x4 cur, int64_t i0, int64_t K, uint32_t v, RowLse &st,
+                                          const double *etab, const double *tab, TopVecs<E> &top) {
+    constexpr int P = E::kPer;
+    if constexpr (kAvg || !E::kBf16) {
+        float x[P];
+        if constexpr (kWhole)
+            E::values(cur, x);
+        else
+            vec_values<E>(cur, i0, K, x);  // past K: -inf
+        if constexpr (kAvg) top.insert((TopVecs<E>::key16(E::key_of(vec_max<P>(x))) << 16) | (v & 0xFFFFu));
+        if constexpr (!E::kBf16) lse_add<P>(st.m, st.thr, st.s1, x, tab);
+    }
+    if constexpr (E::kBf16) {
+        if constexpr (kWhole)
+            bf16_lse_add_whole(st, cur, etab, tab);
+        else
+            bf16_lse_add(st, cur, i0, K, etab, tab);
+    }
+}
+
+// One row's log-sum-exp terms for the thread's elements i_first + s kStride
+// (sweeps s = 0 .. nsw - 1) into st.  `nxt` holds the row's first vector on
+// entry and, when has_next, the first vector of row rn on return, so that
+// the next row's load overlaps this row's end.  Sweeps before the last are
+// whole for every lane: their loads take the sweep's offset as a scalar.
+// With kAvg it also keeps the thread's kTopVecs largest vector maxima (top,
+// empty on entry; indices past 16 bits wrap, and the per-token wave kernel
+// is then not used).
+template <class E, bool kAvg>
+__device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_first, int64_t K, int nsw,
+                                 u32x4 &nxt, RowLse &st, const double *etab, const double *tab, TopVecs<E> &top) {
+    constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * E::kPer;
+    constexpr uint32_t kSweepBytes = kRowThreads * 16;
+    const uint32_t voff = static_cast<uint32_t>(i_first * E::kElem);
+    const int64_t i_last = i_first + static_cast<int64_t>(nsw - 1) * kStride;  // the last sweep's element
+    int s = 0;
+    for (; s < nsw - 2; ++s) {
+        const u32x4 cur = nxt;
+        nxt = __builtin_amdgcn_raw_buffer_load_b128(r, voff, (s + 1) * kSweepBytes, kLoadPolicy);
+        vec_terms<E, kAvg, true>(cur, 0, K, static_cast<uint32_t>(s), st, etab, tab, top);
+    }
+    if (nsw >= 2) {  // s = nsw - 2: the next load is the last sweep's, which a lane may lack
+        const u32x4 cur = nxt;
+        if (i_last < K) nxt = __builtin_amdgcn_raw_buffer_load_b128(r, voff, (nsw - 1) * kSweepBytes, kLoadPolicy);
+        vec_terms<E, kAvg, true>(cur, 0, K, static_cast<uint32_t>(nsw - 2), st, etab, tab, top);
+    }
+    const u32x4 cur = nxt;
+    if (has_next && i_first < K) nxt = __builtin_amdgcn_raw_buffer_load_b128(rn, voff, 0, kLoadPolicy);
+    if (i_last < K) vec_terms<E, kAvg, false>(cur, i_last, K, static_cast<uint32_t>(nsw - 1), st, etab, tab, top);
 }
 
 // Every row's wave parts of its log-sum-exp, and the averaged rows'
 // largest vector maxima per thread, into the workspace.  Persistent: thread group g
 // (kRowThreads threads; two per block) streams rows g, g + G, ... (G
 // groups) of the streaming order below; thread lt of a group takes the
-// elements lt * P + j * kStride of its row.  No barriers after the tables
+// elements lt * P + s * kStride of its row.  No barriers after the tables
 // are loaded: each wave streams on its own, its next row's first load
 // issued before its row ends.
 template <class E>
 __global__ __launch_bounds__(kRowsBlock) __attribute__((amdgpu_waves_per_eu(6, 8)))
 void js_rows_kernel(JsParams a, JsWork w) {
+    constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * E::kPer;
     __shared__ double etab[E::kBf16 ? kBfTabEntries : 1];
     __shared__ double tab[kTab];
     if constexpr (E::kBf16) fill_bf16_exp_table(etab);
@@ -585,6 +664,7 @@ void js_rows_kernel(JsParams a, JsWork w) {
     const int64_t i_first = static_cast<int64_t>(lt) * E::kPer;
     const int64_t G = static_cast<int64_t>(gridDim.x) * kRowsPerBlock;
     const int64_t R = static_cast<int64_t>(a.M + 1) * a.U;
+    const int nsw = static_cast<int>((a.K + kStride - 1) / kStride);  // sweeps per row
     // Streaming order: the averaged rows (token u at r = u), then the worker
     // rows (row m U + u at r = U + m U + u), the order of the workspace parts.
     auto row_of = [&](int64_t r) -> rsrc_t {
@@ -606,9 +686,9 @@ void js_rows_kernel(JsParams a, JsWork w) {
         TopVecs<E> top;
         const bool avg = r < a.U;
         if (avg)
-            row_terms<E, true>(rr, rn, has_next, i_first, a.K, nxt, st, etab, tab, top);
+            row_terms<E, true>(rr, rn, has_next, i_first, a.K, nsw, nxt, st, etab, tab, top);
         else
-            row_terms<E, false>(rr, rn, has_next, i_first, a.K, nxt, st, etab, tab, top);
+            row_terms<E, false>(rr, rn, has_next, i_first, a.K, nsw, nxt, st, etab, tab, top);
         double ml, sl;
         row_lse_lane(st, ml, sl, tab);
         const LsePart p = wave_lse(ml, sl, tab);
@@ -874,12 +954,15 @@ __global__ __launch_bounds__(kRowsBlock) void js_rows_pattern_kernel(JsParams a,
 }
 
 // ------------------------------------------------- per token, one wave each
-constexpr int kWaveTokens = kBlock / kWave;       // tokens per block of js_token_wave_kernel
-constexpr int kRtPerLane = kRowThreads / kWave;   // row threads whose recorded maxima a lane takes
-constexpr int kWaveCand = 512;                    // candidates a token may have
+constexpr int kWaveTokens = kBlock / kWave;            // tokens per block of js_token_wave_kernel
+constexpr int kRtPerLane = kRowThreads / kWave;        // row threads whose recorded maxima a lane takes
+constexpr int kRecords = kRowThreads * kTopVecs;       // recorded vector maxima per token
+constexpr int kWaveCand = 512;                         // candidates a token may have
 constexpr int kCandPerLane = kWaveCand / kWave;
-constexpr int kWaveMaxK = kRowThreads;            // the selection ranks one maximum per row thread
-constexpr int kJsLanes = kWave / kJsGroup;        // lanes per worker in the JS terms
+constexpr int kWaveMaxK = kRowThreads;                 // the selection ranks one maximum per row thread
+constexpr int kJsLanes = kWave / kJsGroup;             // lanes per worker in the JS terms
+constexpr int kReadRound = 4;                          // recorded vectors a lane reads at once
+constexpr int kGather = 16;                            // worker logits a lane gathers at once
 
 // Orders a wave's LDS accesses: what a lane wrote before it is visible to
 // every lane of the wave after it.
@@ -889,37 +972,87 @@ __device__ inline void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Slots, in lane order, for the lanes that set `pred`: base, base + 1, ...;
+// base (wave-uniform) grows by their number.  Every lane of the wave calls it.
+__device__ inline int wave_append(bool pred, int &base) {
+    const uint64_t m = __ballot(pred);
+    const int slot = base + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                static_cast<uint32_t>(m >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)));
+    base += __popcll(m);
+    return slot;
+}
+
+__device__ inline uint64_t readlane64(uint64_t x, int l) {
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), l));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x >> 32), l));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
 // One wave's LDS in js_token_wave_kernel.
 struct __align__(16) WaveLds {
+    uint64_t comp[kWaveCand];  // candidates: key << 32 | ~index, larger = earlier in (key desc, index asc)
+    float val[kWaveCand];
     union {
-        struct {
-            uint64_t comp[kWaveCand];  // key << 32 | ~index: larger = earlier in (key desc, index asc)
-            float val[kWaveCand];
-        } cand;
+        uint32_t queue[kRecords];  // first elements of the recorded vectors to read again
         struct {
             int32_t idx[kWaveMaxK];
             double la[kWaveMaxK];
         } out;  // the selected tokens in index order, log pbar
     } u;
-    int32_t sel_idx[kWaveMaxK + 4];
-    float sel_val[kWaveMaxK];
-    uint32_t hist[256];
     double lse[kJsGroup];
-    int nsel;
 };
+
+// The ranks of the candidates a lane holds (candidate lane + q kWave in
+// mine[q]; 0 past the C candidates): the number of candidates above each,
+// from one comparison per candidate, read across lanes.  Then each selected
+// candidate's position in index order among the selected (rank < k).
+template <int N>
+__device__ inline void rank_candidates(const uint64_t (&mine)[kCandPerLane], int C, int k, int (&rk)[kCandPerLane],
+                                       int (&pos)[kCandPerLane]) {
+#pragma unroll
+    for (int q = 0; q < N; ++q) rk[q] = 0;
+#pragma unroll
+    for (int qq = 0; qq < N; ++qq) {
+        const int nj = C - qq * kWave < kWave ? C - qq * kWave : kWave;
+        for (int j = 0; j < nj; ++j) {
+            const uint64_t c = readlane64(mine[qq], j);
+#pragma unroll
+            for (int q = 0; q < N; ++q) rk[q] += c > mine[q] ? 1 : 0;
+        }
+    }
+    uint32_t my[N];
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+        my[q] = 0xFFFFFFFFu - static_cast<uint32_t>(mine[q]);
+        pos[q] = 0;
+    }
+#pragma unroll
+    for (int qq = 0; qq < N; ++qq) {
+        const int nj = C - qq * kWave < kWave ? C - qq * kWave : kWave;
+        for (int j = 0; j < nj; ++j) {
+            if (__builtin_amdgcn_readlane(rk[qq], j) >= k) continue;  // not selected (wave-uniform)
+            const uint32_t idx =
+                0xFFFFFFFFu - static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(mine[qq]), j));
+#pragma unroll
+            for (int q = 0; q < N; ++q) pos[q] += idx < my[q] ? 1 : 0;
+        }
+    }
+}
 
 // Per token, one wave (token u = blockIdx.x * kWaveTokens + wave; no block
 // barriers after the exp table): the averaged row's log-sum-exp from its
-// wave parts; T0, the k-th largest of the 1024 recorded vector maxima (a
-// radix select, sixteen per lane), which is at most the row's k-th largest
-// key, so the selected tokens are among the elements with key >= T0 (on
-// these inputs a little over k); the lanes read again only the vectors
-// whose maxima reach T0, collect those elements in LDS, and
-// each candidate takes its exact rank under (key descending, index
-// ascending) from one 64-bit comparison per other candidate; the selected
-// tokens in index order; then the JS terms, kJsLanes lanes per worker.  A
-// token with more than kWaveCand candidates (a row of many equal logits) is
-// flagged and left to js_token_radix_kernel.  k <= kWaveMaxK.
+// wave parts; T0, the k-th largest of the 1024 recorded vector maxima (16-bit
+// keys, built from the top bit down by counting with ballots), which is at
+// most the row's k-th largest key, so the selected tokens are among the
+// elements with key >= T0 (on these inputs a little over k); the vectors
+// whose maxima reach T0 go to a queue and are read again in one round, and
+// their elements at or above T0 are appended to the candidates in lane
+// order; each candidate's rank under (key descending, index ascending) and
+// its place in index order come from comparisons read across lanes; then
+// the JS terms, kJsLanes lanes per worker, with a lane's gathers issued
+// together.  A token with more than kWaveCand candidates (a row of many
+// equal logits) is flagged and left to js_token_radix_kernel.
+// k <= kWaveMaxK.
 template <class E>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4, 8)))
 void js_token_wave_kernel(JsParams a, JsWork w) {
@@ -927,67 +1060,41 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * P;  // elements per row sweep
     __shared__ double tab[kTab];
     __shared__ WaveLds lds[kWaveTokens];
-    load_exp_table(tab);
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t u = static_cast<int64_t>(blockIdx.x) * kWaveTokens + wave;
-    if (u >= a.U) return;  // the whole wave
+    const bool live = u < a.U;  // the whole wave
+
+    // The largest vector maxima of row threads lane + q kWave (entries
+    // key16 << 16 | vector index, largest first; 0: none) and the averaged
+    // row's wave parts, loaded while the exp table is.
+    u32x4 tq[kRtPerLane];
+    LsePart pa[kRowWaves];
+    if (live) {
+#pragma unroll
+        for (int q = 0; q < kRtPerLane; ++q) tq[q] = w.top[u * kRowThreads + lane + q * kWave];
+#pragma unroll
+        for (int j = 0; j < kRowWaves; ++j) pa[j] = w.part[u * kRowWaves + j];
+    }
+    load_exp_table(tab);
+    if (!live) return;
     WaveLds &L = lds[wave];
     const int k = a.k;
     const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
-    const double lse_a = row_lse(w.part + u * kRowWaves, tab);
+    const double lse_a = lse_of_parts(pa, tab);
 
-    // The largest vector maxima of row threads lane + q kWave (entries
-    // key16 << 16 | vector index, largest first; 0: none).
-    u32x4 tq[kRtPerLane];
-#pragma unroll
-    for (int q = 0; q < kRtPerLane; ++q) tq[q] = w.top[u * kRowThreads + lane + q * kWave];
-
-    // T0: radix select of the k-th largest 16-bit key among the 1024
-    // entries, 8 bits per pass; lane l takes the bins 255 - 4l .. 252 - 4l.
-    uint32_t prefix = 0;
-    int need = k;
-    for (int pass = 0; pass < 2; ++pass) {
-        const int shift = 8 - 8 * pass;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) L.hist[lane + i * kWave] = 0;
-        wave_sync();
+    // T0: the largest t with at least k entries whose key reaches it (an
+    // empty entry counts as key 0), one bit at a time from the top.
+    uint32_t T0 = 0;
+    for (int b = 15; b >= 0; --b) {
+        const uint32_t t = T0 | (1u << b);
+        int cnt = 0;
 #pragma unroll
         for (int q = 0; q < kRtPerLane; ++q)
 #pragma unroll
-            for (int i = 0; i < kTopVecs; ++i) {
-                const uint32_t k16 = tq[q][i] >> 16;
-                if (pass == 0 || (k16 >> 8) == prefix) atomicAdd(&L.hist[(k16 >> shift) & 255u], 1u);
-            }
-        wave_sync();
-        int c[4], c4 = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            c[i] = static_cast<int>(L.hist[255 - 4 * lane - i]);
-            c4 += c[i];
-        }
-        int incl = c4;
-        for (int o = 1; o < kWave; o <<= 1) {
-            const int t = __shfl_up(incl, o);
-            if (lane >= o) incl += t;
-        }
-        int bin = -1, nin = 0, run = incl - c4;
-        if (run < need && need <= incl) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if (bin < 0 && run + c[i] >= need) {
-                    bin = 255 - 4 * lane - i;
-                    nin = need - run;
-                }
-                run += c[i];
-            }
-        }
-        const int src = __ffsll(static_cast<unsigned long long>(__ballot(bin >= 0))) - 1;
-        prefix = (prefix << 8) | static_cast<uint32_t>(__shfl(bin, src));
-        need = __shfl(nin, src);
-        wave_sync();  // every lane has read the histogram before the next pass clears it
+            for (int i = 0; i < kTopVecs; ++i) cnt += __popcll(__ballot((tq[q][i] >> 16) >= t));
+        if (cnt >= k) T0 = t;
     }
-    const uint32_t T0 = prefix;
 
     // The k-th largest of distinct vectors' maxima is at most the row's
     // k-th largest key, so the selected tokens are among the candidates: the
@@ -996,45 +1103,55 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     // reach T0: a row thread's recorded ones, or any of its vectors when even
     // its fourth entry reaches T0 (it may have more).
     const uint32_t kthr = E::kBf16 ? T0 : T0 << 16;
-    if (lane == 0) L.nsel = 0;
-    wave_sync();
-    auto collect = [&](u32x4 t, int64_t i0) {
+    int nsel = 0;  // candidates appended so far (wave-uniform)
+    auto collect = [&](bool have, u32x4 t, int64_t i0) {
         float v[P];
         E::values(t, v);
-        const int64_t left = a.K - i0;
-        const int n = left >= P ? P : static_cast<int>(left);
 #pragma unroll
         for (int j = 0; j < P; ++j) {
-            if (j < n && E::key_of(v[j]) >= kthr) {
-                const int slot = atomicAdd(&L.nsel, 1);
-                if (slot < kWaveCand) {
-                    L.u.cand.comp[slot] = (static_cast<uint64_t>(E::key_of(v[j])) << 32) |
-                                          (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
-                    L.u.cand.val[slot] = v[j];
-                }
+            const uint32_t key = E::key_of(v[j]);
+            const bool c = have && i0 + j < a.K && key >= kthr;
+            const int slot = wave_append(c, nsel);
+            if (c && slot < kWaveCand) {
+                L.comp[slot] = (static_cast<uint64_t>(key) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
+                L.val[slot] = v[j];
             }
         }
     };
+    int nq = 0;
 #pragma unroll
     for (int q = 0; q < kRtPerLane; ++q) {
         const uint32_t last = tq[q][kTopVecs - 1];
-        if (last != 0 && (last >> 16) >= T0) continue;  // read below, by the whole wave
+        const bool crowded = last != 0 && (last >> 16) >= T0;  // read below, by the whole wave
         const int64_t rt = lane + q * kWave;
-        u32x4 t[kTopVecs];
-        int64_t at[kTopVecs];
-        bool use[kTopVecs];
 #pragma unroll
         for (int i = 0; i < kTopVecs; ++i) {
             const uint32_t e = tq[q][i];
-            at[i] = rt * P + static_cast<int64_t>(e & 0xFFFFu) * kStride;
-            use[i] = e != 0 && (e >> 16) >= T0 && at[i] < a.K;
-            t[i] = u32x4{0, 0, 0, 0};
-            if (use[i]) t[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>(at[i] * E::kElem), 0,
-                                                                     kLoadPolicy);
+            const int64_t at = rt * P + static_cast<int64_t>(e & 0xFFFFu) * kStride;
+            const bool use = !crowded && e != 0 && (e >> 16) >= T0 && at < a.K;
+            const int slot = wave_append(use, nq);
+            if (use) L.u.queue[slot] = static_cast<uint32_t>(at);
+        }
+    }
+    nq = __builtin_amdgcn_readfirstlane(nq);
+    wave_sync();
+    for (int s0 = 0; s0 < nq; s0 += kReadRound * kWave) {
+        u32x4 t[kReadRound];
+        int64_t at[kReadRound];
+        bool have[kReadRound];
+#pragma unroll
+        for (int j = 0; j < kReadRound; ++j) {
+            const int s = s0 + j * kWave + lane;
+            have[j] = s < nq;
+            at[j] = have[j] ? static_cast<int64_t>(L.u.queue[s]) : 0;
+            t[j] = u32x4{0, 0, 0, 0};
+            if (have[j])
+                t[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>(at[j] * E::kElem), 0,
+                                                             kLoadPolicy);
         }
 #pragma unroll
-        for (int i = 0; i < kTopVecs; ++i)
-            if (use[i]) collect(t[i], at[i]);
+        for (int j = 0; j < kReadRound; ++j)
+            if (s0 + j * kWave < nq) collect(have[j], t[j], at[j]);
     }
     // A row thread whose fourth entry reaches T0 may have more such vectors
     // (rare): the whole wave reads all of its vectors, one per lane.
@@ -1045,73 +1162,53 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
         while (scan != 0) {
             const int64_t rt = __builtin_ctzll(scan) + q * kWave;
             scan &= scan - 1;
-            for (int64_t i0 = rt * P + lane * kStride; i0 < a.K; i0 += kWave * kStride)
-                collect(__builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>(i0 * E::kElem), 0, kLoadPolicy),
-                        i0);
+            for (int64_t b0 = rt * P; b0 < a.K; b0 += kWave * kStride) {
+                const int64_t i0 = b0 + lane * kStride;
+                const bool have = i0 < a.K;
+                u32x4 t = u32x4{0, 0, 0, 0};
+                if (have) t = __builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>(i0 * E::kElem), 0,
+                                                                    kLoadPolicy);
+                collect(have, t, i0);
+            }
         }
     }
-    wave_sync();
-    const int C = L.nsel;
+    const int C = __builtin_amdgcn_readfirstlane(nsel);
     if (C > kWaveCand) {  // the same in every lane
         if (lane == 0) w.flag[u] = 1;
         return;
     }
-    if (lane == 0 && (C & 1)) L.u.cand.comp[C] = 0;  // pad to even: below every candidate
     wave_sync();
 
-    // Each candidate's rank; the first k are selected.
+    // Each candidate's rank (the first k are selected) and its place in
+    // index order among the selected.
     const int nc = (C + kWave - 1) / kWave;
     uint64_t mine[kCandPerLane];
-    int rk[kCandPerLane];
+    float mval[kCandPerLane];
 #pragma unroll
     for (int q = 0; q < kCandPerLane; ++q) {
         const int c = lane + q * kWave;
-        mine[q] = c < C ? L.u.cand.comp[c] : 0;
-        rk[q] = 0;
-    }
-    for (int j = 0; j < C; j += 2) {
-        const u32x4 o = *reinterpret_cast<const u32x4 *>(&L.u.cand.comp[j]);
-        const uint64_t c0 = (static_cast<uint64_t>(o[1]) << 32) | o[0];
-        const uint64_t c1 = (static_cast<uint64_t>(o[3]) << 32) | o[2];
-#pragma unroll
-        for (int q = 0; q < kCandPerLane; ++q)
-            if (q < nc) rk[q] += (c0 > mine[q] ? 1 : 0) + (c1 > mine[q] ? 1 : 0);
-    }
-#pragma unroll
-    for (int q = 0; q < kCandPerLane; ++q) {
-        const int c = lane + q * kWave;
-        if (c < C && rk[q] < k) {
-            L.sel_idx[rk[q]] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(mine[q]));
-            L.sel_val[rk[q]] = L.u.cand.val[c];
+        mine[q] = 0;
+        mval[q] = 0.0f;
+        if (q < nc && c < C) {
+            mine[q] = L.comp[c];
+            mval[q] = L.val[c];
         }
     }
-    if (lane < 4 && k + lane < ((k + 3) & ~3)) L.sel_idx[k + lane] = INT32_MAX;  // above every token
-    wave_sync();
-
-    // The selected tokens in index order (indices are distinct), with the
-    // averaged model's log-probabilities; the candidates are no longer read.
-    constexpr int kSelPerLane = kWaveMaxK / kWave;
-    int32_t my[kSelPerLane];
-    int pos[kSelPerLane];
+    int rk[kCandPerLane], pos[kCandPerLane];
+    if (nc <= 2)
+        rank_candidates<2>(mine, C, k, rk, pos);
+    else if (nc <= 4)
+        rank_candidates<4>(mine, C, k, rk, pos);
+    else
+        rank_candidates<kCandPerLane>(mine, C, k, rk, pos);
+    // The queue is no longer read: its space takes the selected tokens in
+    // index order, with the averaged model's log-probabilities.
 #pragma unroll
-    for (int q = 0; q < kSelPerLane; ++q) {
-        const int t = lane + q * kWave;
-        my[q] = t < k ? L.sel_idx[t] : INT32_MAX;
-        pos[q] = 0;
-    }
-    for (int j = 0; j < k; j += 4) {
-        const u32x4 o = *reinterpret_cast<const u32x4 *>(&L.sel_idx[j]);
-#pragma unroll
-        for (int q = 0; q < kSelPerLane; ++q)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) pos[q] += static_cast<int32_t>(o[i]) < my[q] ? 1 : 0;
-    }
-#pragma unroll
-    for (int q = 0; q < kSelPerLane; ++q) {
-        const int t = lane + q * kWave;
-        if (t < k) {
-            L.u.out.idx[pos[q]] = my[q];
-            L.u.out.la[pos[q]] = static_cast<double>(L.sel_val[t]) - lse_a;
+    for (int q = 0; q < kCandPerLane; ++q) {
+        const int c = lane + q * kWave;
+        if (q < nc && c < C && rk[q] < k) {
+            L.u.out.idx[pos[q]] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(mine[q]));
+            L.u.out.la[pos[q]] = static_cast<double>(mval[q]) - lse_a;
         }
     }
     wave_sync();
@@ -1120,35 +1217,36 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
 
     // JS terms, kJsGroup workers at a time: worker jw of the group takes
     // lanes [jw, jw + 1) * kJsLanes, lane l of them the selected tokens l,
-    // l + kJsLanes, ... in index order; their sum is d's.
+    // l + kJsLanes, ... in index order; their sum is d's.  The workers'
+    // log-sum-exp parts are loaded while the first gathers are in flight.
     constexpr double kLog2 = 0.69314718055994530942;
     const int jw = lane / kJsLanes, l = lane % kJsLanes;
     for (int64_t w0 = 0; w0 < a.M; w0 += kJsGroup) {
         const int nw = a.M - w0 < kJsGroup ? static_cast<int>(a.M - w0) : kJsGroup;
-        if (lane < nw) L.lse[lane] = row_lse(w.part + (a.U + (w0 + lane) * a.U + u) * kRowWaves, tab);
-        wave_sync();
+        const bool mine_w = jw < nw;
+        const int64_t row = (w0 + (mine_w ? jw : 0)) * a.U + u;
+        const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
         double acc = 0.0;
-        const int64_t row = (w0 + (jw < nw ? jw : 0)) * a.U + u;
-        if (jw < nw) {
-            const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
-            const double lse_w = L.lse[jw];
-            constexpr int kGather = 4;  // gathers a lane has in flight
-            for (int t0 = l; t0 < k; t0 += kGather * kJsLanes) {
-                float z[kGather];
+        for (int t0 = 0; t0 < k; t0 += kGather * kJsLanes) {
+            float z[kGather];
 #pragma unroll
-                for (int q = 0; q < kGather; ++q) {
-                    const int t = t0 + q * kJsLanes;
-                    z[q] = t < k ? E::at_ptr(zrow, L.u.out.idx[t]) : 0.0f;
-                }
+            for (int q = 0; q < kGather; ++q) {
+                const int t = t0 + l + q * kJsLanes;
+                z[q] = mine_w && t < k ? E::at_ptr(zrow, L.u.out.idx[t]) : 0.0f;
+            }
+            if (t0 == 0) {
+                if (lane < nw) L.lse[lane] = row_lse(w.part + (a.U + (w0 + lane) * a.U + u) * kRowWaves, tab);
+                wave_sync();
+            }
+            const double lse_w = L.lse[mine_w ? jw : 0];
 #pragma unroll
-                for (int q = 0; q < kGather; ++q) {
-                    const int t = t0 + q * kJsLanes;
-                    if (t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, L.u.out.la[t]);
-                }
+            for (int q = 0; q < kGather; ++q) {
+                const int t = t0 + l + q * kJsLanes;
+                if (mine_w && t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, L.u.out.la[t]);
             }
         }
         for (int o = kJsLanes / 2; o > 0; o >>= 1) acc += shfl_xor_d(acc, o);
-        if (l == 0 && jw < nw) a.d_out[row] = sqrt((acc > 0.0 ? acc : 0.0) / kLog2);
+        if (l == 0 && mine_w) a.d_out[row] = sqrt((acc > 0.0 ? acc : 0.0) / kLog2);
         wave_sync();  // L.lse is rewritten by the next group
     }
     if (lane == 0) w.flag[u] = 0;
