@@ -991,7 +991,6 @@ __device__ inline uint64_t readlane64(uint64_t x, int l) {
 // One wave's LDS in js_token_wave_kernel.
 struct __align__(16) WaveLds {
     uint64_t comp[kWaveCand];  // candidates: key << 32 | ~index, larger = earlier in (key desc, index asc)
-    float val[kWaveCand];
     union {
         uint32_t queue[kRecords];  // first elements of the recorded vectors to read again
         struct {
@@ -1002,39 +1001,77 @@ struct __align__(16) WaveLds {
     double lse[kJsGroup];
 };
 
-// The ranks of the candidates a lane holds (candidate lane + q kWave in
-// mine[q]; 0 past the C candidates): the number of candidates above each,
-// from one comparison per candidate, read across lanes.  Then each selected
-// candidate's position in index order among the selected (rank < k).
-template <int N>
-__device__ inline void rank_candidates(const uint64_t (&mine)[kCandPerLane], int C, int k, int (&rk)[kCandPerLane],
-                                       int (&pos)[kCandPerLane]) {
+__device__ inline uint64_t shfl_xor_u64(uint64_t x, int mask) {
+    const uint32_t lo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(static_cast<uint32_t>(x)), mask));
+    const uint32_t hi = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x >> 32), mask));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Sorts the wave's 64 R words (word p = lane + 64 r in v[r] of lane
+// `lane`) in place, descending or ascending: Batcher's bitonic network,
+// partners in other lanes exchanged by shuffles, partners in the same lane
+// (distances of 64 and more) in registers.
+template <int R, bool kDescending>
+__device__ inline void wave_bitonic_sort(uint64_t (&v)[R], int lane) {
 #pragma unroll
-    for (int q = 0; q < N; ++q) rk[q] = 0;
+    for (int k = 2; k <= kWave * R; k <<= 1) {
 #pragma unroll
-    for (int qq = 0; qq < N; ++qq) {
-        const int nj = C - qq * kWave < kWave ? C - qq * kWave : kWave;
-        for (int j = 0; j < nj; ++j) {
-            const uint64_t c = readlane64(mine[qq], j);
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= kWave) {
+                const int jr = j / kWave;
 #pragma unroll
-            for (int q = 0; q < N; ++q) rk[q] += c > mine[q] ? 1 : 0;
+                for (int r = 0; r < R; ++r) {
+                    if (r & jr) continue;
+                    const bool down = ((r * kWave) & k) == 0;  // this pair's block sorts downwards
+                    const uint64_t x = v[r], y = v[r | jr];
+                    const bool big_first = down == kDescending;
+                    const uint64_t hi = x > y ? x : y, lo = x > y ? y : x;
+                    v[r] = big_first ? hi : lo;
+                    v[r | jr] = big_first ? lo : hi;
+                }
+            } else {
+                const bool lower = (lane & j) == 0;
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const uint64_t o = shfl_xor_u64(v[r], j);
+                    const bool down = ((lane + r * kWave) & k) == 0;
+                    const bool take_big = (lower == (down == kDescending));
+                    v[r] = take_big ? (v[r] > o ? v[r] : o) : (v[r] > o ? o : v[r]);
+                }
+            }
         }
     }
-    uint32_t my[N];
+}
+
+// The selection from C candidates (candidate c in slot c of L.comp, as
+// key << 32 | ~index; 64 R slots at least): the candidates sorted
+// descending, the first k selected, those sorted by index; into L.u.out
+// the selected tokens in index order with log pbar = value - lse_a (the
+// value recovered from the key).
+template <class E, int R>
+__device__ inline void select_sorted(const uint64_t *comp, int C, int k, int lane, double lse_a, int32_t *out_idx,
+                                     double *out_la) {
+    uint64_t v[R];
 #pragma unroll
-    for (int q = 0; q < N; ++q) {
-        my[q] = 0xFFFFFFFFu - static_cast<uint32_t>(mine[q]);
-        pos[q] = 0;
+    for (int r = 0; r < R; ++r) {
+        const int c = lane + r * kWave;
+        v[r] = c < C ? comp[c] : 0;  // 0: below every candidate
     }
+    wave_bitonic_sort<R, true>(v, lane);
 #pragma unroll
-    for (int qq = 0; qq < N; ++qq) {
-        const int nj = C - qq * kWave < kWave ? C - qq * kWave : kWave;
-        for (int j = 0; j < nj; ++j) {
-            if (__builtin_amdgcn_readlane(rk[qq], j) >= k) continue;  // not selected (wave-uniform)
-            const uint32_t idx =
-                0xFFFFFFFFu - static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(mine[qq]), j));
+    for (int r = 0; r < R; ++r) {
+        const int p = lane + r * kWave;
+        // index << 32 | key for the selected, above every index otherwise
+        v[r] = p < k ? (static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(v[r])) << 32) | (v[r] >> 32)
+                     : ~0ull;
+    }
+    wave_bitonic_sort<R, false>(v, lane);
 #pragma unroll
-            for (int q = 0; q < N; ++q) pos[q] += idx < my[q] ? 1 : 0;
+    for (int r = 0; r < R; ++r) {
+        const int p = lane + r * kWave;
+        if (p < k) {
+            out_idx[p] = static_cast<int32_t>(v[r] >> 32);
+            out_la[p] = static_cast<double>(E::value_of(static_cast<uint32_t>(v[r]))) - lse_a;
         }
     }
 }
@@ -1047,9 +1084,9 @@ __device__ inline void rank_candidates(const uint64_t (&mine)[kCandPerLane], int
 // elements with key >= T0 (on these inputs a little over k); the vectors
 // whose maxima reach T0 go to a queue and are read again in one round, and
 // their elements at or above T0 are appended to the candidates in lane
-// order; each candidate's rank under (key descending, index ascending) and
-// its place in index order come from comparisons read across lanes; then
-// the JS terms, kJsLanes lanes per worker, with a lane's gathers issued
+// order; the candidates are sorted under (key descending, index
+// ascending) by a bitonic network across the wave, the first k then by
+// index; then the JS terms, kJsLanes lanes per worker, with a lane's gathers issued
 // together.  A token with more than kWaveCand candidates (a row of many
 // equal logits) is flagged and left to js_token_radix_kernel.
 // k <= kWaveMaxK.
@@ -1112,10 +1149,8 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
             const uint32_t key = E::key_of(v[j]);
             const bool c = have && i0 + j < a.K && key >= kthr;
             const int slot = wave_append(c, nsel);
-            if (c && slot < kWaveCand) {
+            if (c && slot < kWaveCand)
                 L.comp[slot] = (static_cast<uint64_t>(key) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
-                L.val[slot] = v[j];
-            }
         }
     };
     int nq = 0;
@@ -1179,38 +1214,13 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     }
     wave_sync();
 
-    // Each candidate's rank (the first k are selected) and its place in
-    // index order among the selected.
-    const int nc = (C + kWave - 1) / kWave;
-    uint64_t mine[kCandPerLane];
-    float mval[kCandPerLane];
-#pragma unroll
-    for (int q = 0; q < kCandPerLane; ++q) {
-        const int c = lane + q * kWave;
-        mine[q] = 0;
-        mval[q] = 0.0f;
-        if (q < nc && c < C) {
-            mine[q] = L.comp[c];
-            mval[q] = L.val[c];
-        }
-    }
-    int rk[kCandPerLane], pos[kCandPerLane];
-    if (nc <= 2)
-        rank_candidates<2>(mine, C, k, rk, pos);
-    else if (nc <= 4)
-        rank_candidates<4>(mine, C, k, rk, pos);
+    // The selection, by sorting: the queue is no longer read, and its space
+    // takes the selected tokens in index order, with the averaged model's
+    // log-probabilities.
+    if (C <= 2 * kWave)
+        select_sorted<E, 2>(L.comp, C, k, lane, lse_a, L.u.out.idx, L.u.out.la);
     else
-        rank_candidates<kCandPerLane>(mine, C, k, rk, pos);
-    // The queue is no longer read: its space takes the selected tokens in
-    // index order, with the averaged model's log-probabilities.
-#pragma unroll
-    for (int q = 0; q < kCandPerLane; ++q) {
-        const int c = lane + q * kWave;
-        if (q < nc && c < C && rk[q] < k) {
-            L.u.out.idx[pos[q]] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(mine[q]));
-            L.u.out.la[pos[q]] = static_cast<double>(mval[q]) - lse_a;
-        }
-    }
+        select_sorted<E, kCandPerLane>(L.comp, C, k, lane, lse_a, L.u.out.idx, L.u.out.la);
     wave_sync();
     if (a.topk_out)
         for (int t = lane; t < k; t += kWave) a.topk_out[u * k + t] = L.u.out.idx[t];
@@ -1289,11 +1299,13 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
              reinterpret_cast<int32_t *>(ws + o_flag)};
     const int64_t groups = ((static_cast<int64_t>(M) + 1) * U + kRowsPerBlock - 1) / kRowsPerBlock;
     const int64_t grid = std::min<int64_t>(groups, static_cast<int64_t>(kRowsBlocksPerCu) * std::max(num_cus, 1));
-    const dim3 tokens(static_cast<unsigned>(U));
     const dim3 token_waves(static_cast<unsigned>((U + kWaveTokens - 1) / kWaveTokens));
     // The wave kernel names a row thread's vectors by 16-bit indices.
     const bool wave_path =
         k <= kWaveMaxK && js_thread_vectors(K, bf16 ? JsBF16::kPer : JsF32::kPer) <= kTopIndexLimit;
+    // The radix kernel takes every token, or after the wave kernel only the
+    // flagged ones (few): then a few blocks per CU walk the flags.
+    const dim3 tokens(static_cast<unsigned>(wave_path ? std::min<int64_t>(U, 4 * std::max(num_cus, 1)) : U));
     if (bf16) {
         hipLaunchKernelGGL(js_rows_kernel<JsBF16>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
         if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsBF16>, token_waves, dim3(kBlock), 0, stream, p, w);
