@@ -362,6 +362,30 @@ def test_js_row_padding_is_never_used(env, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_hundreds_of_candidates(env, dtype):
+    """Averaged rows with a wide tie at the k-th value: 60 tokens above it
+    and t tokens on it (t = 90 .. 450, scattered), the rest below.  The
+    threshold from the recorded vector maxima is the tied value, so the
+    per-token selection sorts 60 + t candidates (past two per lane for most
+    tokens, up to its limit of 512) and must split the tie by index."""
+    fgd, torch = env
+    M, U, K, k = 2, 6, 40_000, 100
+    A, W = slog.numpy_logits(M, U, K, K, "f32", seed=83)
+    rng = np.random.default_rng(84)
+    A = np.clip(A, -6.0, 1.5).astype(np.float32)
+    for u, t in enumerate((90, 150, 250, 330, 400, 450)):
+        pos = rng.choice(K, size=60 + t, replace=False)
+        A[u, pos[:60]] = 5.0 + rng.integers(0, 4, size=60).astype(np.float32)
+        A[u, pos[60:]] = 3.0
+    if dtype == "bf16":
+        import torch as _t
+
+        A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+        W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_js_candidate_overflow_mixed_with_ordinary_tokens(env, dtype):
     """Tokens whose averaged row is one repeated logit give every element as
     a candidate of the per-token wave selection (more than it holds); those
