@@ -752,163 +752,180 @@ void js_token_radix_kernel(JsParams a, JsWork w, const int32_t *flag) {
 
     const int tid = threadIdx.x;
     const int k = a.k;
+    __shared__ int64_t s_tok[kBlock];
+    __shared__ int s_ntok;
     bool have_tab = false;
-    for (int64_t u = blockIdx.x; u < a.U; u += gridDim.x) {
-        if (flag && flag[u] == 0) continue;  // the same in every thread
-        if (!have_tab) {  // the blocks of unflagged tokens leave without it
-            load_exp_table(tab);
-            have_tab = true;
+    // The block's tokens u = blockIdx.x + j gridDim.x, kBlock values of j at
+    // a time: all of them, or (flag != nullptr) those flagged, their flags
+    // read by the block's threads at once.
+    const int64_t n_mine = (a.U - blockIdx.x + gridDim.x - 1) / gridDim.x;
+    for (int64_t j0 = 0; j0 < n_mine; j0 += kBlock) {
+        int ntok = static_cast<int>(n_mine - j0 < kBlock ? n_mine - j0 : kBlock);
+        if (flag) {
+            if (tid == 0) s_ntok = 0;
+            __syncthreads();
+            const int64_t uu = blockIdx.x + (j0 + tid) * gridDim.x;
+            if (tid < ntok && flag[uu] != 0) s_tok[atomicAdd(&s_ntok, 1)] = uu;
+            __syncthreads();
+            ntok = s_ntok;
         }
-        const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
-        const double lse_a = row_lse(w.part + u * kRowWaves, tab);
-        {
-            // Radix select of the k-th largest key, 8 bits per pass from the top.
-            uint32_t prefix = 0;
-            int need = k, count_eq = 0;
-            for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
-                const int shift = E::kKeyBits - 8 * (pass + 1);
-                hist[tid] = 0;
+        for (int q = 0; q < ntok; ++q) {
+            const int64_t u = flag ? s_tok[q] : blockIdx.x + (j0 + q) * gridDim.x;
+            if (!have_tab) {  // blocks without a flagged token leave without it
+                load_exp_table(tab);
+                have_tab = true;
+            }
+            const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
+            const double lse_a = row_lse(w.part + u * kRowWaves, tab);
+            {
+                // Radix select of the k-th largest key, 8 bits per pass from the top.
+                uint32_t prefix = 0;
+                int need = k, count_eq = 0;
+                for (int pass = 0; pass < E::kKeyBits / 8; ++pass) {
+                    const int shift = E::kKeyBits - 8 * (pass + 1);
+                    hist[tid] = 0;
+                    __syncthreads();
+                    for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
+                        float v[P];
+                        uint32_t key[P];
+                        const int n = load_vec<E>(ra, i0, a.K, v, key);
+    #pragma unroll
+                        for (int j = 0; j < P; ++j)
+                            if (j < n && (pass == 0 || (key[j] >> (shift + 8)) == prefix))
+                                atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
+                    }
+                    __syncthreads();
+                    int bin, need_in;
+                    hist_pick(hist, need, s_wsum, s_pick, bin, need_in);
+                    count_eq = static_cast<int>(hist[bin]);  // read before the next pass clears it
+                    prefix = (prefix << 8) | static_cast<uint32_t>(bin);
+                    need = need_in;
+                    __syncthreads();
+                }
+                const uint32_t T = prefix;
+                const int need_eq = need;
+                const bool take_all_eq = count_eq == need_eq;
+
+                // Collect the keys above T (and those equal to T when all of them are
+                // taken); the list order does not matter, it is sorted below.
+                if (tid == 0) s_nsel = 0;
                 __syncthreads();
                 for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
                     float v[P];
                     uint32_t key[P];
                     const int n = load_vec<E>(ra, i0, a.K, v, key);
-#pragma unroll
-                    for (int j = 0; j < P; ++j)
-                        if (j < n && (pass == 0 || (key[j] >> (shift + 8)) == prefix))
-                            atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
-                }
-                __syncthreads();
-                int bin, need_in;
-                hist_pick(hist, need, s_wsum, s_pick, bin, need_in);
-                count_eq = static_cast<int>(hist[bin]);  // read before the next pass clears it
-                prefix = (prefix << 8) | static_cast<uint32_t>(bin);
-                need = need_in;
-                __syncthreads();
-            }
-            const uint32_t T = prefix;
-            const int need_eq = need;
-            const bool take_all_eq = count_eq == need_eq;
-
-            // Collect the keys above T (and those equal to T when all of them are
-            // taken); the list order does not matter, it is sorted below.
-            if (tid == 0) s_nsel = 0;
-            __syncthreads();
-            for (int64_t i0 = static_cast<int64_t>(tid) * P; i0 < a.K; i0 += kStride) {
-                float v[P];
-                uint32_t key[P];
-                const int n = load_vec<E>(ra, i0, a.K, v, key);
-#pragma unroll
-                for (int j = 0; j < P; ++j) {
-                    if (j < n && (key[j] > T || (take_all_eq && key[j] == T))) {
-                        const int slot = atomicAdd(&s_nsel, 1);
-                        sel_idx[slot] = static_cast<int32_t>(i0 + j);
-                        sel_val[slot] = v[j];
-                    }
-                }
-            }
-            __syncthreads();
-            if (!take_all_eq) {
-                // Ties straddle the threshold: take the equal keys in index order,
-                // one block sweep at a time (thread order is element order within
-                // a sweep), until need_eq are taken.
-                const int lane = tid & (kWave - 1), wave = tid / kWave;
-                int remaining = need_eq;
-                for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
-                    const int64_t i0 = base + static_cast<int64_t>(tid) * P;
-                    float v[P];
-                    uint32_t key[P];
-                    int n = 0, cnt = 0;
-                    if (i0 < a.K) {
-                        n = load_vec<E>(ra, i0, a.K, v, key);
-#pragma unroll
-                        for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
-                    }
-                    int incl = cnt;  // inclusive prefix over the wave's lanes
-                    for (int o = 1; o < kWave; o <<= 1) {
-                        const int t = __shfl_up(incl, o);
-                        if (lane >= o) incl += t;
-                    }
-                    if (lane == kWave - 1) s_wsum[wave] = incl;
-                    __syncthreads();
-                    int rank = incl - cnt;
-                    for (int wv = 0; wv < wave; ++wv) rank += s_wsum[wv];
-                    if (i0 < a.K) {
-#pragma unroll
-                        for (int j = 0; j < P; ++j) {
-                            if (j < n && key[j] == T) {
-                                if (rank < remaining) {
-                                    const int slot = atomicAdd(&s_nsel, 1);
-                                    sel_idx[slot] = static_cast<int32_t>(i0 + j);
-                                    sel_val[slot] = v[j];
-                                }
-                                ++rank;
-                            }
+    #pragma unroll
+                    for (int j = 0; j < P; ++j) {
+                        if (j < n && (key[j] > T || (take_all_eq && key[j] == T))) {
+                            const int slot = atomicAdd(&s_nsel, 1);
+                            sel_idx[slot] = static_cast<int32_t>(i0 + j);
+                            sel_val[slot] = v[j];
                         }
                     }
-                    __syncthreads();
-                    remaining = k - s_nsel;
-                    __syncthreads();  // every thread has read s_nsel before s_wsum is rewritten
+                }
+                __syncthreads();
+                if (!take_all_eq) {
+                    // Ties straddle the threshold: take the equal keys in index order,
+                    // one block sweep at a time (thread order is element order within
+                    // a sweep), until need_eq are taken.
+                    const int lane = tid & (kWave - 1), wave = tid / kWave;
+                    int remaining = need_eq;
+                    for (int64_t base = 0; base < a.K && remaining > 0; base += kStride) {
+                        const int64_t i0 = base + static_cast<int64_t>(tid) * P;
+                        float v[P];
+                        uint32_t key[P];
+                        int n = 0, cnt = 0;
+                        if (i0 < a.K) {
+                            n = load_vec<E>(ra, i0, a.K, v, key);
+    #pragma unroll
+                            for (int j = 0; j < P; ++j) cnt += (j < n && key[j] == T) ? 1 : 0;
+                        }
+                        int incl = cnt;  // inclusive prefix over the wave's lanes
+                        for (int o = 1; o < kWave; o <<= 1) {
+                            const int t = __shfl_up(incl, o);
+                            if (lane >= o) incl += t;
+                        }
+                        if (lane == kWave - 1) s_wsum[wave] = incl;
+                        __syncthreads();
+                        int rank = incl - cnt;
+                        for (int wv = 0; wv < wave; ++wv) rank += s_wsum[wv];
+                        if (i0 < a.K) {
+    #pragma unroll
+                            for (int j = 0; j < P; ++j) {
+                                if (j < n && key[j] == T) {
+                                    if (rank < remaining) {
+                                        const int slot = atomicAdd(&s_nsel, 1);
+                                        sel_idx[slot] = static_cast<int32_t>(i0 + j);
+                                        sel_val[slot] = v[j];
+                                    }
+                                    ++rank;
+                                }
+                            }
+                        }
+                        __syncthreads();
+                        remaining = k - s_nsel;
+                        __syncthreads();  // every thread has read s_nsel before s_wsum is rewritten
+                    }
                 }
             }
-        }
 
-        // Rank sort by token index (indices are distinct), then the averaged
-        // model's log-probabilities of the selected tokens.
-        // Pad to a multiple of 4 with an index above every token.
-        if (tid < 4 && k + tid < ((k + 3) & ~3)) sel_idx[k + tid] = INT32_MAX;
-        __syncthreads();
-        for (int t = tid; t < k; t += kBlock) {
-            const int32_t my = sel_idx[t];
-            int r = 0;
-            for (int j = 0; j < k; j += 4) {
-                const u32x4 o = *reinterpret_cast<const u32x4 *>(&sel_idx[j]);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) r += static_cast<int32_t>(o[q]) < my ? 1 : 0;
-            }
-            out.idx[r] = my;
-            out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
-        }
-        __syncthreads();
-        if (a.topk_out)
-            for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = out.idx[t];
-
-        // JS terms, kJsGroup workers at a time: worker j of the group takes
-        // threads [j, j + 1) * kWorkerLanes (half a wave), thread l of them
-        // the selected tokens l, l + kWorkerLanes, ... in index order; the
-        // half-wave sum is d's.
-        constexpr double kLog2 = 0.69314718055994530942;
-        const int j = tid / kWorkerLanes, l = tid % kWorkerLanes;
-        for (int64_t w0 = 0; w0 < a.M; w0 += kJsGroup) {
-            const int nw = a.M - w0 < kJsGroup ? static_cast<int>(a.M - w0) : kJsGroup;
-            if (tid < nw) s_lse[tid] = row_lse(w.part + (a.U + (w0 + tid) * a.U + u) * kRowWaves, tab);
+            // Rank sort by token index (indices are distinct), then the averaged
+            // model's log-probabilities of the selected tokens.
+            // Pad to a multiple of 4 with an index above every token.
+            if (tid < 4 && k + tid < ((k + 3) & ~3)) sel_idx[k + tid] = INT32_MAX;
             __syncthreads();
-            double acc = 0.0;
-            const int64_t row = (w0 + (j < nw ? j : 0)) * a.U + u;
-            if (j < nw) {
-                const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
-                const double lse_w = s_lse[j];
-                constexpr int kGather = 4;  // gathers a thread has in flight
-                for (int t0 = l; t0 < k; t0 += kGather * kWorkerLanes) {
-                    float z[kGather];
-#pragma unroll
-                    for (int q = 0; q < kGather; ++q) {
-                        const int t = t0 + q * kWorkerLanes;
-                        z[q] = t < k ? E::at_ptr(zrow, out.idx[t]) : 0.0f;
-                    }
-#pragma unroll
-                    for (int q = 0; q < kGather; ++q) {
-                        const int t = t0 + q * kWorkerLanes;
-                        if (t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, out.la[t]);
+            for (int t = tid; t < k; t += kBlock) {
+                const int32_t my = sel_idx[t];
+                int r = 0;
+                for (int j = 0; j < k; j += 4) {
+                    const u32x4 o = *reinterpret_cast<const u32x4 *>(&sel_idx[j]);
+    #pragma unroll
+                    for (int q = 0; q < 4; ++q) r += static_cast<int32_t>(o[q]) < my ? 1 : 0;
+                }
+                out.idx[r] = my;
+                out.la[r] = static_cast<double>(sel_val[t]) - lse_a;
+            }
+            __syncthreads();
+            if (a.topk_out)
+                for (int t = tid; t < k; t += kBlock) a.topk_out[u * k + t] = out.idx[t];
+
+            // JS terms, kJsGroup workers at a time: worker j of the group takes
+            // threads [j, j + 1) * kWorkerLanes (half a wave), thread l of them
+            // the selected tokens l, l + kWorkerLanes, ... in index order; the
+            // half-wave sum is d's.
+            constexpr double kLog2 = 0.69314718055994530942;
+            const int j = tid / kWorkerLanes, l = tid % kWorkerLanes;
+            for (int64_t w0 = 0; w0 < a.M; w0 += kJsGroup) {
+                const int nw = a.M - w0 < kJsGroup ? static_cast<int>(a.M - w0) : kJsGroup;
+                if (tid < nw) s_lse[tid] = row_lse(w.part + (a.U + (w0 + tid) * a.U + u) * kRowWaves, tab);
+                __syncthreads();
+                double acc = 0.0;
+                const int64_t row = (w0 + (j < nw ? j : 0)) * a.U + u;
+                if (j < nw) {
+                    const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
+                    const double lse_w = s_lse[j];
+                    constexpr int kGather = 4;  // gathers a thread has in flight
+                    for (int t0 = l; t0 < k; t0 += kGather * kWorkerLanes) {
+                        float z[kGather];
+    #pragma unroll
+                        for (int q = 0; q < kGather; ++q) {
+                            const int t = t0 + q * kWorkerLanes;
+                            z[q] = t < k ? E::at_ptr(zrow, out.idx[t]) : 0.0f;
+                        }
+    #pragma unroll
+                        for (int q = 0; q < kGather; ++q) {
+                            const int t = t0 + q * kWorkerLanes;
+                            if (t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, out.la[t]);
+                        }
                     }
                 }
+                for (int o = kWorkerLanes / 2; o > 0; o >>= 1) acc += shfl_xor_d(acc, o);
+                if (l == 0 && j < nw) a.d_out[row] = sqrt((acc > 0.0 ? acc : 0.0) / kLog2);
+                __syncthreads();  // s_lse is rewritten by the next group
             }
-            for (int o = kWorkerLanes / 2; o > 0; o >>= 1) acc += shfl_xor_d(acc, o);
-            if (l == 0 && j < nw) a.d_out[row] = sqrt((acc > 0.0 ? acc : 0.0) / kLog2);
-            __syncthreads();  // s_lse is rewritten by the next group
+            // The next token reuses the shared arrays, and the next group of
+            // tokens s_tok: the last barrier above follows every read of them.
         }
-        // The next token reuses the shared arrays: the last barrier above
-        // follows every read of them.
     }
 }
 
@@ -976,8 +993,8 @@ __device__ inline void wave_sync() {
 // base (wave-uniform) grows by their number.  Every lane of the wave calls it.
 __device__ inline int wave_append(bool pred, int &base) {
     const uint64_t m = __ballot(pred);
-    const int slot = base + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                                static_cast<uint32_t>(m >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)));
+    const uint32_t below = __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u);  // set lanes before this one
+    const int slot = base + static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32), below));
     base += __popcll(m);
     return slot;
 }
