@@ -97,8 +97,11 @@ struct JsF32 {
 #pragma unroll
         for (int j = 0; j < 4; ++j) v[j] = __uint_as_float(t[j]);
     }
-    // Element i of the row that starts at `row` (a gather).
-    __device__ static float at_ptr(const char *row, int64_t i) { return reinterpret_cast<const float *>(row)[i]; }
+    // Element i of the row that starts at `row` (a gather; nontemporal: the
+    // line is not kept).
+    __device__ static float at_ptr(const char *row, int64_t i) {
+        return __builtin_nontemporal_load(reinterpret_cast<const float *>(row) + i);
+    }
     // The key of a value, and the value of a key that some value has.
     __device__ static uint32_t key_of(float v) {
         uint32_t b = __float_as_uint(v);
@@ -129,9 +132,11 @@ struct JsBF16 {
             v[2 * j + 1] = __uint_as_float(t[j] & 0xFFFF0000u);
         }
     }
-    // Element i of the row that starts at `row` (a gather).
+    // Element i of the row that starts at `row` (a gather; nontemporal: the
+    // line is not kept).
     __device__ static float at_ptr(const char *row, int64_t i) {
-        return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t *>(row)[i]) << 16);
+        const uint16_t h = __builtin_nontemporal_load(reinterpret_cast<const uint16_t *>(row) + i);
+        return __uint_as_float(static_cast<uint32_t>(h) << 16);
     }
     // The key of a value (a bf16 widened to float), and the value of a key
     // that some value has.
