@@ -984,7 +984,7 @@ constexpr int kCandPerLane = kWaveCand / kWave;
 constexpr int kWaveMaxK = kRowThreads;                 // the selection ranks one maximum per row thread
 constexpr int kJsLanes = kWave / kJsGroup;             // lanes per worker in the JS terms
 constexpr int kReadRound = 4;                          // recorded vectors a lane reads at once
-constexpr int kGather = 16;                            // worker logits a lane gathers at once
+constexpr int kWaveGather = 16;                        // worker logits a lane gathers at once
 
 // Orders a wave's LDS accesses: what a lane wrote before it is visible to
 // every lane of the wave after it.
@@ -1002,12 +1002,6 @@ __device__ inline int wave_append(bool pred, int &base) {
     const int slot = base + static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32), below));
     base += __popcll(m);
     return slot;
-}
-
-__device__ inline uint64_t readlane64(uint64_t x, int l) {
-    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), l));
-    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x >> 32), l));
-    return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 // One wave's LDS in js_token_wave_kernel.
@@ -1259,10 +1253,10 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
         const int64_t row = (w0 + (mine_w ? jw : 0)) * a.U + u;
         const char *zrow = static_cast<const char *>(a.workers) + row * a.ldk * E::kElem;
         double acc = 0.0;
-        for (int t0 = 0; t0 < k; t0 += kGather * kJsLanes) {
-            float z[kGather];
+        for (int t0 = 0; t0 < k; t0 += kWaveGather * kJsLanes) {
+            float z[kWaveGather];
 #pragma unroll
-            for (int q = 0; q < kGather; ++q) {
+            for (int q = 0; q < kWaveGather; ++q) {
                 const int t = t0 + l + q * kJsLanes;
                 z[q] = mine_w && t < k ? E::at_ptr(zrow, L.u.out.idx[t]) : 0.0f;
             }
@@ -1272,7 +1266,7 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
             }
             const double lse_w = L.lse[mine_w ? jw : 0];
 #pragma unroll
-            for (int q = 0; q < kGather; ++q) {
+            for (int q = 0; q < kWaveGather; ++q) {
                 const int t = t0 + l + q * kJsLanes;
                 if (mine_w && t < k) acc += js_term(static_cast<double>(z[q]) - lse_w, L.u.out.la[t]);
             }
