@@ -362,6 +362,23 @@ def test_js_row_padding_is_never_used(env, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("sweeps,extra", [(1, -1), (1, 0), (1, 1), (2, 0), (2, 5), (3, 1), (3, -7)])
+def test_js_sweep_boundaries(env, dtype, sweeps, extra):
+    """Vocabularies around whole sweeps of a row (256 row threads x one
+    16-byte vector each): a row of one sweep, one element more or less, two
+    and three sweeps, a ragged last vector; the last sweep is the only one
+    some lanes lack or hold in part."""
+    fgd, torch = env
+    per = 8 if dtype == "bf16" else 4
+    K = sweeps * 256 * per + extra
+    k = min(100, K)
+    ldk = -(-K // per) * per
+    print(f"[js] sweeps {sweeps} extra {extra} {dtype} K {K}", flush=True)
+    A, W = slog.numpy_logits(3, 5, K, ldk, dtype, seed=K)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_js_hundreds_of_candidates(env, dtype):
     """Averaged rows with a wide tie at the k-th value: 60 tokens above it
     and t tokens on it (t = 90 .. 450, scattered), the rest below.  The
