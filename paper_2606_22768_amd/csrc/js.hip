@@ -546,7 +546,9 @@ __device__ inline double row_lse(const LsePart *p, const double *tab) {
     return lse_of_parts(q, tab);
 }
 
-// Packed 16-bit lanes: two bf16 logits of a 32-bit word at once.
+// Packed 16-bit lanes: two bf16 logits of a 32-bit word at once.  The word
+// is copied with memcpy: with this toolchain, __builtin_bit_cast of an
+// element t[j] of a u32x4 compiled to a read of t[0] for every j.
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ u16x2 as_u16x2(uint32_t x) {
     u16x2 r;
@@ -1100,9 +1102,9 @@ __device__ inline void select_sorted(const uint64_t *comp, int C, int k, int lan
 // elements with key >= T0 (on these inputs a little over k); the vectors
 // whose maxima reach T0 go to a queue and are read again in one round, and
 // their elements at or above T0 are appended to the candidates in lane
-// order; the candidates are sorted under (key descending, index
-// ascending) by a bitonic network across the wave, the first k then by
-// index; then the JS terms, kJsLanes lanes per worker, with a lane's gathers issued
+// order; the candidates are sorted under (key descending, index ascending)
+// by a bitonic network across the wave, the first k then by index; then
+// the JS terms, kJsLanes lanes per worker, with a lane's gathers issued
 // together.  A token with more than kWaveCand candidates (a row of many
 // equal logits) is flagged and left to js_token_radix_kernel.
 // k <= kWaveMaxK.
@@ -1223,8 +1225,12 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
             }
         }
     }
+    // More candidates than the wave holds go to the radix kernel; fewer than
+    // k cannot occur (each of the k entries at or above T0 names a distinct
+    // vector holding an element at or above it) and would leave selected
+    // slots without a token, so that too is handed on rather than gathered.
     const int C = __builtin_amdgcn_readfirstlane(nsel);
-    if (C > kWaveCand) {  // the same in every lane
+    if (C > kWaveCand || C < k) {  // the same in every lane
         if (lane == 0) w.flag[u] = 1;
         return;
     }
