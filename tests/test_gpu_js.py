@@ -417,6 +417,19 @@ def test_js_candidate_overflow_mixed_with_ordinary_tokens(env, dtype):
     _check(fgd, torch, A, W, dtype, K, k)
 
 
+@pytest.mark.parametrize("k", [50, 300])
+def test_js_many_tokens_with_flagged_ones(env, k):
+    """3000 tokens: more than the radix kernel's blocks, so each block walks
+    several tokens' flags (k = 50, every 37th token's averaged row one
+    repeated logit and so flagged) or several tokens (k = 300: every token
+    goes to the radix kernel)."""
+    fgd, torch = env
+    M, U, K, ldk = 2, 3000, 700, 704
+    A, W = slog.numpy_logits(M, U, K, ldk, "bf16", seed=k)
+    A[::37, :K] = A[::37, :1]
+    _check(fgd, torch, A, W, "bf16", K, k)
+
+
 def test_js_workspace_reused_across_shapes(env):
     """One workspace serves calls of different sizes in turn (bf16, then
     float32 over fewer tokens, then bf16 again): each call writes what it
