@@ -117,7 +117,7 @@ def js_bench(args, fgd, torch):
     HBM; a step is one fgd_js_distance call (distances and their means)."""
     from synth import logits as slog
 
-    w = JS_WORKLOAD
+    w = dict(JS_WORKLOAD, dtype=args.js_dtype)
     M, U, K, k = w["M"], w["U"], w["K"], w["k"]
     es = 2 if w["dtype"] == "bf16" else 4
     print(f"[bench] generating JS logits M={M} U={U} K={K}", file=sys.stderr, flush=True)
@@ -168,10 +168,11 @@ def js_bench(args, fgd, torch):
            "config": {"workload": wl, "workers": M, "tokens": U, "vocab": K,
                       "top_k": k, "dtype": w["dtype"], "bytes_per_step": nbytes},
            # Bound: HBM.  Every logit is read once by the row kernel (all
-           # M + 1 rows per token); the per-token kernel reads the averaged
-           # rows once more only where a batch may hold a top-k candidate,
-           # and gathers the workers' logits of the selected tokens.  Most
-           # bf16 logits cost a table read instead of a float64 exp.
+           # M + 1 rows per token); the per-token kernel reads again only
+           # the averaged rows' recorded vectors whose maxima reach its
+           # threshold, and gathers the workers' logits of the selected
+           # tokens.  Most bf16 logits cost a table read instead of a
+           # float64 exp.
            "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(achieved / HBM_PEAK_GBS, 4),
                         "traffic": None if tr is None else tr["total_bytes"], "traffic_detail": tr,
@@ -409,6 +410,8 @@ def main():
                          "about 12 s of single-threaded oracle work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
+    ap.add_argument("--js-dtype", choices=["bf16", "f32"], default="bf16",
+                    help="storage of the logits in --mode js (the benchmark workload is bf16)")
     ap.add_argument("--mode", choices=["fused", "split", "js", "consensus"], default="fused",
                     help="fused: one-pass outer step (the benchmark); split: Mix1 half on a side stream "
                          "overlapping a stand-in inner loop, then the blocking half; js: Jensen-Shannon "
