@@ -117,7 +117,7 @@ def js_bench(args, fgd, torch):
     HBM; a step is one fgd_js_distance call (distances and their means)."""
     from synth import logits as slog
 
-    w = dict(JS_WORKLOAD, dtype=args.js_dtype)
+    w = dict(JS_WORKLOAD, dtype=args.js_dtype, k=args.js_topk)
     M, U, K, k = w["M"], w["U"], w["K"], w["k"]
     es = 2 if w["dtype"] == "bf16" else 4
     print(f"[bench] generating JS logits M={M} U={U} K={K}", file=sys.stderr, flush=True)
@@ -412,6 +412,9 @@ def main():
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the plain-copy reference, GB")
     ap.add_argument("--js-dtype", choices=["bf16", "f32"], default="bf16",
                     help="storage of the logits in --mode js (the benchmark workload is bf16)")
+    ap.add_argument("--js-topk", type=int, default=100,
+                    help="top-k tokens of --mode js (the paper's and the benchmark's 100; above 256 every "
+                         "token takes the radix kernel)")
     ap.add_argument("--mode", choices=["fused", "split", "js", "consensus"], default="fused",
                     help="fused: one-pass outer step (the benchmark); split: Mix1 half on a side stream "
                          "overlapping a stand-in inner loop, then the blocking half; js: Jensen-Shannon "
