@@ -19,13 +19,13 @@
 //                          barriers): per row, each wave's (shift, sum) part
 //                          of the log-sum-exp; per averaged row, each row
 //                          thread's four largest vector maxima (key, index)
-//   js_token_wave_kernel   (k <= 256) one wave per token: the averaged row's
+//   js_token_wave_kernel   (k <= 512) one wave per token: the averaged row's
 //                          lse from its parts, the selection (a threshold from
 //                          the recorded maxima, a second read of only the
 //                          vectors that reach it), the JS terms; a token with
 //                          too many candidates is flagged
 //   js_token_radix_kernel  per token, a radix select over the whole row: every
-//                          token when k > 256, else only the flagged ones
+//                          token when k > 512, else only the flagged ones
 //   js_mean_kernel         the per-worker mean of d
 //
 // Rows.  bf16 logits take only 65536 bit patterns, and the exp of every bf16
@@ -981,9 +981,9 @@ __global__ __launch_bounds__(kRowsBlock) void js_rows_pattern_kernel(JsParams a,
 constexpr int kWaveTokens = kBlock / kWave;            // tokens per block of js_token_wave_kernel
 constexpr int kRtPerLane = kRowThreads / kWave;        // row threads whose recorded maxima a lane takes
 constexpr int kRecords = kRowThreads * kTopVecs;       // recorded vector maxima per token
-constexpr int kWaveCand = 512;                         // candidates a token may have
-constexpr int kCandPerLane = kWaveCand / kWave;
-constexpr int kWaveMaxK = kRowThreads;                 // the selection ranks one maximum per row thread
+constexpr int kWaveCandSmall = 512;                    // candidates a token may have, k <= 256
+constexpr int kWaveCandLarge = 1024;                   // the same, 256 < k <= 512
+constexpr int kWaveMaxK = kWaveCandLarge / 2;          // k the wave kernel takes (at most half its candidates)
 constexpr int kJsLanes = kWave / kJsGroup;             // lanes per worker in the JS terms
 constexpr int kReadRound = 4;                          // recorded vectors a lane reads at once
 constexpr int kWaveGather = 16;                        // worker logits a lane gathers at once
@@ -1006,14 +1006,16 @@ __device__ inline int wave_append(bool pred, int &base) {
     return slot;
 }
 
-// One wave's LDS in js_token_wave_kernel.
+// One wave's LDS in js_token_wave_kernel with up to kCand candidates and
+// k <= kCand / 2.
+template <int kCand>
 struct __align__(16) WaveLds {
-    uint64_t comp[kWaveCand];  // candidates: key << 32 | ~index, larger = earlier in (key desc, index asc)
+    uint64_t comp[kCand];  // candidates: key << 32 | ~index, larger = earlier in (key desc, index asc)
     union {
         uint32_t queue[kRecords];  // first elements of the recorded vectors to read again
         struct {
-            int32_t idx[kWaveMaxK];
-            double la[kWaveMaxK];
+            int32_t idx[kCand / 2];
+            double la[kCand / 2];
         } out;  // the selected tokens in index order, log pbar
     } u;
     double lse[kJsGroup];
@@ -1105,16 +1107,17 @@ __device__ inline void select_sorted(const uint64_t *comp, int C, int k, int lan
 // order; the candidates are sorted under (key descending, index ascending)
 // by a bitonic network across the wave, the first k then by index; then
 // the JS terms, kJsLanes lanes per worker, with a lane's gathers issued
-// together.  A token with more than kWaveCand candidates (a row of many
-// equal logits) is flagged and left to js_token_radix_kernel.
-// k <= kWaveMaxK.
-template <class E>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4, 8)))
+// together.  A token with more than kCand candidates (a row of many equal
+// logits) is flagged and left to js_token_radix_kernel.  k <= kCand / 2:
+// kCand 512 keeps a block's LDS at 35 KB, 1024 (for 256 < k <= 512) takes
+// 58 KB.
+template <class E, int kCand>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kCand == kWaveCandSmall ? 4 : 2, 8)))
 void js_token_wave_kernel(JsParams a, JsWork w) {
     constexpr int P = E::kPer;
     constexpr int64_t kStride = static_cast<int64_t>(kRowThreads) * P;  // elements per row sweep
     __shared__ double tab[kTab];
-    __shared__ WaveLds lds[kWaveTokens];
+    __shared__ WaveLds<kCand> lds[kWaveTokens];
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t u = static_cast<int64_t>(blockIdx.x) * kWaveTokens + wave;
@@ -1133,7 +1136,7 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     }
     load_exp_table(tab);
     if (!live) return;
-    WaveLds &L = lds[wave];
+    WaveLds<kCand> &L = lds[wave];
     const int k = a.k;
     const rsrc_t ra = js_row(a.avg, u, a.ldk, E::kElem);
     const double lse_a = lse_of_parts(pa, tab);
@@ -1167,7 +1170,7 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
             const uint32_t key = E::key_of(v[j]);
             const bool c = have && i0 + j < a.K && key >= kthr;
             const int slot = wave_append(c, nsel);
-            if (c && slot < kWaveCand)
+            if (c && slot < kCand)
                 L.comp[slot] = (static_cast<uint64_t>(key) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(i0 + j));
         }
     };
@@ -1230,7 +1233,7 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     // vector holding an element at or above it) and would leave selected
     // slots without a token, so that too is handed on rather than gathered.
     const int C = __builtin_amdgcn_readfirstlane(nsel);
-    if (C > kWaveCand || C < k) {  // the same in every lane
+    if (C > kCand || C < k) {  // the same in every lane
         if (lane == 0) w.flag[u] = 1;
         return;
     }
@@ -1241,8 +1244,10 @@ void js_token_wave_kernel(JsParams a, JsWork w) {
     // log-probabilities.
     if (C <= 2 * kWave)
         select_sorted<E, 2>(L.comp, C, k, lane, lse_a, L.u.out.idx, L.u.out.la);
+    else if (C <= 8 * kWave || kCand <= 8 * kWave)  // 8 per lane holds every candidate of the small kernel
+        select_sorted<E, 8>(L.comp, C, k, lane, lse_a, L.u.out.idx, L.u.out.la);
     else
-        select_sorted<E, kCandPerLane>(L.comp, C, k, lane, lse_a, L.u.out.idx, L.u.out.la);
+        select_sorted<E, kCand / kWave>(L.comp, C, k, lane, lse_a, L.u.out.idx, L.u.out.la);
     wave_sync();
     if (a.topk_out)
         for (int t = lane; t < k; t += kWave) a.topk_out[u * k + t] = L.u.out.idx[t];
@@ -1330,12 +1335,18 @@ bool js_launch(const void *avg, const void *workers, int32_t bf16, int32_t M, in
     const dim3 tokens(static_cast<unsigned>(wave_path ? std::min<int64_t>(U, 4 * std::max(num_cus, 1)) : U));
     if (bf16) {
         hipLaunchKernelGGL(js_rows_kernel<JsBF16>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
-        if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsBF16>, token_waves, dim3(kBlock), 0, stream, p, w);
+        if (wave_path && k <= kWaveCandSmall / 2)
+            hipLaunchKernelGGL((js_token_wave_kernel<JsBF16, kWaveCandSmall>), token_waves, dim3(kBlock), 0, stream, p, w);
+        else if (wave_path)
+            hipLaunchKernelGGL((js_token_wave_kernel<JsBF16, kWaveCandLarge>), token_waves, dim3(kBlock), 0, stream, p, w);
         hipLaunchKernelGGL(js_token_radix_kernel<JsBF16>, tokens, dim3(kBlock), 0, stream, p, w,
                            wave_path ? static_cast<const int32_t *>(w.flag) : nullptr);
     } else {
         hipLaunchKernelGGL(js_rows_kernel<JsF32>, dim3(static_cast<unsigned>(grid)), dim3(kRowsBlock), 0, stream, p, w);
-        if (wave_path) hipLaunchKernelGGL(js_token_wave_kernel<JsF32>, token_waves, dim3(kBlock), 0, stream, p, w);
+        if (wave_path && k <= kWaveCandSmall / 2)
+            hipLaunchKernelGGL((js_token_wave_kernel<JsF32, kWaveCandSmall>), token_waves, dim3(kBlock), 0, stream, p, w);
+        else if (wave_path)
+            hipLaunchKernelGGL((js_token_wave_kernel<JsF32, kWaveCandLarge>), token_waves, dim3(kBlock), 0, stream, p, w);
         hipLaunchKernelGGL(js_token_radix_kernel<JsF32>, tokens, dim3(kBlock), 0, stream, p, w,
                            wave_path ? static_cast<const int32_t *>(w.flag) : nullptr);
     }

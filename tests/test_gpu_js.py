@@ -100,6 +100,10 @@ CASES = [
     (1, 4, 32000, 32000, "bf16", 100),       # bf16: many exact ties among the logits
     (2, 3, 7, 8, "f32", 7),                  # full vocabulary (k = K)
     (2, 3, 500, 504, "bf16", 500),
+    (2, 4, 2000, 2000, "f32", 257),          # k past the smaller per-token wave kernel
+    (3, 5, 9000, 9008, "bf16", 400),
+    (2, 4, 6000, 6000, "f32", 512),          # the wave kernel's largest k
+    (2, 3, 4000, 4000, "bf16", 513),         # every token to the radix kernel
     (4, 2, 20000, 20000, "f32", 1024),       # largest k
     (5, 3, 3000, 3000, "bf16", 1),
 ]
@@ -384,7 +388,8 @@ def test_js_hundreds_of_candidates(env, dtype):
     and t tokens on it (t = 90 .. 450, scattered), the rest below.  The
     threshold from the recorded vector maxima is the tied value, so the
     per-token selection sorts 60 + t candidates (past two per lane for most
-    tokens, up to its limit of 512) and must split the tie by index."""
+    tokens, up to 512, the limit of the kernel that takes k = 100) and must
+    split the tie by index."""
     fgd, torch = env
     M, U, K, k = 2, 6, 40_000, 100
     A, W = slog.numpy_logits(M, U, K, K, "f32", seed=83)
@@ -394,6 +399,29 @@ def test_js_hundreds_of_candidates(env, dtype):
         pos = rng.choice(K, size=60 + t, replace=False)
         A[u, pos[:60]] = 5.0 + rng.integers(0, 4, size=60).astype(np.float32)
         A[u, pos[60:]] = 3.0
+    if dtype == "bf16":
+        import torch as _t
+
+        A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+        W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_js_hundreds_of_candidates_large_k(env, dtype):
+    """k = 400 (the per-token wave kernel for 256 < k <= 512): 300 tokens
+    above a tied value and t on it (t = 120 .. 760), so 420 .. 1060
+    candidates: sorted at eight or sixteen per lane, and the last token,
+    past the kernel's 1024, handed to the radix kernel."""
+    fgd, torch = env
+    M, U, K, k = 2, 6, 40_000, 400
+    A, W = slog.numpy_logits(M, U, K, K, "f32", seed=85)
+    rng = np.random.default_rng(86)
+    A = np.clip(A, -6.0, 1.5).astype(np.float32)
+    for u, t in enumerate((120, 200, 450, 600, 720, 760)):
+        pos = rng.choice(K, size=300 + t, replace=False)
+        A[u, pos[:300]] = 5.0 + rng.integers(0, 4, size=300).astype(np.float32)
+        A[u, pos[300:]] = 3.0
     if dtype == "bf16":
         import torch as _t
 
@@ -417,12 +445,12 @@ def test_js_candidate_overflow_mixed_with_ordinary_tokens(env, dtype):
     _check(fgd, torch, A, W, dtype, K, k)
 
 
-@pytest.mark.parametrize("k", [50, 300])
+@pytest.mark.parametrize("k", [50, 300, 600])
 def test_js_many_tokens_with_flagged_ones(env, k):
     """3000 tokens: more than the radix kernel's blocks, so each block walks
-    several tokens' flags (k = 50, every 37th token's averaged row one
-    repeated logit and so flagged) or several tokens (k = 300: every token
-    goes to the radix kernel)."""
+    several tokens' flags (k = 50 and 300, the two per-token wave kernels;
+    every 37th token's averaged row is one repeated logit and so flagged)
+    or several tokens (k = 600: every token goes to the radix kernel)."""
     fgd, torch = env
     M, U, K, ldk = 2, 3000, 700, 704
     A, W = slog.numpy_logits(M, U, K, ldk, "bf16", seed=k)
