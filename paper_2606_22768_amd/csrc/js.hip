@@ -512,6 +512,15 @@ struct TopVecs {
     __device__ static uint32_t med3(uint32_t a, uint32_t b, uint32_t c) { return max(min(a, b), min(max(a, b), c)); }
 };
 
+// The row streamed at position q of the row kernels' order: token-major,
+// token u's averaged row (row u of the workspace parts) then its M worker
+// rows (row U + m U + u), so every round of the persistent grid holds the
+// same share of averaged rows, whose terms cost more.
+__device__ inline int64_t js_stream_row(int64_t q, int32_t M, int64_t U) {
+    const int64_t u = q / (M + 1), j = q - u * (M + 1);
+    return j == 0 ? u : U + (j - 1) * U + u;
+}
+
 // Vectors per row thread, at most (a row of K logits, P per vector).
 inline int64_t js_thread_vectors(int64_t K, int per) {
     return ((K + per - 1) / per + kRowThreads - 1) / kRowThreads;
@@ -654,8 +663,8 @@ __device__ inline void row_terms(rsrc_t r, rsrc_t rn, bool has_next, int64_t i_f
 
 // Every row's wave parts of its log-sum-exp, and the averaged rows'
 // largest vector maxima per thread, into the workspace.  Persistent: thread group g
-// (kRowThreads threads; two per block) streams rows g, g + G, ... (G
-// groups) of the streaming order below; thread lt of a group takes the
+// (kRowThreads threads; two per block) streams the rows at positions g,
+// g + G, ... (G groups) of js_stream_row's order; thread lt of a group takes the
 // elements lt * P + s * kStride of its row.  No barriers after the tables
 // are loaded: each wave streams on its own, its next row's first load
 // issued before its row ends.
@@ -672,23 +681,24 @@ void js_rows_kernel(JsParams a, JsWork w) {
     const int64_t G = static_cast<int64_t>(gridDim.x) * kRowsPerBlock;
     const int64_t R = static_cast<int64_t>(a.M + 1) * a.U;
     const int nsw = static_cast<int>((a.K + kStride - 1) / kStride);  // sweeps per row
-    // Streaming order: the averaged rows (token u at r = u), then the worker
-    // rows (row m U + u at r = U + m U + u), the order of the workspace parts.
+    // Row r of the workspace parts: the averaged rows (token u at r = u),
+    // then the worker rows (row m U + u at r = U + m U + u).
     auto row_of = [&](int64_t r) -> rsrc_t {
         return r < a.U ? js_row(a.avg, r, a.ldk, E::kElem) : js_row(a.workers, r - a.U, a.ldk, E::kElem);
     };
     // The group index is uniform in a wave: in a scalar register, the row's
     // buffer descriptor stays scalar (no per-load waterfall).
     const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kRowThreads));
-    int64_t r = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + g;
+    int64_t q = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + g;  // streaming position
     u32x4 nxt = {0, 0, 0, 0};
-    if (r < R && i_first < a.K)
-        nxt = __builtin_amdgcn_raw_buffer_load_b128(row_of(r), static_cast<uint32_t>(i_first * E::kElem), 0,
-                                                    kLoadPolicy);
-    for (; r < R; r += G) {
-        const bool has_next = r + G < R;
+    if (q < R && i_first < a.K)
+        nxt = __builtin_amdgcn_raw_buffer_load_b128(row_of(js_stream_row(q, a.M, a.U)),
+                                                    static_cast<uint32_t>(i_first * E::kElem), 0, kLoadPolicy);
+    for (; q < R; q += G) {
+        const int64_t r = js_stream_row(q, a.M, a.U);
+        const bool has_next = q + G < R;
         const rsrc_t rr = row_of(r);
-        const rsrc_t rn = has_next ? row_of(r + G) : rr;
+        const rsrc_t rn = has_next ? row_of(js_stream_row(q + G, a.M, a.U)) : rr;
         RowLse st;
         TopVecs<E> top;
         const bool avg = r < a.U;
@@ -952,15 +962,16 @@ __global__ __launch_bounds__(kRowsBlock) void js_rows_pattern_kernel(JsParams a,
         return r < a.U ? js_row(a.avg, r, a.ldk, E::kElem) : js_row(a.workers, r - a.U, a.ldk, E::kElem);
     };
     const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kRowThreads));
-    int64_t r = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + g;
+    int64_t q = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + g;  // streaming position
     u32x4 nxt = {0, 0, 0, 0};
-    if (r < R && i_first < a.K)
-        nxt = __builtin_amdgcn_raw_buffer_load_b128(row_of(r), static_cast<uint32_t>(i_first * E::kElem), 0,
-                                                    kLoadPolicy);
-    for (; r < R; r += G) {
-        const bool has_next = r + G < R;
+    if (q < R && i_first < a.K)
+        nxt = __builtin_amdgcn_raw_buffer_load_b128(row_of(js_stream_row(q, a.M, a.U)),
+                                                    static_cast<uint32_t>(i_first * E::kElem), 0, kLoadPolicy);
+    for (; q < R; q += G) {
+        const int64_t r = js_stream_row(q, a.M, a.U);
+        const bool has_next = q + G < R;
         const rsrc_t rr = row_of(r);
-        const rsrc_t rn = has_next ? row_of(r + G) : rr;
+        const rsrc_t rn = has_next ? row_of(js_stream_row(q + G, a.M, a.U)) : rr;
         uint32_t acc = 0;
         for (int64_t i0 = i_first; i0 < a.K; i0 += kStride) {
             const u32x4 cur = nxt;
