@@ -413,7 +413,7 @@ def main():
     ap.add_argument("--js-dtype", choices=["bf16", "f32"], default="bf16",
                     help="storage of the logits in --mode js (the benchmark workload is bf16)")
     ap.add_argument("--js-topk", type=int, default=100,
-                    help="top-k tokens of --mode js (the paper's and the benchmark's 100; above 256 every "
+                    help="top-k tokens of --mode js (the paper's and the benchmark's 100; above 512 every "
                          "token takes the radix kernel)")
     ap.add_argument("--mode", choices=["fused", "split", "js", "consensus"], default="fused",
                     help="fused: one-pass outer step (the benchmark); split: Mix1 half on a side stream "
