@@ -431,6 +431,33 @@ def test_js_hundreds_of_candidates_large_k(env, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("k,top,tied", [(256, 200, 312), (256, 200, 313), (400, 300, 724), (400, 300, 725)])
+def test_js_candidate_capacity_boundaries(env, dtype, k, top, tied):
+    """Exactly as many candidates as a per-token wave kernel holds, and one
+    more: `top` tokens above a tied value and `tied` tokens on it, the rest
+    below, so the threshold from the recorded vector maxima is the tied
+    value and the candidates number top + tied: 512 and 513 for k = 256 (the
+    kernel for k <= 256 holds 512), 1024 and 1025 for k = 400 (the one for
+    256 < k <= 512 holds 1024); one past the capacity goes to the radix
+    kernel.  The tie at the k-th value is split by index."""
+    fgd, torch = env
+    M, U, K = 2, 2, 40_000
+    A, W = slog.numpy_logits(M, U, K, K, "f32", seed=91)
+    rng = np.random.default_rng(92)
+    A = np.clip(A, -6.0, 1.5).astype(np.float32)
+    for u in range(U):
+        pos = rng.choice(K, size=top + tied, replace=False)
+        A[u, pos[:top]] = 5.0 + rng.integers(0, 4, size=top).astype(np.float32)
+        A[u, pos[top:]] = 3.0
+    if dtype == "bf16":
+        import torch as _t
+
+        A = _t.from_numpy(A).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+        W = _t.from_numpy(W).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    _check(fgd, torch, A, W, dtype, K, k)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_js_candidate_overflow_mixed_with_ordinary_tokens(env, dtype):
     """Tokens whose averaged row is one repeated logit give every element as
     a candidate of the per-token wave selection (more than it holds); those
