@@ -514,7 +514,7 @@ struct TopVecs {
 
 // The row streamed at position q of the row kernels' order: token-major,
 // token u's averaged row (row u of the workspace parts) then its M worker
-// rows (row U + m U + u), so every round of the persistent grid holds the
+// rows (row U + m U + u), so every pass of the persistent grid holds the
 // same share of averaged rows, whose terms cost more.
 __device__ inline int64_t js_stream_row(int64_t q, int32_t M, int64_t U) {
     const int64_t u = q / (M + 1), j = q - u * (M + 1);
